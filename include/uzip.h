@@ -1,0 +1,160 @@
+/*
+ * uzip.h -- C ABI of the MI355X (gfx950) block-wise lossless float codec.
+ *
+ * The operation is the lossless compression that UCCL-Zip places inside
+ * GPU communication (arXiv 2604.17172):
+ *   - section 2.1.2: every value is split into its exponent byte (the
+ *     "compressed part") and its sign+fraction bits (the "uncompressed
+ *     part"); the exponent bytes are ANS-coded block by block and the
+ *     variable-length block outputs are concatenated into one stream;
+ *   - section 3.3.1: each block codes with its own frequency table built
+ *     from its own data (localized tables), in one fused launch with no
+ *     third coalescing pass;
+ *   - section 3.2.3: split-send -- the uncompressed part is final right
+ *     after the split and may be sent before coding finishes;
+ *   - section 3.4: the per-hop step of a compressed all-reduce:
+ *     decompress, reduce, recompress;
+ *   - section 4.1: the metadata carries dtype and the sizes before and
+ *     after compression.
+ *
+ * Stream layout (little-endian; pad16(x) rounds x up to a multiple of 16,
+ * padding bytes are zero):
+ *     0  u32 magic 0x31505A55   4 u8 version = 1   5 u8 dtype
+ *     6  u8 prob_bits = 11      7 u8 flags = 0
+ *     8  u32 block_elems       12 u32 n_blocks
+ *    16  u64 n_elems           24 u64 total_bytes
+ *    32  u32 dir[n_blocks]: bit 31 = STORED, bits 30..0 = end offset of
+ *        the block's section within the coded plane, in 16-byte units
+ *    raw plane at 32 + pad16(4 n_blocks): (E-1) bytes per element, the low
+ *        bytes of the value rotated left by one bit (sign in bit 0)
+ *    coded plane at raw_off + pad16((E-1) n): one section per block
+ *  A CODED section is u32 state[64] | u8 present[32] | u16 f[k] |
+ *  u16 word[W] | pad; the 11-bit table f (sum 2048) comes from the
+ *  block's histogram and the words are those of 64 interleaved rANS
+ *  states (state interval [2^15, 2^31), 16-bit renormalisation, lane j
+ *  codes elements 512 r + 8 j .. +7 of round r).  A block whose coded
+ *  section would not be smaller than its n_b symbol bytes is STORED.
+ *
+ * Conventions for every call:
+ *   - All buffers are caller-owned device memory (flags and chunk_sizes may
+ *     also be host-mapped memory).  The library never allocates or frees.
+ *   - Every call only checks its arguments on the host and enqueues work on
+ *     the given stream; it returns before the GPU has run.  Results (and
+ *     *d_status) are valid once the stream reaches that point.
+ *   - Device pointers must be 16-byte aligned.
+ *   - block_bytes is a power of two in [4096, 262144].
+ *   - Calls that overlap in time need separate workspaces.
+ *   - Host-side errors are returned immediately and nothing is enqueued.
+ *     Device-side errors (corrupt streams) are written to *d_status (the
+ *     first error wins; the caller zeroes it before the call).  No call
+ *     writes outside [d_out, d_out + out_cap) or its workspace.
+ */
+#ifndef UZIP_H
+#define UZIP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { UZIP_BF16 = 0, UZIP_FP16 = 1, UZIP_FP32 = 2 } uzip_dtype;
+
+typedef enum {
+  UZIP_OK = 0,
+  UZIP_EINVAL = -1,      /* bad argument (dtype, sizes, alignment, block size) */
+  UZIP_ENOSPC = -2,      /* output capacity or workspace too small */
+  UZIP_ECORRUPT = -3,    /* device status: stream corrupt or not matching the call */
+  UZIP_EHIP = -4,        /* a HIP runtime call failed */
+  UZIP_EUNSUPPORTED = -5 /* the device is not gfx950 */
+} uzip_status;
+
+/* operation codes for uzip_workspace_size */
+enum { UZIP_OP_COMPRESS = 0, UZIP_OP_DECOMPRESS = 1, UZIP_OP_REDUCE = 2, UZIP_OP_CHUNKED = 3 };
+
+/* Largest possible stream for n_elems values (every block STORED), in
+ * bytes.  Section 4.1's "size after compression" never exceeds it.
+ * Returns 0 for invalid arguments. */
+size_t uzip_max_compressed_size(uzip_dtype dtype, uint64_t n_elems, uint32_t block_bytes);
+
+/* Device workspace bytes that `op` needs (section 4.1 bounds the
+ * compressor's footprint; this is ours).  For UZIP_OP_CHUNKED pass the
+ * chunk size in `aux`; for UZIP_OP_REDUCE pass n_in in `aux` and add the
+ * flag UZIP_WS_NO_OUT_RAW (1 << 16) when d_out_raw will be NULL.  Returns
+ * 0 for invalid arguments (a zero-byte workspace is never valid for
+ * COMPRESS, CHUNKED or REDUCE). */
+#define UZIP_WS_NO_OUT_RAW (1u << 16)
+size_t uzip_workspace_size(int op, uzip_dtype dtype, uint64_t n_elems, uint32_t block_bytes,
+                           uint64_t aux);
+
+/* Compress n_elems values at d_in (section 2.1.2 Steps 1-3 with the
+ * localized tables of section 3.3.1, fused in one launch).
+ *   d_out, out_cap: stream buffer, out_cap >= uzip_max_compressed_size.
+ *   d_out_size:     device u64 receiving total_bytes (may be NULL).
+ *   d_ws, ws_bytes: workspace of uzip_workspace_size(UZIP_OP_COMPRESS, ...).
+ * Errors: EINVAL, ENOSPC, EHIP, EUNSUPPORTED. */
+uzip_status uzip_compress(const void *d_in, uint64_t n_elems, uzip_dtype dtype,
+                          uint32_t block_bytes, void *d_out, size_t out_cap,
+                          uint64_t *d_out_size, void *d_ws, size_t ws_bytes,
+                          hipStream_t stream);
+
+/* Decompress a stream (the receiver side of sections 3.2 and 3.4).
+ *   d_in, in_bytes: the stream (in_bytes >= its total_bytes).
+ *   dtype, n_elems: what the caller expects; the header must agree.
+ *   d_out, out_cap: n_elems values, out_cap >= n_elems * element size.
+ *   d_status:       device u32, set to UZIP_ECORRUPT if the stream is
+ *                   corrupt or does not match (may be NULL).
+ *   d_ws, ws_bytes: not used by this version (pass NULL, 0).
+ * Errors: EINVAL, ENOSPC, EHIP, EUNSUPPORTED. */
+uzip_status uzip_decompress(const void *d_in, size_t in_bytes, uzip_dtype dtype,
+                            uint64_t n_elems, void *d_out, size_t out_cap,
+                            uint32_t *d_status, void *d_ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/* Fused decompress -> reduce -> recompress of one rank's share (section
+ * 3.4, the CopyReducePacks step with compression fused in).
+ *   d_in[i], in_bytes[i] (host arrays of n_in entries, 1 <= n_in <= 16):
+ *     streams of the same dtype, n_elems and block size.
+ *   d_local_raw: uncompressed local addend, added last (may be NULL; the
+ *     selective compression of section 3.4 leaves local data raw).
+ *   The sum is taken element by element in IEEE binary32 in input order,
+ *   acc = x_0, acc = acc + x_i, rounded to nearest even into dtype (NaN
+ *   becomes the canonical quiet NaN), and compressed with block_bytes.
+ *   d_out, out_cap, d_out_size: as for uzip_compress.
+ *   d_out_raw: receives the reduced tensor (may be NULL).
+ *   d_status: as for uzip_decompress.
+ * Errors: EINVAL, ENOSPC, EHIP, EUNSUPPORTED. */
+uzip_status uzip_reduce_fused(const void *const *d_in, const size_t *in_bytes, int n_in,
+                              const void *d_local_raw, uzip_dtype dtype, uint64_t n_elems,
+                              uint32_t block_bytes, void *d_out, size_t out_cap,
+                              uint64_t *d_out_size, void *d_out_raw, uint32_t *d_status,
+                              void *d_ws, size_t ws_bytes, hipStream_t stream);
+
+/* Split-send producer (section 3.2.3): the tensor is cut into chunks of
+ * chunk_bytes (a multiple of block_bytes); chunk c is compressed as an
+ * independent stream at d_out + c * slot_bytes, byte-identical to
+ * uzip_compress of that slice.
+ *   slot_bytes >= uzip_max_compressed_size(one full chunk).
+ *   flags[2c]   is set to `epoch` once chunk c's raw plane is final
+ *               (its offset is computable from dtype and the chunk size),
+ *   chunk_sizes[c] receives the chunk's total_bytes, then
+ *   flags[2c+1] is set to `epoch` once the whole chunk stream is final.
+ *   Both are stored with system-scope release ordering, so host-mapped
+ *   flags may be polled by a host thread.  Use a new epoch per call.
+ * Errors: EINVAL, ENOSPC, EHIP, EUNSUPPORTED. */
+uzip_status uzip_compress_chunked(const void *d_in, uint64_t n_elems, uzip_dtype dtype,
+                                  uint32_t block_bytes, uint64_t chunk_bytes, void *d_out,
+                                  size_t slot_bytes, uint64_t *chunk_sizes, uint32_t *flags,
+                                  uint32_t epoch, void *d_ws, size_t ws_bytes,
+                                  hipStream_t stream);
+
+/* Static string naming a status code. */
+const char *uzip_status_str(uzip_status status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

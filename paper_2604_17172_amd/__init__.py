@@ -1,0 +1,212 @@
+"""Python binding of libuzip (gfx950 block-wise lossless float codec).
+
+The C functions keep their names (``uzip_compress``, ``uzip_decompress``,
+``uzip_reduce_fused``, ``uzip_compress_chunked``, ...); this module only
+marshals arguments.  torch provides device memory and the current stream;
+every step of the codec runs in the HIP kernels of ``csrc/uzip.hip``.
+There is no CPU fallback: importing this module fails if the library has
+not been built.
+
+Convenience wrappers (``compress``, ``decompress``, ``reduce_fused``,
+``compress_chunked``) allocate outputs and workspaces with torch and call
+the C ABI on ``torch.cuda.current_stream()``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+from .build import LIB_PATH
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is missing: build it with `python paper_2604_17172_amd/build.py` "
+        "(or __graft_entry__.build()); there is no fallback implementation")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+BF16, FP16, FP32 = 0, 1, 2
+OP_COMPRESS, OP_DECOMPRESS, OP_REDUCE, OP_CHUNKED = 0, 1, 2, 3
+WS_NO_OUT_RAW = 1 << 16
+OK, EINVAL, ENOSPC, ECORRUPT, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+
+_c = ctypes
+_vp, _u32, _u64, _sz, _int = _c.c_void_p, _c.c_uint32, _c.c_uint64, _c.c_size_t, _c.c_int
+
+_lib.uzip_max_compressed_size.argtypes = [_int, _u64, _u32]
+_lib.uzip_max_compressed_size.restype = _sz
+_lib.uzip_workspace_size.argtypes = [_int, _int, _u64, _u32, _u64]
+_lib.uzip_workspace_size.restype = _sz
+_lib.uzip_compress.argtypes = [_vp, _u64, _int, _u32, _vp, _sz, _vp, _vp, _sz, _vp]
+_lib.uzip_compress.restype = _int
+_lib.uzip_decompress.argtypes = [_vp, _sz, _int, _u64, _vp, _sz, _vp, _vp, _sz, _vp]
+_lib.uzip_decompress.restype = _int
+_lib.uzip_reduce_fused.argtypes = [_c.POINTER(_vp), _c.POINTER(_sz), _int, _vp, _int, _u64, _u32, _vp, _sz,
+                                   _vp, _vp, _vp, _vp, _sz, _vp]
+_lib.uzip_reduce_fused.restype = _int
+_lib.uzip_compress_chunked.argtypes = [_vp, _u64, _int, _u32, _u64, _vp, _sz, _vp, _vp, _u32, _vp, _sz, _vp]
+_lib.uzip_compress_chunked.restype = _int
+_lib.uzip_status_str.argtypes = [_int]
+_lib.uzip_status_str.restype = _c.c_char_p
+
+EXPORTED = ["uzip_max_compressed_size", "uzip_workspace_size", "uzip_compress", "uzip_decompress",
+            "uzip_reduce_fused", "uzip_compress_chunked", "uzip_status_str"]
+
+
+class UzipError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {uzip_status_str(status)} ({status})")
+        self.status = status
+
+
+# ---------------------------------------------------------------- raw C ABI
+def uzip_max_compressed_size(dtype: int, n_elems: int, block_bytes: int) -> int:
+    return _lib.uzip_max_compressed_size(dtype, n_elems, block_bytes)
+
+
+def uzip_workspace_size(op: int, dtype: int, n_elems: int, block_bytes: int, aux: int = 0) -> int:
+    return _lib.uzip_workspace_size(op, dtype, n_elems, block_bytes, aux)
+
+
+def uzip_compress(d_in, n_elems, dtype, block_bytes, d_out, out_cap, d_out_size, d_ws, ws_bytes, stream) -> int:
+    return _lib.uzip_compress(d_in, n_elems, dtype, block_bytes, d_out, out_cap, d_out_size, d_ws, ws_bytes, stream)
+
+
+def uzip_decompress(d_in, in_bytes, dtype, n_elems, d_out, out_cap, d_status, d_ws, ws_bytes, stream) -> int:
+    return _lib.uzip_decompress(d_in, in_bytes, dtype, n_elems, d_out, out_cap, d_status, d_ws, ws_bytes, stream)
+
+
+def uzip_reduce_fused(d_in, in_bytes, n_in, d_local_raw, dtype, n_elems, block_bytes, d_out, out_cap,
+                      d_out_size, d_out_raw, d_status, d_ws, ws_bytes, stream) -> int:
+    ptrs = (_vp * n_in)(*d_in)
+    sizes = (_sz * n_in)(*in_bytes)
+    return _lib.uzip_reduce_fused(ptrs, sizes, n_in, d_local_raw, dtype, n_elems, block_bytes, d_out, out_cap,
+                                  d_out_size, d_out_raw, d_status, d_ws, ws_bytes, stream)
+
+
+def uzip_compress_chunked(d_in, n_elems, dtype, block_bytes, chunk_bytes, d_out, slot_bytes, chunk_sizes,
+                          flags, epoch, d_ws, ws_bytes, stream) -> int:
+    return _lib.uzip_compress_chunked(d_in, n_elems, dtype, block_bytes, chunk_bytes, d_out, slot_bytes,
+                                      chunk_sizes, flags, epoch, d_ws, ws_bytes, stream)
+
+
+def uzip_status_str(status: int) -> str:
+    return _lib.uzip_status_str(status).decode()
+
+
+# ---------------------------------------------------------------- torch helpers
+_TORCH_DTYPE = {torch.bfloat16: BF16, torch.float16: FP16, torch.float32: FP32}
+_NAME_DTYPE = {"bf16": BF16, "fp16": FP16, "fp32": FP32}
+_ELEM = {BF16: 2, FP16: 2, FP32: 4}
+_BITS = {BF16: torch.int16, FP16: torch.int16, FP32: torch.int32}
+
+
+def dtype_code(dt) -> int:
+    if isinstance(dt, int):
+        return dt
+    if isinstance(dt, str):
+        return _NAME_DTYPE[dt]
+    return _TORCH_DTYPE[dt]
+
+
+def _stream(stream) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _check(rc: int, what: str) -> None:
+    if rc != OK:
+        raise UzipError(rc, what)
+
+
+def _dev_empty(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 16), dtype=torch.uint8, device=device)
+
+
+def compress(x: torch.Tensor, block_bytes: int = 65536, dtype=None, out: torch.Tensor | None = None,
+             ws: torch.Tensor | None = None, stream=None):
+    """Compress a contiguous CUDA tensor (bf16/fp16/fp32, or an int16/int32
+    bit view with ``dtype`` given).  Returns (stream buffer, device u64 size)."""
+    assert x.is_cuda and x.is_contiguous()
+    dt = dtype_code(dtype if dtype is not None else x.dtype)
+    n = x.numel()
+    cap = uzip_max_compressed_size(dt, n, block_bytes)
+    if cap == 0:
+        _check(EINVAL, "uzip_compress")
+    if out is None:
+        out = _dev_empty(cap, x.device)
+    wsb = uzip_workspace_size(OP_COMPRESS, dt, n, block_bytes)
+    if ws is None:
+        ws = _dev_empty(wsb, x.device)
+    size = torch.zeros(1, dtype=torch.int64, device=x.device)
+    _check(uzip_compress(x.data_ptr() if n else None, n, dt, block_bytes, out.data_ptr(), out.numel(),
+                         size.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream)), "uzip_compress")
+    return out, size
+
+
+def decompress(s: torch.Tensor, dtype, n_elems: int, out: torch.Tensor | None = None,
+               in_bytes: int | None = None, stream=None):
+    """Decompress a stream.  Returns (bit-pattern tensor, device u32 status)."""
+    dt = dtype_code(dtype)
+    if out is None:
+        out = torch.empty(max(n_elems, 1), dtype=_BITS[dt], device=s.device)[:n_elems]
+    status = torch.zeros(1, dtype=torch.int32, device=s.device)
+    nbytes = s.numel() * s.element_size() if in_bytes is None else in_bytes
+    _check(uzip_decompress(s.data_ptr(), nbytes, dt, n_elems, out.data_ptr() if n_elems else None,
+                           n_elems * _ELEM[dt], status.data_ptr(), None, 0, _stream(stream)), "uzip_decompress")
+    return out, status
+
+
+def reduce_fused(streams, dtype, n_elems: int, block_bytes: int = 65536, local: torch.Tensor | None = None,
+                 want_raw: bool = True, in_bytes=None, out: torch.Tensor | None = None,
+                 ws: torch.Tensor | None = None, stream=None):
+    """Fused decompress -> fp32 reduce -> recompress.  Returns
+    (stream buffer, device u64 size, reduced tensor or None, device status)."""
+    dt = dtype_code(dtype)
+    dev = streams[0].device
+    cap = uzip_max_compressed_size(dt, n_elems, block_bytes)
+    if out is None:
+        out = _dev_empty(cap, dev)
+    raw = torch.empty(max(n_elems, 1), dtype=_BITS[dt], device=dev)[:n_elems] if want_raw else None
+    aux = len(streams) | (0 if want_raw else WS_NO_OUT_RAW)
+    wsb = uzip_workspace_size(OP_REDUCE, dt, n_elems, block_bytes, aux)
+    if ws is None:
+        ws = _dev_empty(wsb, dev)
+    size = torch.zeros(1, dtype=torch.int64, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    sizes = in_bytes if in_bytes is not None else [t.numel() * t.element_size() for t in streams]
+    _check(uzip_reduce_fused([t.data_ptr() for t in streams], sizes, len(streams),
+                             local.data_ptr() if local is not None else None, dt, n_elems, block_bytes,
+                             out.data_ptr(), out.numel(), size.data_ptr(),
+                             raw.data_ptr() if raw is not None and n_elems else None, status.data_ptr(),
+                             ws.data_ptr(), ws.numel(), _stream(stream)), "uzip_reduce_fused")
+    return out, size, raw, status
+
+
+def compress_chunked(x: torch.Tensor, block_bytes: int, chunk_bytes: int, dtype=None, epoch: int = 1,
+                     flags: torch.Tensor | None = None, out: torch.Tensor | None = None,
+                     ws: torch.Tensor | None = None, stream=None):
+    """Split-send producer.  Returns (buffer of n_chunks slots, slot_bytes,
+    device u64 chunk sizes, flags [2 n_chunks] u32)."""
+    assert x.is_cuda and x.is_contiguous()
+    dt = dtype_code(dtype if dtype is not None else x.dtype)
+    n = x.numel()
+    e = _ELEM[dt]
+    ce = chunk_bytes // e
+    chunks = (n + ce - 1) // ce
+    slot = uzip_max_compressed_size(dt, min(n, ce), block_bytes)
+    slot = (slot + 255) // 256 * 256
+    if out is None:
+        out = _dev_empty(slot * max(chunks, 1), x.device)
+    wsb = uzip_workspace_size(OP_CHUNKED, dt, n, block_bytes, chunk_bytes)
+    if ws is None:
+        ws = _dev_empty(wsb, x.device)
+    sizes = torch.zeros(max(chunks, 1), dtype=torch.int64, device=x.device)
+    if flags is None:
+        flags = torch.zeros(2 * max(chunks, 1), dtype=torch.int32, device=x.device)
+    _check(uzip_compress_chunked(x.data_ptr() if n else None, n, dt, block_bytes, chunk_bytes, out.data_ptr(),
+                                 slot, sizes.data_ptr(), flags.data_ptr(), epoch, ws.data_ptr(), ws.numel(),
+                                 _stream(stream)), "uzip_compress_chunked")
+    return out, slot, sizes, flags

@@ -1,0 +1,189 @@
+// uzip_device.h -- device building blocks of the gfx950 codec kernels.
+//
+// Wave64 primitives, the element transform of the split step (section
+// 2.1.2, Step 1), stream geometry and the per-block table helpers shared by
+// the compress, decompress and fused-reduce kernels.
+#pragma once
+
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace uzip {
+
+// ---- format constants (stream version 1) ----
+constexpr uint32_t kProbBits = 11;          // table resolution: frequencies sum to 2^11
+constexpr uint32_t kM = 1u << kProbBits;
+constexpr uint32_t kStateLo = 1u << 15;     // coder state interval [2^15, 2^31)
+constexpr uint32_t kLanes = 64;             // interleaved states per block (one wave64)
+constexpr uint32_t kPerLane = 8;            // consecutive elements per lane and round
+constexpr uint32_t kRound = kLanes * kPerLane;
+constexpr uint32_t kHeaderBytes = 32;
+constexpr uint32_t kSectionFixed = 288;     // 64 states + 32-byte presence bitmap
+constexpr uint32_t kMagic = 0x31505A55u;
+constexpr uint32_t kVersion = 1;
+constexpr uint32_t kStoredBit = 0x80000000u;
+
+// status words of the single-pass scan over block sizes (decoupled look-back)
+constexpr uint64_t kFlagAggregate = 1ull << 62;
+constexpr uint64_t kFlagInclusive = 2ull << 62;
+constexpr uint64_t kValueMask = (1ull << 62) - 1;
+
+// LDS layout constants
+constexpr uint32_t kHistReplicas = 8;       // sub-histograms, lane & 7
+constexpr uint32_t kHistStride = 257;       // odd stride: replicas of a bin in distinct banks
+constexpr uint32_t kHistBytes = kHistReplicas * kHistStride * 4;
+constexpr uint32_t kEncTableBytes = 256 * 16;
+constexpr uint32_t kLutBytes = kM * 4;
+constexpr uint32_t kStageHead = 800;        // room for state/bitmap/f[256] before the words
+constexpr uint32_t kStageTail = 32;         // zero bytes after the words
+
+__host__ __device__ constexpr uint64_t pad16(uint64_t x) { return (x + 15u) & ~uint64_t(15); }
+
+// Geometry of one stream (a whole tensor or one chunk of it).
+struct Geom {
+  uint64_t n;          // elements in the stream
+  uint32_t n_blocks;
+  uint64_t raw_off;    // byte offset of the raw plane
+  uint64_t coded_off;  // byte offset of the coded plane
+};
+
+__host__ __device__ inline Geom make_geom(uint64_t n, uint32_t block_elems, uint32_t E) {
+  Geom g;
+  g.n = n;
+  g.n_blocks = (uint32_t)((n + block_elems - 1) / block_elems);
+  g.raw_off = kHeaderBytes + pad16(4ull * g.n_blocks);
+  g.coded_off = g.raw_off + pad16((uint64_t)(E - 1) * n);
+  return g;
+}
+
+// ---- wave64 primitives ----
+__device__ inline uint32_t lane_id() { return __lane_id(); }
+
+__device__ inline uint32_t mbcnt(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+__device__ inline uint32_t wave_sum(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ inline uint64_t wave_sum64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ inline uint32_t wave_max(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    uint32_t w = __shfl_xor(v, o);
+    v = w > v ? w : v;
+  }
+  return v;
+}
+
+// exclusive prefix sum over lanes
+__device__ inline uint32_t wave_excl_scan(uint32_t v) {
+  uint32_t lane = lane_id();
+  uint32_t inc = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    uint32_t w = __shfl_up(inc, o);
+    if (lane >= (uint32_t)o) inc += w;
+  }
+  return inc - v;
+}
+
+__device__ inline uint32_t uniform(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// ---- element transform (section 2.1.2, Step 1) ----
+// A value is rotated left by one bit so that the sign lands in bit 0; the
+// top byte is then the coded symbol (the exponent byte) and the remaining
+// low bytes are the raw sign+fraction part.
+__device__ inline uint32_t rotl16x2(uint32_t v) {
+  return ((v << 1) & 0xFFFEFFFEu) | ((v >> 15) & 0x00010001u);
+}
+__device__ inline uint32_t rotr16x2(uint32_t v) {
+  return ((v >> 1) & 0x7FFF7FFFu) | ((v << 15) & 0x80008000u);
+}
+__device__ inline uint32_t rotl32(uint32_t v) { return (v << 1) | (v >> 31); }
+__device__ inline uint32_t rotr32(uint32_t v) { return (v >> 1) | (v << 31); }
+
+// Eight consecutive elements of one lane, split into symbols and raw bytes.
+// sym: 8 bytes; raw: 8 bytes (16-bit types) or 24 bytes (fp32).
+struct Group {
+  uint32_t sym[2];
+  uint32_t raw[6];
+};
+
+// 16-bit elements packed two per word (element 2q in the low half).
+__device__ inline void split16(const uint32_t w[4], Group &g) {
+  uint32_t r0 = rotl16x2(w[0]), r1 = rotl16x2(w[1]), r2 = rotl16x2(w[2]), r3 = rotl16x2(w[3]);
+  g.sym[0] = __builtin_amdgcn_perm(r1, r0, 0x07050301u);
+  g.sym[1] = __builtin_amdgcn_perm(r3, r2, 0x07050301u);
+  g.raw[0] = __builtin_amdgcn_perm(r1, r0, 0x06040200u);
+  g.raw[1] = __builtin_amdgcn_perm(r3, r2, 0x06040200u);
+}
+
+__device__ inline void merge16(const uint32_t sym[2], const uint32_t raw[2], uint32_t w[4]) {
+  w[0] = rotr16x2(__builtin_amdgcn_perm(sym[0], raw[0], 0x05010400u));
+  w[1] = rotr16x2(__builtin_amdgcn_perm(sym[0], raw[0], 0x07030602u));
+  w[2] = rotr16x2(__builtin_amdgcn_perm(sym[1], raw[1], 0x05010400u));
+  w[3] = rotr16x2(__builtin_amdgcn_perm(sym[1], raw[1], 0x07030602u));
+}
+
+__device__ inline void split32(const uint32_t w[8], Group &g) {
+  uint32_t r[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) r[q] = rotl32(w[q]);
+  g.sym[0] = (r[0] >> 24) | ((r[1] >> 24) << 8) | ((r[2] >> 24) << 16) | (r[3] & 0xFF000000u);
+  g.sym[1] = (r[4] >> 24) | ((r[5] >> 24) << 8) | ((r[6] >> 24) << 16) | (r[7] & 0xFF000000u);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    uint32_t a = r[4 * h] & 0xFFFFFFu, b = r[4 * h + 1] & 0xFFFFFFu;
+    uint32_t c = r[4 * h + 2] & 0xFFFFFFu, d = r[4 * h + 3] & 0xFFFFFFu;
+    g.raw[3 * h + 0] = a | (b << 24);
+    g.raw[3 * h + 1] = (b >> 8) | (c << 16);
+    g.raw[3 * h + 2] = (c >> 16) | (d << 8);
+  }
+}
+
+__device__ inline void merge32(const uint32_t sym[2], const uint32_t raw[6], uint32_t w[8]) {
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    uint32_t r0 = raw[3 * h], r1 = raw[3 * h + 1], r2 = raw[3 * h + 2];
+    uint32_t a = r0 & 0xFFFFFFu;
+    uint32_t b = (r0 >> 24) | ((r1 & 0xFFFFu) << 8);
+    uint32_t c = (r1 >> 16) | ((r2 & 0xFFu) << 16);
+    uint32_t d = r2 >> 8;
+    uint32_t s = sym[h];
+    w[4 * h + 0] = rotr32(a | (s << 24));
+    w[4 * h + 1] = rotr32(b | ((s >> 8) << 24));
+    w[4 * h + 2] = rotr32(c | ((s >> 16) << 24));
+    w[4 * h + 3] = rotr32(d | ((s >> 24) << 24));
+  }
+}
+
+__device__ inline uint32_t sym_at(const uint32_t sym[2], uint32_t t) {
+  return (sym[t >> 2] >> (8 * (t & 3))) & 0xFFu;
+}
+
+// ---- scalar conversions for the fused reduce ----
+__device__ inline float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+__device__ inline uint32_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if (f != f) return 0x7FC0u;
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+__device__ inline float fp16_to_f32(uint32_t h) {
+  return __half2float(__ushort_as_half((unsigned short)h));
+}
+__device__ inline uint32_t f32_to_fp16(float f) {
+  if (f != f) return 0x7E00u;
+  return (uint32_t)__half_as_ushort(__float2half_rn(f));
+}
+
+}  // namespace uzip

@@ -1,0 +1,80 @@
+"""The C-ABI library loads, exports what include/uzip.h declares, and its
+host-side logic (sizes, argument checks) is right.  No GPU is touched: every
+call here returns before the library makes any HIP call."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import ref
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "uzip.h")).read()
+    return sorted(set(re.findall(r"\b(uzip_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    import paper_2604_17172_amd as uz
+    names = _declared()
+    assert set(names) == set(uz.EXPORTED)
+    for name in names:
+        assert hasattr(uz._lib, name), name
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16", "fp32"])
+@pytest.mark.parametrize("bb", [4096, 65536, 262144])
+def test_max_size_matches_oracle(dtype, bb):
+    import paper_2604_17172_amd as uz
+    for n in (0, 1, 511, 4097, 1 << 20, (1 << 20) + 7, 1 << 29):
+        assert uz.uzip_max_compressed_size(uz.dtype_code(dtype), n, bb) == ref.max_compressed_size(dtype, n, bb)
+
+
+def test_invalid_arguments_rejected_on_host():
+    import paper_2604_17172_amd as uz
+    assert uz.uzip_max_compressed_size(7, 100, 65536) == 0
+    assert uz.uzip_max_compressed_size(0, 100, 65535) == 0
+    assert uz.uzip_max_compressed_size(0, 100, 2048) == 0
+    assert uz.uzip_max_compressed_size(0, 100, 524288) == 0
+    assert uz.uzip_compress(None, 10, 7, 65536, None, 0, None, None, 0, None) == uz.EINVAL
+    assert uz.uzip_compress(None, 10, 0, 65535, None, 0, None, None, 0, None) == uz.EINVAL
+    # misaligned pointers
+    assert uz.uzip_compress(16, 10, 0, 65536, 24, 1 << 20, None, 32, 1 << 20, None) == uz.EINVAL
+    # output too small
+    assert uz.uzip_compress(16, 1000, 0, 65536, 32, 100, None, 48, 1 << 20, None) == uz.ENOSPC
+    assert uz.uzip_decompress(16, 100, 9, 10, 32, 100, None, None, 0, None) == uz.EINVAL
+    assert uz.uzip_decompress(16, 100, 0, 1000, 32, 100, None, None, 0, None) == uz.ENOSPC
+    assert uz.uzip_reduce_fused([16] * 17, [64] * 17, 17, None, 0, 10, 65536, 32, 1 << 20, None, None,
+                                None, 48, 1 << 20, None) == uz.EINVAL
+    assert uz.uzip_reduce_fused([], [], 0, None, 0, 10, 65536, 32, 1 << 20, None, None,
+                                None, 48, 1 << 20, None) == uz.EINVAL
+    # chunk size not a multiple of the block size
+    assert uz.uzip_compress_chunked(16, 1000, 0, 65536, 65536 + 4096, 32, 1 << 20, 48, 64, 1, 80,
+                                    1 << 20, None) == uz.EINVAL
+    assert uz.uzip_workspace_size(uz.OP_CHUNKED, 0, 1000, 65536, 3000) == 0
+    assert uz.uzip_workspace_size(uz.OP_REDUCE, 0, 1000, 65536, 0) == 0
+    assert uz.uzip_workspace_size(uz.OP_REDUCE, 0, 1000, 65536, 17) == 0
+
+
+def test_workspace_sizes_are_bounded():
+    """The workspace is a few bytes per block, plus the reduced tensor when
+    the caller does not take it (section 4.1 bounds the compressor's
+    footprint; ours is far below it)."""
+    import paper_2604_17172_amd as uz
+    n = 1 << 29
+    ws = uz.uzip_workspace_size(uz.OP_COMPRESS, 0, n, 65536)
+    assert 0 < ws <= 8 * (n // 32768) + 1024
+    wsc = uz.uzip_workspace_size(uz.OP_CHUNKED, 0, n, 65536, 4 << 20)
+    assert 0 < wsc <= 16 * (n // 32768) + 4096
+    wr = uz.uzip_workspace_size(uz.OP_REDUCE, 0, 1 << 23, 65536, 8 | uz.WS_NO_OUT_RAW)
+    assert wr >= 2 * (1 << 23)
+
+
+def test_status_strings():
+    import paper_2604_17172_amd as uz
+    assert uz.uzip_status_str(0) == "ok"
+    assert "corrupt" in uz.uzip_status_str(uz.ECORRUPT)
+    assert uz.uzip_status_str(123) == "unknown status"

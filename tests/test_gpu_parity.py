@@ -1,0 +1,286 @@
+"""GPU parity: the HIP library against the CPU oracle, byte for byte.
+
+Sizes here are ones the oracle finishes in seconds while spanning many
+codec blocks, several chunks and ragged tails.  Every call goes through the
+C ABI (via the ctypes binding).  Integer codec work must be bit-exact; the
+fused reduce is a fixed-order binary32 sum, so its output is bit-exact too.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import ref
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+EB = {"bf16": 2, "fp16": 2, "fp32": 4}
+NP_BITS = {"bf16": np.int16, "fp16": np.int16, "fp32": np.int32}
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def uz():
+    import paper_2604_17172_amd as m
+    return m
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def to_dev_bits(x, dtype):
+    return dev(x.view(NP_BITS[dtype]))
+
+
+def host_bits(t, dtype):
+    return t.cpu().numpy().view(np.uint16 if EB[dtype] == 2 else np.uint32)
+
+
+def gpu_compress(uz, x, dtype, bb):
+    xt = to_dev_bits(x, dtype)
+    out, size = uz.compress(xt, bb, dtype=dtype)
+    torch.cuda.synchronize()
+    n = int(size.item())
+    return out, out[:n].cpu().numpy()
+
+
+def special_words(dtype, n, seed):
+    rng = np.random.default_rng(seed)
+    bits = 8 * EB[dtype]
+    specials = {"bf16": [0x0000, 0x8000, 0x7F80, 0xFF80, 0x7FC0, 0x7F81, 0xFFFF, 0x0001, 0x807F],
+                "fp16": [0x0000, 0x8000, 0x7C00, 0xFC00, 0x7E00, 0x7C01, 0xFFFF, 0x0001, 0x83FF],
+                "fp32": [0, 0x80000000, 0x7F800000, 0xFF800000, 0x7FC00000, 0x7F800001, 0xFFFFFFFF, 1,
+                         0x807FFFFF]}[dtype]
+    if dtype == "bf16":
+        x = W.normal_bf16(n, seed=seed)
+    elif dtype == "fp16":
+        x = W.grad_fp16(n, seed=seed)
+    else:
+        x = W.grad_fp32(n, seed=seed)
+    if n:
+        pos = rng.integers(0, n, max(1, n // 20))
+        x[pos] = rng.choice(specials, pos.size)
+        noise = rng.integers(0, n, max(1, n // 100))
+        x[noise] = rng.integers(0, 1 << bits, noise.size, dtype=np.uint64).astype(x.dtype)
+    return x
+
+
+def check_roundtrip(uz, x, dtype, bb, label):
+    say(f"[parity] {label}: dtype={dtype} n={x.size} block={bb}")
+    want = ref.compress(x, dtype, bb)
+    out, got = gpu_compress(uz, x, dtype, bb)
+    assert got.size == want.size, f"{label}: size {got.size} != oracle {want.size}"
+    if not np.array_equal(got, want):
+        bad = np.nonzero(got != want)[0]
+        raise AssertionError(f"{label}: {bad.size} bytes differ, first at {bad[0]}")
+    y, status = uz.decompress(out, dtype, x.size)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0, label
+    assert np.array_equal(host_bits(y, dtype), x), f"{label}: decode not lossless"
+    # the GPU decoder on the oracle's stream
+    y2, status2 = uz.decompress(dev(want), dtype, x.size)
+    torch.cuda.synchronize()
+    assert int(status2.item()) == 0 and np.array_equal(host_bits(y2, dtype), x), label
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16", "fp32"])
+@pytest.mark.parametrize("n", [1, 511, 512, 513, 8191, 70_001])
+def test_edge_sizes(uz, dtype, n):
+    x = special_words(dtype, n, seed=n)
+    for bb in (4096, 65536):
+        check_roundtrip(uz, x, dtype, bb, f"edge n={n}")
+
+
+def test_normal_bf16_4MiB_blocks_64k(uz):
+    """The 4 MiB N(0, 0.02) bf16 configuration with 64 KiB blocks."""
+    x = W.normal_bf16()
+    check_roundtrip(uz, x, "bf16", 65536, "normal_bf16_4MiB")
+
+
+@pytest.mark.parametrize("dtype,bb", [("fp32", 262144), ("fp16", 262144), ("bf16", 262144), ("fp32", 4096)])
+def test_grad_and_large_blocks(uz, dtype, bb):
+    n = 3 * (bb // EB[dtype]) + 12345
+    x = {"fp32": W.grad_fp32, "fp16": W.grad_fp16, "bf16": W.normal_bf16}[dtype](n, seed=3)
+    check_roundtrip(uz, x, dtype, bb, f"grad {dtype}")
+
+
+def test_weight_sync_prefix(uz):
+    x = W.weight_sync(1 << 23)   # embedding + first layers: N(0,1), N(0,0.02), N(1,0.05) regions
+    check_roundtrip(uz, x, "bf16", 65536, "weight_sync prefix")
+    x = W.weight_sync(136_134_656 + 2_000_000)[-6_000_000:]   # across the embedding/layer boundary
+    check_roundtrip(uz, np.ascontiguousarray(x), "bf16", 65536, "weight_sync boundary")
+
+
+def test_kv_cache_small(uz):
+    x = W.kv_cache(layers=2, tokens=512)
+    check_roundtrip(uz, x, "bf16", 65536, "kv_cache small")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16", "fp32"])
+def test_all_stored_random_bits(uz, dtype):
+    x = W.random_bits(200_003, 8 * EB[dtype], seed=9)
+    check_roundtrip(uz, x, dtype, 65536, "random bits")
+
+
+def test_single_symbol_blocks(uz):
+    x = np.full(3 * 32768 + 5, 0x3F80, np.uint16)
+    x[40000:40010] = 0x4000
+    check_roundtrip(uz, x, "bf16", 65536, "constant blocks")
+
+
+def test_uniform_bf16(uz):
+    x = W.uniform_bf16(1 << 21, seed=11)
+    check_roundtrip(uz, x, "bf16", 65536, "uniform bf16")
+
+
+def test_empty_tensor(uz):
+    say("[parity] empty")
+    x = np.zeros(0, np.uint16)
+    out, size = uz.compress(torch.zeros(0, dtype=torch.int16, device="cuda"), 65536, dtype="bf16")
+    torch.cuda.synchronize()
+    assert int(size.item()) == 32
+    assert np.array_equal(out[:32].cpu().numpy(), ref.compress(x, "bf16", 65536))
+    y, status = uz.decompress(out, "bf16", 0)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0 and y.numel() == 0
+
+
+# ---------------------------------------------------------- split-send producer
+@pytest.mark.parametrize("dtype,bb,cb,n", [("bf16", 65536, 1 << 20, 3 * (1 << 19) + 77_777),
+                                           ("fp32", 262144, 1 << 20, 2 * (1 << 18) + 1),
+                                           ("fp16", 4096, 16384, 100_000)])
+def test_chunked_producer_matches_per_chunk_oracle(uz, dtype, bb, cb, n):
+    say(f"[parity] chunked dtype={dtype} n={n} block={bb} chunk={cb}")
+    x = special_words(dtype, n, seed=31)
+    xt = to_dev_bits(x, dtype)
+    out, slot, sizes, flags = uz.compress_chunked(xt, bb, cb, dtype=dtype, epoch=7)
+    torch.cuda.synchronize()
+    want = ref.compress_chunked(x, dtype, bb, cb)
+    sz = sizes.cpu().numpy()
+    fl = flags.cpu().numpy()
+    assert np.all(fl == 7)
+    buf = out.cpu().numpy()
+    ce = cb // EB[dtype]
+    for c, w in enumerate(want):
+        assert sz[c] == w.size
+        assert np.array_equal(buf[c * slot:c * slot + w.size], w), f"chunk {c}"
+        y, st = uz.decompress(out[c * slot:(c + 1) * slot], dtype, min(ce, n - c * ce))
+        torch.cuda.synchronize()
+        assert int(st.item()) == 0
+        assert np.array_equal(host_bits(y, dtype), x[c * ce:(c + 1) * ce])
+
+
+def test_chunked_flags_host_mapped(uz):
+    """Flags in pinned host memory: the device publishes them with
+    system-scope release stores; the host sees the final values."""
+    say("[parity] chunked host-mapped flags")
+    x = W.normal_bf16(5 * (1 << 19), seed=5)
+    xt = to_dev_bits(x, "bf16")
+    flags = torch.zeros(2 * 5, dtype=torch.int32).pin_memory()
+    out, slot, sizes, fl = uz.compress_chunked(xt, 65536, 1 << 20, dtype="bf16", epoch=3, flags=flags)
+    torch.cuda.synchronize()
+    assert np.all(flags.numpy() == 3)
+    want = ref.compress_chunked(x, "bf16", 65536, 1 << 20)
+    buf = out.cpu().numpy()
+    for c, w in enumerate(want):
+        assert np.array_equal(buf[c * slot:c * slot + w.size], w)
+
+
+# ---------------------------------------------------------- fused reduce
+@pytest.mark.parametrize("dtype", ["bf16", "fp16", "fp32"])
+@pytest.mark.parametrize("n_in", [1, 2, 8])
+def test_reduce_matches_oracle(uz, dtype, n_in):
+    n = 150_001
+    bb = 65536 if dtype != "fp32" else 262144
+    say(f"[parity] reduce dtype={dtype} n_in={n_in} n={n}")
+    xs = [special_words(dtype, n, seed=200 + i) for i in range(n_in)]
+    streams = [ref.compress(v, dtype, bb) for v in xs]
+    local = special_words(dtype, n, seed=77)
+    for use_local in (False, True):
+        for want_raw in (True, False):
+            dstreams = [dev(s) for s in streams]
+            out, size, raw, status = uz.reduce_fused(dstreams, dtype, n, bb,
+                                                     local=to_dev_bits(local, dtype) if use_local else None,
+                                                     want_raw=want_raw)
+            torch.cuda.synchronize()
+            want_s, want_y = ref.reduce(streams, dtype, n, bb, local=local if use_local else None)
+            assert int(status.item()) == 0
+            got = out[:int(size.item())].cpu().numpy()
+            assert np.array_equal(got, want_s), (use_local, want_raw)
+            if want_raw:
+                assert np.array_equal(host_bits(raw, dtype), want_y)
+
+
+def test_reduce_sixteen_inputs_with_stored_blocks(uz):
+    n = 70_000
+    say("[parity] reduce n_in=16")
+    xs = [special_words("bf16", n, seed=300 + i) for i in range(15)] + [W.random_bits(n, 16, seed=5)]
+    streams = [ref.compress(v, "bf16", 65536) for v in xs]
+    out, size, raw, status = uz.reduce_fused([dev(s) for s in streams], "bf16", n, 65536)
+    torch.cuda.synchronize()
+    want_s, want_y = ref.reduce(streams, "bf16", n, 65536)
+    assert int(status.item()) == 0
+    assert np.array_equal(out[:int(size.item())].cpu().numpy(), want_s)
+    assert np.array_equal(host_bits(raw, "bf16"), want_y)
+
+
+def test_reduce_eight_slices_share(uz):
+    """Eight bf16 shares [tokens x 8192] with per-token scales (64 tokens)."""
+    xs = W.reduce_slices(n_in=8, tokens=64, hidden=8192, seed=5)
+    n = xs[0].size
+    say("[parity] reduce 8 slices")
+    streams = [ref.compress(v, "bf16", 65536) for v in xs]
+    out, size, raw, status = uz.reduce_fused([dev(s) for s in streams], "bf16", n, 65536)
+    torch.cuda.synchronize()
+    want_s, want_y = ref.reduce(streams, "bf16", n, 65536)
+    assert int(status.item()) == 0
+    assert np.array_equal(out[:int(size.item())].cpu().numpy(), want_s)
+    assert np.array_equal(host_bits(raw, "bf16"), want_y)
+
+
+# ---------------------------------------------------------- corrupt streams
+def test_corrupt_streams_reported(uz):
+    """Header, directory and truncation damage is reported through the
+    device status word; the decoder's reads stay inside the stream."""
+    say("[parity] corrupt streams")
+    x = W.normal_bf16(100_000, seed=8)
+    good = ref.compress(x, "bf16", 4096)
+    cases = []
+    for off in (0, 4, 5, 6, 7, 8, 12, 16, 24, 32, 36):
+        bad = good.copy()
+        bad[off] ^= 0x5A
+        cases.append((f"byte {off}", bad, good.size))
+    cases.append(("truncated", good, good.size - 16))
+    cases.append(("tiny", good, 8))
+    for label, s, nbytes in cases:
+        y, status = uz.decompress(dev(s), "bf16", 100_000, in_bytes=nbytes)
+        torch.cuda.synchronize()
+        assert int(status.item()) == uz.ECORRUPT, label
+    # payload damage: never out of bounds; mostly detected
+    rng = np.random.default_rng(3)
+    detected = 0
+    for _ in range(40):
+        bad = good.copy()
+        pos = int(rng.integers(100, good.size))
+        bad[pos] ^= 1 << int(rng.integers(0, 8))
+        y, status = uz.decompress(dev(bad), "bf16", 100_000)
+        torch.cuda.synchronize()
+        detected += int(status.item()) != 0 or not np.array_equal(host_bits(y, "bf16"), x)
+    assert detected >= 30
+
+
+def test_reduce_rejects_mismatched_inputs(uz):
+    say("[parity] reduce mismatch")
+    a = W.normal_bf16(50_000, seed=1)
+    s1 = ref.compress(a, "bf16", 65536)
+    s2 = ref.compress(a[:40_000], "bf16", 65536)
+    out, size, raw, status = uz.reduce_fused([dev(s1), dev(s2)], "bf16", 50_000, 65536)
+    torch.cuda.synchronize()
+    assert int(status.item()) == uz.ECORRUPT

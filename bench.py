@@ -1,0 +1,246 @@
+#!/usr/bin/env python3
+"""Benchmark of the gfx950 block-wise lossless float codec on one MI355X.
+
+Workload: the 1 GiB bf16 weight-sync buffer (a 0.5B-parameter transformer's
+weights, 2^29 elements, 64 KiB codec blocks; workloads.weight_sync).  One
+step compresses the whole buffer (uzip_compress) and decompresses the
+stream again (uzip_decompress), inputs resident in HBM.  ``value`` is the
+uncompressed bytes of the buffer divided by the time of one step.  The line
+also reports compress and decompress rates separately, the ratio, the
+split-send producer on the same buffer (4 MiB chunks, host-mapped flags),
+the fused reduce of eight 16 MiB bf16 shares, the HBM roofline of the
+dominant kernel and the CPU oracle timed on a bounded sample.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "compress & decompress GB/s (uncompressed) + ratio, % of HBM roofline, 1 GPU"
+HBM_PEAK_GBPS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_weight_sync_bf16_1GiB.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2604_17172_amd", "csrc", "uzip.hip")
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for name in ("uzip.hip", "uzip_device.h"):
+        with open(os.path.join(os.path.dirname(KERNEL_SRC), name), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary, or None if it is missing or the kernels changed since."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    k = t.get("kernels", {}).get(kernel)
+    if not k:
+        return None
+    return k.get("hbm_bytes_per_launch")
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true", help="skip the chunked and reduce legs")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a 1 GiB device copy (counter calibration under rocprofv3)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the codec shards per GPU with no exchange; see the design notes)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import workloads as W
+    import paper_2604_17172_amd as uz  # fails loudly without the HIP library
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+
+    # ---------------- workload: 1 GiB bf16 weight-sync buffer ----------------
+    bb = 65536
+    t0 = time.time()
+    x_host = W.weight_sync()
+    n = x_host.size
+    nbytes = 2 * n
+    log(f"[bench] generated weight_sync n={n} in {time.time() - t0:.1f}s")
+    x = torch.from_numpy(x_host.view(np.int16)).to(dev)
+    cap = uz.uzip_max_compressed_size(uz.BF16, n, bb)
+    out = torch.empty(cap, dtype=torch.uint8, device=dev)
+    ws = torch.empty(uz.uzip_workspace_size(uz.OP_COMPRESS, uz.BF16, n, bb), dtype=torch.uint8, device=dev)
+    y = torch.empty_like(x)
+
+    size = status = None
+    for _ in range(args.warmup):
+        _, size = uz.compress(x, bb, dtype="bf16", out=out, ws=ws)
+        _, status = uz.decompress(out, "bf16", n, out=y)
+    torch.cuda.synchronize()
+    total = int(size.item())
+    if int(status.item()) != 0 or not torch.equal(x, y):
+        log("[bench] round trip is NOT lossless")
+        return 1
+    log(f"[bench] warmup done, ratio {total / nbytes:.4f}")
+
+    comp_ms, dec_ms, evs = [], [], []
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record(stream)
+        uz.compress(x, bb, dtype="bf16", out=out, ws=ws)
+        e[1].record(stream)
+        uz.decompress(out, "bf16", n, out=y)
+        e[2].record(stream)
+        evs.append(e)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    for e in evs:
+        comp_ms.append(e[0].elapsed_time(e[1]))
+        dec_ms.append(e[1].elapsed_time(e[2]))
+    ms_per_step = 1e3 * wall / args.steps
+    c_ms = float(np.mean(comp_ms))
+    d_ms = float(np.mean(dec_ms))
+    comp_gbps = nbytes / (c_ms * 1e-3) / 1e9
+    dec_gbps = nbytes / (d_ms * 1e-3) / 1e9
+    value = nbytes / (ms_per_step * 1e-3) / 1e9
+    log(f"[bench] compress {c_ms:.3f} ms ({comp_gbps:.0f} GB/s)  decompress {d_ms:.3f} ms ({dec_gbps:.0f} GB/s)")
+
+    # roofline of the dominant kernel: algorithmic HBM bytes per launch
+    alg_comp = nbytes + total      # read the tensor, write the stream
+    alg_dec = total + nbytes       # read the stream, write the tensor
+    if c_ms >= d_ms:
+        dom, dom_ms, dom_bytes, kname = "compress", c_ms, alg_comp, "encode_kernel<bf16>"
+    else:
+        dom, dom_ms, dom_bytes, kname = "decompress", d_ms, alg_dec, "decode_kernel<bf16>"
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "kernel": kname, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                "traffic": measured_traffic(kname),
+                "algorithmic_bytes_per_launch": dom_bytes,
+                "compress_frac": round(alg_comp / (c_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                "decompress_frac": round(alg_dec / (d_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)}
+
+    extras = {}
+    if not args.no_extras:
+        # ------------- split-send producer: 4 MiB chunks, host-mapped flags -------------
+        cb = 4 << 20
+        chunks = (nbytes + cb - 1) // cb
+        flags = torch.zeros(2 * chunks, dtype=torch.int32).pin_memory()
+        slot = (uz.uzip_max_compressed_size(uz.BF16, cb // 2, bb) + 255) // 256 * 256
+        cout = torch.empty(slot * chunks, dtype=torch.uint8, device=dev)
+        cws = torch.empty(uz.uzip_workspace_size(uz.OP_CHUNKED, uz.BF16, n, bb, cb), dtype=torch.uint8, device=dev)
+        reps = 5
+        times = []
+        for r in range(reps + 1):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            _, _, sizes, _ = uz.compress_chunked(x, bb, cb, dtype="bf16", epoch=r + 1, flags=flags, out=cout, ws=cws)
+            b.record(stream)
+            torch.cuda.synchronize()
+            if r > 0:
+                times.append(a.elapsed_time(b))
+        assert bool((flags == reps + 1).all())
+        ch_ms = float(np.mean(times))
+        extras["chunked"] = {"chunk_bytes": cb, "chunks": chunks, "ms": round(ch_ms, 4),
+                             "GBps": round(nbytes / (ch_ms * 1e-3) / 1e9, 1),
+                             "ratio": round(float(sizes.sum().item()) / nbytes, 4)}
+        log(f"[bench] chunked producer {ch_ms:.3f} ms")
+
+        # ------------- fused reduce: 8 compressed bf16 shares [1024 x 8192] -------------
+        shares = W.reduce_slices()
+        rn = shares[0].size
+        streams = []
+        for s in shares:
+            st, sz = uz.compress(torch.from_numpy(s.view(np.int16)).to(dev), bb, dtype="bf16")
+            streams.append(st[:int(sz.item())].clone())
+        in_bytes = [t.numel() for t in streams]
+        rcap = uz.uzip_max_compressed_size(uz.BF16, rn, bb)
+        rout = torch.empty(rcap, dtype=torch.uint8, device=dev)
+        rws = torch.empty(uz.uzip_workspace_size(uz.OP_REDUCE, uz.BF16, rn, bb, 8), dtype=torch.uint8, device=dev)
+        times = []
+        for r in range(reps + 1):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            _, rsz, raw, rst = uz.reduce_fused(streams, "bf16", rn, bb, out=rout, ws=rws)
+            b.record(stream)
+            torch.cuda.synchronize()
+            if r > 0:
+                times.append(a.elapsed_time(b))
+        assert int(rst.item()) == 0
+        r_ms = float(np.mean(times))
+        moved = sum(in_bytes) + int(rsz.item()) + 2 * rn
+        extras["reduce"] = {"n_in": 8, "share_elems": rn, "ms": round(r_ms, 4),
+                            "input_GBps_uncompressed": round(8 * 2 * rn / (r_ms * 1e-3) / 1e9, 1),
+                            "hbm_frac": round(moved / (r_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                            "ratio_in": round(sum(in_bytes) / (8 * 2 * rn), 4),
+                            "ratio_out": round(int(rsz.item()) / (2 * rn), 4)}
+        log(f"[bench] fused reduce {r_ms:.3f} ms")
+
+    if args.calibrate_copy:
+        # a plain device copy of known size, for scaling the HBM counters
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import ref
+        sample = x_host[: 1 << 27]  # first 256 MiB of the buffer
+        t0 = time.perf_counter()
+        s = ref.compress(sample, "bf16", bb)
+        yy = ref.decompress(s, "bf16", sample.size)
+        dt = time.perf_counter() - t0
+        assert yy is not None and np.array_equal(yy, sample)
+        cpu = {"value": round(2 * sample.size / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+               "sample": "compress+decompress round trip of the first 256 MiB of the weight-sync buffer, "
+                         "single-threaded C oracle",
+               "seconds": round(dt, 2)}
+        log(f"[bench] cpu oracle {dt:.1f}s")
+
+    line = {
+        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32",
+        "data": "synthetic",
+        "config": {"workload": "weight_sync_bf16_1GiB", "elem_dtype": "bf16", "n_elems": n,
+                   "block_bytes": bb, "step": "uzip_compress + uzip_decompress of the whole buffer"},
+        "compress_GBps": round(comp_gbps, 1), "decompress_GBps": round(dec_gbps, 1),
+        "compress_ms": round(c_ms, 4), "decompress_ms": round(d_ms, 4),
+        "ratio": round(total / nbytes, 5), "compressed_bytes": total,
+        "roofline": roofline, "cpu_baseline": cpu, **extras,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -63,8 +63,13 @@ struct EncodeArgs {
   const uint8_t *ins[kMaxInputs];
   uint64_t in_bytes[kMaxInputs];
   const uint8_t *local_raw;
-  uint8_t *ybuf;            // reduced tensor, re-read by pass 2
+  uint8_t *ybuf;            // reduced tensor re-read by pass 2 (large blocks)
+  uint8_t *yout;            // caller's copy of the reduced tensor (may be null)
   uint32_t *dstatus;
+  // small-block path: per-workgroup overflow slots for the staged words
+  uint16_t *slots;
+  uint32_t slot_words;
+  uint32_t lds_words;       // staging words held in LDS
 };
 
 struct DecodeArgs {
@@ -246,10 +251,14 @@ __device__ bool build_lut(const uint8_t *sec, uint64_t sec_len, uint32_t *lut, u
       hi = mid - 1;
   }
   uint32_t s = lo;
+  uint32_t c0 = cum_s[s], fs = f_s[s];
   for (uint32_t q = 0; q < 32; ++q, ++slot) {
-    while (slot >= (uint32_t)cum_s[s] + f_s[s]) ++s;
-    uint32_t fs = f_s[s];
-    lut[slot] = fs | ((slot - cum_s[s]) << 12) | (s << 24);
+    while (slot >= c0 + fs) {
+      ++s;
+      c0 = cum_s[s];
+      fs = f_s[s];
+    }
+    lut[slot] = fs | ((slot - c0) << 12) | (s << 24);
   }
   __syncthreads();
   k_out = k;
@@ -428,332 +437,663 @@ __device__ inline uint32_t from_f32(float f) {
 }
 
 // ---------------------------------------------------------------------------
-// encode_kernel: compress / split-send producer / fused reduce
+// Symbols of a whole block (up to 64 rounds, block_elems <= 32768) stay in
+// registers between the histogram pass and the coding pass, with static
+// register indices only: a pass walks the block in 4 groups of 16 rounds
+// with the 16 rounds unrolled, always touching vector v3 (pass 1) or v3
+// (pass 2), and the four vectors rotate cyclically between groups.
 // ---------------------------------------------------------------------------
-template <int DT, bool REDUCE>
+typedef uint32_t v32u __attribute__((ext_vector_type(32)));
+struct SymRegs {
+  v32u v0, v1, v2, v3;
+};
+constexpr uint32_t kRegRounds = 64;
+
+// pass 1: group g was just written to v3; move it down (v0 ends up with group 0)
+__device__ __forceinline__ void shift_down(SymRegs &S) {
+  S.v0 = S.v1;
+  S.v1 = S.v2;
+  S.v2 = S.v3;
+}
+// pass 2: group g in v3 has been coded; bring group g-1 up
+__device__ __forceinline__ void shift_up(SymRegs &S) {
+  S.v3 = S.v2;
+  S.v2 = S.v1;
+  S.v1 = S.v0;
+}
+
+// One encoder sub-step of every lane (rANS coding function with 16-bit
+// renormalisation).  Emitted words go to virtual staging index
+// pos - cnt + rank: index v >= lo lives in LDS at lds[v - lo], smaller
+// indices in the workgroup's overflow slot in global memory.
+template <bool OVF, bool FULL>
+__device__ __forceinline__ void enc_step(uint32_t &x, const uint4 e, bool valid, uint32_t &pos, uint16_t *lds,
+                                         uint16_t *ovf, uint32_t lo) {
+  const bool emit = (FULL || valid) && x >= e.y;
+  const uint64_t m = __ballot(emit);
+  const uint32_t cnt = (uint32_t)__popcll(m);
+  const uint32_t base = pos - cnt;
+  if (!OVF || base >= lo) {
+    if (emit) {
+      lds[base - lo + mbcnt(m)] = (uint16_t)x;
+      x >>= 16;
+    }
+  } else if (emit) {
+    const uint32_t v = base + mbcnt(m);
+    if (v >= lo)
+      lds[v - lo] = (uint16_t)x;
+    else
+      ovf[v] = (uint16_t)x;
+    x >>= 16;
+  }
+  pos = base;
+  if (FULL || valid) {
+    const uint32_t q = __umulhi(x, e.x) >> (e.z >> 24);
+    x = x + __umul24(q, e.z) + e.w;
+  }
+}
+
+template <int E>
+__device__ __forceinline__ void load_full(const uint8_t *base, uint64_t first, uint32_t w[4 * (E / 2)]) {
+  const uint4 *p = (const uint4 *)(base + first * E);
+  uint4 a = p[0];
+  w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
+  if (E == 4) {
+    uint4 b = p[1];
+    w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
+  }
+}
+
+template <int E>
+__device__ __forceinline__ void store_raw_full(uint8_t *plane, uint64_t first, const Group &g) {
+  uint2 *q = (uint2 *)(plane + (uint64_t)(E - 1) * first);
+  q[0] = make_uint2(g.raw[0], g.raw[1]);
+  if (E == 4) {
+    q[1] = make_uint2(g.raw[2], g.raw[3]);
+    q[2] = make_uint2(g.raw[4], g.raw[5]);
+  }
+}
+
+__device__ __forceinline__ void hist_add8(uint32_t *h, const Group &g, uint32_t valid) {
+#pragma unroll
+  for (uint32_t q = 0; q < 8; ++q)
+    if (q < valid) atomicAdd(&h[sym_at(g.sym, q)], 1u);
+}
+
+// ---------------------------------------------------------------------------
+// encode_kernel: compress / split-send producer / fused reduce.
+// Persistent workgroups of one wave take blocks in ticket order.
+// SMALL: block_elems <= 32768, the block's symbols stay in registers and the
+//   LDS staging area holds a.lds_words words, the rest spills to the
+//   workgroup's overflow slot.  Otherwise the coding pass re-reads the block
+//   and LDS holds the whole staging area.
+// ---------------------------------------------------------------------------
+template <int DT, bool REDUCE, bool SMALL>
 __global__ void __launch_bounds__(64) encode_kernel(EncodeArgs a) {
   constexpr int E = (DT == 2) ? 4 : 2;
   constexpr int NW = 4 * (E / 2);
+  constexpr int D = 4;  // pass-1 load pipeline depth (rounds)
   extern __shared__ __align__(16) uint8_t smem[];
   uint4 *enc = (uint4 *)smem;
   uint32_t *hist = (uint32_t *)(smem + kEncTableBytes);
   uint8_t *stage = smem + a.pass2_off;
   uint16_t *stage16 = (uint16_t *)(stage + kStageHead);
   const uint32_t lane = lane_id();
+  uint16_t *ovf = SMALL ? a.slots + (uint64_t)blockIdx.x * a.slot_words : nullptr;
+  const uint32_t lo = SMALL ? a.wcap - a.lds_words : 0;  // virtual index of stage16[0]
 
-  uint32_t b = 0;
-  if (lane == 0) b = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  b = uniform(b);
-  if (b >= a.n_blocks) return;
+  while (true) {
+    uint32_t b = 0;
+    if (lane == 0) b = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    b = uniform(b);
+    if (b >= a.n_blocks) break;
 
-  const uint32_t chunk = b / a.blocks_per_chunk;
-  const uint32_t lb = b - chunk * a.blocks_per_chunk;
-  const uint32_t first_block = b - lb;
-  const uint64_t chunk_first = (uint64_t)chunk * a.chunk_elems;
-  const uint64_t chunk_n = (a.n - chunk_first) < a.chunk_elems ? (a.n - chunk_first) : a.chunk_elems;
-  const Geom g = make_geom(chunk_n, a.block_elems, E);
-  uint8_t *sout = a.out + (uint64_t)chunk * a.slot_bytes;
-  const uint64_t blk0 = (uint64_t)lb * a.block_elems;  // chunk-relative
-  const uint32_t n_b = (uint32_t)((chunk_n - blk0) < a.block_elems ? (chunk_n - blk0) : a.block_elems);
-  const uint32_t rounds = (n_b + kRound - 1) / kRound;
-  const bool last_in_chunk = (lb + 1 == g.n_blocks);
-  const uint8_t *src = REDUCE ? a.ybuf : a.in + chunk_first * E;  // pass 2 source
+    const uint32_t chunk = b / a.blocks_per_chunk;
+    const uint32_t lb = b - chunk * a.blocks_per_chunk;
+    const uint32_t first_block = b - lb;
+    const uint64_t chunk_first = (uint64_t)chunk * a.chunk_elems;
+    const uint64_t chunk_n = (a.n - chunk_first) < a.chunk_elems ? (a.n - chunk_first) : a.chunk_elems;
+    const Geom g = make_geom(chunk_n, a.block_elems, E);
+    uint8_t *sout = a.out + (uint64_t)chunk * a.slot_bytes;
+    const uint64_t blk0 = (uint64_t)lb * a.block_elems;  // chunk-relative
+    const uint32_t n_b = (uint32_t)((chunk_n - blk0) < a.block_elems ? (chunk_n - blk0) : a.block_elems);
+    const uint32_t rounds = (n_b + kRound - 1) / kRound;
+    const uint32_t full = n_b / kRound;
+    const bool last_in_chunk = (lb + 1 == g.n_blocks);
+    const uint8_t *src = REDUCE ? a.ybuf : a.in + chunk_first * E;  // pass-2 source (large blocks)
+    uint8_t *raw_plane = sout + g.raw_off;
+    uint32_t *h = hist + (lane & (kHistReplicas - 1)) * kHistStride;
+    SymRegs S;
 
-  // ---- pass 1: split, raw plane, histogram ----
-  for (uint32_t i = lane; i < kHistReplicas * kHistStride; i += 64) hist[i] = 0;
-  __syncthreads();
+    // ---- pass 1: split, raw plane to its final place, histogram ----
+    for (uint32_t i = lane; i < kHistReplicas * kHistStride; i += 64) hist[i] = 0;
+    __syncthreads();
 
-  if constexpr (!REDUCE) {
-    for (uint32_t r = 0; r < rounds; ++r) {
-      uint32_t i0 = r * kRound + kPerLane * lane;
-      uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
-      if (valid == 0) continue;
-      uint32_t w[NW];
-      load_words<E>(src, blk0 + i0, valid, w);
-      Group gr;
-      split_group<E>(w, gr);
-      store_raw<E>(sout + g.raw_off, blk0 + i0, valid, gr);
-      uint32_t *h = hist + (lane & (kHistReplicas - 1)) * kHistStride;
-#pragma unroll
-      for (uint32_t q = 0; q < 8; ++q)
-        if (q < valid) atomicAdd(&h[sym_at(gr.sym, q)], 1u);
-    }
-  } else {
-    // fused reduce: decode block b of every input, add in order, round
-    uint32_t *luts = (uint32_t *)(smem + kEncTableBytes + kHistBytes);
-    uint16_t *cum_s = (uint16_t *)(smem + kEncTableBytes + kHistBytes + a.n_in * kLutBytes);
-    uint16_t *f_s = cum_s + 256;
-    InBlock ib[kMaxInputs];
-    uint32_t x[kMaxInputs], p[kMaxInputs];
-    bool bad = false;
-#pragma unroll
-    for (int i = 0; i < kMaxInputs; ++i) {
-      x[i] = kStateLo;
-      p[i] = 0;
-      ib[i].sec = nullptr;
-      ib[i].words = nullptr;
-      ib[i].raw_plane = nullptr;
-      ib[i].w_avail = 0;
-      ib[i].stored = 1;
-      if (i < a.n_in) {
-        const uint8_t *s = a.ins[i];
-        const uint64_t total = ld64(s + 24);
-        const uint32_t be = ld32(s + 8), nb = ld32(s + 12);
-        bool ok = a.in_bytes[i] >= kHeaderBytes && ld32(s) == kMagic && s[4] == kVersion && s[5] == DT &&
-                  s[6] == kProbBits && s[7] == 0 && be == a.block_elems && nb == g.n_blocks &&
-                  ld64(s + 16) == chunk_n && total <= a.in_bytes[i] && total >= g.coded_off;
-        uint64_t start = 0, end = 0;
-        uint32_t d = 0;
-        if (ok) {
-          d = ld32(s + kHeaderBytes + 4 * lb);
-          start = lb ? 16ull * (ld32(s + kHeaderBytes + 4 * (lb - 1)) & ~kStoredBit) : 0;
-          end = 16ull * (d & ~kStoredBit);
-          ok = end >= start && g.coded_off + end <= total;
+    uint32_t psym0 = 0, psym1 = 0;  // symbols of a partial last round
+    if constexpr (!REDUCE) {
+      auto partial_round = [&]() {
+        const uint32_t i0 = full * kRound + kPerLane * lane;
+        const uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
+        Group gr;
+        gr.sym[0] = gr.sym[1] = 0;
+        if (valid > 0) {
+          uint32_t w[NW];
+          load_words<E>(src, blk0 + i0, valid, w);
+          split_group<E>(w, gr);
+          store_raw<E>(raw_plane, blk0 + i0, valid, gr);
+          hist_add8(h, gr, valid);
         }
-        if (ok) {
-          ib[i].sec = s + g.coded_off + start;
-          ib[i].raw_plane = s + g.raw_off;
-          ib[i].stored = d >> 31;
-          if (ib[i].stored) {
-            ok = end - start >= n_b;
-          } else {
-            uint32_t k = 0;
-            ok = build_lut(ib[i].sec, end - start, luts + i * kM, cum_s, f_s, k);
-            if (ok) {
-              x[i] = ((const uint32_t *)ib[i].sec)[lane];
-              ok = !__any(x[i] < kStateLo || x[i] >= 0x80000000u);
-              ib[i].words = (const uint16_t *)(ib[i].sec + kSectionFixed + 2 * k);
-              ib[i].w_avail = (uint32_t)((end - start - kSectionFixed - 2 * k) / 2);
+        psym0 = gr.sym[0];
+        psym1 = gr.sym[1];
+      };
+      uint32_t buf[D][NW];
+      if (full > 0) {
+#pragma unroll
+        for (int u = 0; u < D; ++u)
+          load_full<E>(src, blk0 + (u < (int)full ? u : full - 1) * kRound + kPerLane * lane, buf[u]);
+      }
+      if constexpr (SMALL) {
+        for (uint32_t gi = 0; gi < 4; ++gi) {
+#pragma unroll
+          for (int rr = 0; rr < 16; ++rr) {
+            const uint32_t r = 16 * gi + rr;
+            if (r < full) {
+              uint32_t w[NW];
+#pragma unroll
+              for (int q = 0; q < NW; ++q) w[q] = buf[rr % D][q];
+              const uint32_t rn = (r + D < full) ? r + D : full - 1;
+              load_full<E>(src, blk0 + rn * kRound + kPerLane * lane, buf[rr % D]);
+              Group gr;
+              split_group<E>(w, gr);
+              S.v3[2 * rr] = gr.sym[0];
+              S.v3[2 * rr + 1] = gr.sym[1];
+              store_raw_full<E>(raw_plane, blk0 + r * kRound + kPerLane * lane, gr);
+              hist_add8(h, gr, 8);
+            } else if (r == full && full < rounds) {
+              partial_round();
+              S.v3[2 * rr] = psym0;
+              S.v3[2 * rr + 1] = psym1;
+            }
+          }
+          if (gi < 3) shift_down(S);
+        }
+      } else {
+        if (full > 0) {
+          uint32_t r = 0;
+          for (; r + D <= full; r += D) {
+#pragma unroll
+            for (int u = 0; u < D; ++u) {
+              uint32_t w[NW];
+#pragma unroll
+              for (int q = 0; q < NW; ++q) w[q] = buf[u][q];
+              const uint32_t rn = (r + u + D < full) ? r + u + D : full - 1;
+              load_full<E>(src, blk0 + rn * kRound + kPerLane * lane, buf[u]);
+              Group gr;
+              split_group<E>(w, gr);
+              store_raw_full<E>(raw_plane, blk0 + (r + u) * kRound + kPerLane * lane, gr);
+              hist_add8(h, gr, 8);
+            }
+          }
+#pragma unroll
+          for (int u = 0; u < D - 1; ++u) {
+            if (r + u < full) {
+              Group gr;
+              split_group<E>(buf[u], gr);
+              store_raw_full<E>(raw_plane, blk0 + (r + u) * kRound + kPerLane * lane, gr);
+              hist_add8(h, gr, 8);
             }
           }
         }
-        if (!ok) {
-          bad = true;
-          ib[i].stored = 1;
-          ib[i].sec = nullptr;
-        }
+        if (full < rounds) partial_round();
       }
-    }
-    __syncthreads();
-    for (uint32_t r = 0; r < rounds; ++r) {
-      uint32_t i0 = r * kRound + kPerLane * lane;
-      uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
-      float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    } else {
+      // fused reduce: decode block b of every input, add in order, round
+      uint32_t *luts = (uint32_t *)(smem + kEncTableBytes + kHistBytes);
+      uint16_t *cum_s = (uint16_t *)(smem + kEncTableBytes + kHistBytes + a.n_in * kLutBytes);
+      uint16_t *f_s = cum_s + 256;
+      InBlock ib[kMaxInputs];
+      uint32_t x[kMaxInputs], p[kMaxInputs];
+      bool bad = false;
 #pragma unroll
       for (int i = 0; i < kMaxInputs; ++i) {
+        x[i] = kStateLo;
+        p[i] = 0;
+        ib[i].sec = nullptr;
+        ib[i].words = nullptr;
+        ib[i].raw_plane = nullptr;
+        ib[i].w_avail = 0;
+        ib[i].stored = 1;
         if (i < a.n_in) {
-          uint32_t sym[2] = {0, 0};
-          if (ib[i].stored) {
-            if (ib[i].sec != nullptr && valid > 0)
-#pragma unroll
-              for (uint32_t q = 0; q < 8; ++q)
-                if (q < valid) sym[q >> 2] |= (uint32_t)ib[i].sec[i0 + q] << (8 * (q & 3));
-          } else {
-#pragma unroll
-            for (uint32_t t = 0; t < kPerLane; ++t) {
-              uint32_t s = decode_step(x[i], t < valid, luts + i * kM, ib[i].words, p[i], ib[i].w_avail, bad);
-              sym[t >> 2] |= s << (8 * (t & 3));
+          const uint8_t *s = a.ins[i];
+          const uint64_t total = ld64(s + 24);
+          const uint32_t be = ld32(s + 8), nb = ld32(s + 12);
+          bool ok = a.in_bytes[i] >= kHeaderBytes && ld32(s) == kMagic && s[4] == kVersion && s[5] == DT &&
+                    s[6] == kProbBits && s[7] == 0 && be == a.block_elems && nb == g.n_blocks &&
+                    ld64(s + 16) == chunk_n && total <= a.in_bytes[i] && total >= g.coded_off;
+          uint64_t start = 0, end = 0;
+          uint32_t d = 0;
+          if (ok) {
+            d = ld32(s + kHeaderBytes + 4 * lb);
+            start = lb ? 16ull * (ld32(s + kHeaderBytes + 4 * (lb - 1)) & ~kStoredBit) : 0;
+            end = 16ull * (d & ~kStoredBit);
+            ok = end >= start && g.coded_off + end <= total;
+          }
+          if (ok) {
+            ib[i].sec = s + g.coded_off + start;
+            ib[i].raw_plane = s + g.raw_off;
+            ib[i].stored = d >> 31;
+            if (ib[i].stored) {
+              ok = end - start >= n_b;
+            } else {
+              uint32_t k = 0;
+              ok = build_lut(ib[i].sec, end - start, luts + i * kM, cum_s, f_s, k);
+              if (ok) {
+                k = uniform(k);
+                x[i] = ((const uint32_t *)ib[i].sec)[lane];
+                ok = !__any(x[i] < kStateLo || x[i] >= 0x80000000u);
+                ib[i].words = (const uint16_t *)(ib[i].sec + kSectionFixed + 2 * k);
+                ib[i].w_avail = (uint32_t)((end - start - kSectionFixed - 2 * k) / 2);
+              }
             }
           }
-          uint32_t raw[6] = {0, 0, 0, 0, 0, 0};
-          if (valid > 0 && ib[i].raw_plane != nullptr) load_raw<E>(ib[i].raw_plane, blk0 + i0, valid, raw);
-          uint32_t w[NW];
-          merge_group<E>(sym, raw, w);
-#pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            uint32_t wq = (E == 2) ? ((w[q >> 1] >> (16 * (q & 1))) & 0xFFFFu) : w[q];
-            float v = to_f32<DT>(wq);
-            acc[q] = (i == 0) ? v : acc[q] + v;
+          if (!ok) {
+            bad = true;
+            ib[i].stored = 1;
+            ib[i].sec = nullptr;
           }
         }
       }
-      if (valid == 0) continue;
-      if (a.local_raw != nullptr) {
-        uint32_t w[NW];
-        load_words<E>(a.local_raw, blk0 + i0, valid, w);
+      __syncthreads();
+      for (uint32_t r = 0; r < rounds; ++r) {
+        uint32_t i0 = r * kRound + kPerLane * lane;
+        uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
+        float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          uint32_t wq = (E == 2) ? ((w[q >> 1] >> (16 * (q & 1))) & 0xFFFFu) : w[q];
-          acc[q] = acc[q] + to_f32<DT>(wq);
+        for (int i = 0; i < kMaxInputs; ++i) {
+          if (i < a.n_in) {
+            uint32_t sym[2] = {0, 0};
+            if (ib[i].stored) {
+              if (ib[i].sec != nullptr && valid > 0) {
+#pragma unroll
+                for (uint32_t q = 0; q < 8; ++q)
+                  if (q < valid) sym[q >> 2] |= (uint32_t)ib[i].sec[i0 + q] << (8 * (q & 3));
+              }
+            } else {
+#pragma unroll
+              for (uint32_t t = 0; t < kPerLane; ++t) {
+                uint32_t s = decode_step(x[i], t < valid, luts + i * kM, ib[i].words, p[i], ib[i].w_avail, bad);
+                sym[t >> 2] |= s << (8 * (t & 3));
+              }
+            }
+            uint32_t raw[6] = {0, 0, 0, 0, 0, 0};
+            if (valid > 0 && ib[i].raw_plane != nullptr) load_raw<E>(ib[i].raw_plane, blk0 + i0, valid, raw);
+            uint32_t w[NW];
+            merge_group<E>(sym, raw, w);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              uint32_t wq = (E == 2) ? ((w[q >> 1] >> (16 * (q & 1))) & 0xFFFFu) : w[q];
+              float v = to_f32<DT>(wq);
+              acc[q] = (i == 0) ? v : acc[q] + v;
+            }
+          }
+        }
+        Group gr;
+        gr.sym[0] = gr.sym[1] = 0;
+        if (valid > 0) {
+          if (a.local_raw != nullptr) {
+            uint32_t w[NW];
+            load_words<E>(a.local_raw, blk0 + i0, valid, w);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              uint32_t wq = (E == 2) ? ((w[q >> 1] >> (16 * (q & 1))) & 0xFFFFu) : w[q];
+              acc[q] = acc[q] + to_f32<DT>(wq);
+            }
+          }
+          uint32_t w[NW];
+#pragma unroll
+          for (int q = 0; q < NW; ++q) w[q] = 0;
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            uint32_t y = from_f32<DT>(acc[q]);
+            if (E == 2)
+              w[q >> 1] |= y << (16 * (q & 1));
+            else
+              w[q] = y;
+          }
+          if (a.yout != nullptr) store_words<E>(a.yout, blk0 + i0, valid, w);
+          if (a.ybuf != a.yout) store_words<E>(a.ybuf, blk0 + i0, valid, w);
+          split_group<E>(w, gr);
+          if (valid < 8) {
+            uint64_t keep = (1ull << (8 * valid)) - 1;
+            uint64_t v = ((uint64_t)gr.sym[1] << 32 | gr.sym[0]) & keep;
+            gr.sym[0] = (uint32_t)v;
+            gr.sym[1] = (uint32_t)(v >> 32);
+          }
+          store_raw<E>(raw_plane, blk0 + i0, valid, gr);
+          hist_add8(h, gr, valid);
         }
       }
-      uint32_t w[NW];
 #pragma unroll
-      for (int q = 0; q < NW; ++q) w[q] = 0;
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        uint32_t y = from_f32<DT>(acc[q]);
-        if (E == 2)
-          w[q >> 1] |= y << (16 * (q & 1));
-        else
-          w[q] = y;
-      }
-      store_words<E>(a.ybuf, blk0 + i0, valid, w);
-      Group gr;
-      split_group<E>(w, gr);
-      store_raw<E>(sout + g.raw_off, blk0 + i0, valid, gr);
-      uint32_t *h = hist + (lane & (kHistReplicas - 1)) * kHistStride;
-#pragma unroll
-      for (uint32_t q = 0; q < 8; ++q)
-        if (q < valid) atomicAdd(&h[sym_at(gr.sym, q)], 1u);
+      for (int i = 0; i < kMaxInputs; ++i)
+        if (i < a.n_in && !ib[i].stored && x[i] != kStateLo) bad = true;
+      if (__any(bad) && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
     }
-#pragma unroll
-    for (int i = 0; i < kMaxInputs; ++i)
-      if (i < a.n_in && !ib[i].stored && x[i] != kStateLo) bad = true;
-    if (__any(bad) && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
-  }
 
-  if (last_in_chunk && lane < 16) {
-    // zero padding after the raw plane (pad16 of (E-1) n bytes)
-    uint64_t rb = g.raw_off + (uint64_t)(E - 1) * chunk_n + lane;
-    if (rb < g.coded_off) sout[rb] = 0;
-  }
-  __syncthreads();
-  if (a.flags != nullptr) {
-    __threadfence_system();
-    publish_chunk(&a.chunk_cnt[2 * chunk], g.n_blocks, &a.flags[2 * chunk], a.epoch);
-  }
-
-  // ---- table ----
-  Table t;
-  build_enc_table(hist, n_b, enc, t);
-  __syncthreads();
-
-  // ---- pass 2: rANS over the block, backwards; words staged in LDS ----
-  for (uint32_t i = lane; i < kStageTail / 4; i += 64)
-    ((uint32_t *)(stage + kStageHead + 2 * a.wcap))[i] = 0;
-  const uint32_t limit_words = (n_b > kSectionFixed + 2 * t.k) ? (n_b - kSectionFixed - 2 * t.k + 1) / 2 : 0;
-  uint32_t pos = a.wcap;  // stage16[pos .. wcap) hold the words written so far
-  uint32_t x = kStateLo;
-  bool stored = (limit_words == 0);
-  for (int r = (int)rounds - 1; r >= 0 && !stored; --r) {
-    uint32_t i0 = (uint32_t)r * kRound + kPerLane * lane;
-    uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
-    uint32_t w[NW];
-    Group gr;
-    gr.sym[0] = gr.sym[1] = 0;
-    if (valid > 0) {
-      load_words<E>(src, blk0 + i0, valid, w);
-      split_group<E>(w, gr);
+    if (last_in_chunk && lane < 16) {
+      // zero padding after the raw plane (pad16 of (E-1) n bytes)
+      uint64_t rb = g.raw_off + (uint64_t)(E - 1) * chunk_n + lane;
+      if (rb < g.coded_off) sout[rb] = 0;
     }
-#pragma unroll
-    for (int tt = kPerLane - 1; tt >= 0; --tt) {
-      const bool v = (uint32_t)tt < valid;
-      uint4 e = enc[sym_at(gr.sym, tt)];
-      const bool emit = v && x >= e.y;
-      const uint64_t m = __ballot(emit);
-      const uint32_t cnt = (uint32_t)__popcll(m);
-      if (emit) {
-        stage16[pos - cnt + mbcnt(m)] = (uint16_t)x;
-        x >>= 16;
-      }
-      pos -= cnt;
-      if (v) {
-        uint32_t q = __umulhi(x, e.x) >> (e.z >> 24);
-        x = x + __umul24(q, e.z & 0xFFFFu) + e.w;
-      }
-    }
-    if (a.wcap - pos >= limit_words) stored = true;  // coded section no smaller than n_b
-  }
-  const uint32_t n_words = a.wcap - pos;
-  const uint64_t img = kSectionFixed + 2ull * t.k + 2ull * n_words;
-  const uint64_t sec_len = stored ? pad16(n_b) : pad16(img);
-
-  // ---- output offset: single-pass scan over the stream's blocks ----
-  const uint64_t excl = lookback(a.status, b, first_block, sec_len / 16, a.ticket + 1);
-  uint8_t *sec = sout + g.coded_off + 16 * excl;
-  if (lane == 0)
-    *(uint32_t *)(sout + kHeaderBytes + 4 * lb) = (stored ? kStoredBit : 0u) | (uint32_t)(excl + sec_len / 16);
-
-  if (!stored) {
-    // assemble states | bitmap | f[k] in front of the words, then copy out
-    const uint32_t A = kStageHead + 2 * pos - (kSectionFixed + 2 * t.k);
-    uint16_t *h16 = (uint16_t *)(stage + A);
-    h16[2 * lane] = (uint16_t)x;
-    h16[2 * lane + 1] = (uint16_t)(x >> 16);
-    if (lane < 16) {
-      uint32_t word = 0;
-      for (uint32_t bit = 0; bit < 16; ++bit) {
-        uint32_t s = 16 * lane + bit;
-        word |= (uint32_t)((t.present[s & 3] >> (s >> 2)) & 1u) << bit;
-      }
-      h16[128 + lane] = (uint16_t)word;
-    }
-    uint32_t rk = t.rank0;
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      if (t.f[q]) h16[144 + rk++] = (uint16_t)t.f[q];
     __syncthreads();
-    const uint32_t *s32 = (const uint32_t *)(stage + (A & ~3u));
-    const uint32_t sh = A & 3u;
-    for (uint32_t u = lane; u < sec_len / 16; u += 64) {
-      const uint32_t *q = s32 + 4 * u;
-      uint4 o;
-      o.x = __builtin_amdgcn_alignbyte(q[1], q[0], sh);
-      o.y = __builtin_amdgcn_alignbyte(q[2], q[1], sh);
-      o.z = __builtin_amdgcn_alignbyte(q[3], q[2], sh);
-      o.w = __builtin_amdgcn_alignbyte(q[4], q[3], sh);
-      ((uint4 *)sec)[u] = o;
+    if (a.flags != nullptr) {
+      __threadfence_system();
+      publish_chunk(&a.chunk_cnt[2 * chunk], g.n_blocks, &a.flags[2 * chunk], a.epoch);
     }
-  } else {
-    // STORED: the block's symbol bytes, zero-padded to 16
-    const uint32_t padded = (uint32_t)pad16(n_b);
-    for (uint32_t r = 0; r < rounds; ++r) {
-      uint32_t i0 = r * kRound + kPerLane * lane;
-      if (i0 >= padded) continue;
-      uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
-      Group gr;
-      gr.sym[0] = gr.sym[1] = 0;
-      if (valid > 0) {
+
+    // ---- table ----
+    Table t;
+    build_enc_table(hist, n_b, enc, t);
+    t.k = uniform(t.k);
+    __syncthreads();
+
+    // ---- pass 2: rANS over the block, backwards; words staged ----
+    for (uint32_t i = lane; i < kStageTail / 4; i += 64)
+      ((uint32_t *)(stage + kStageHead + 2 * (a.wcap - lo)))[i] = 0;
+    const uint32_t limit_words = (n_b > kSectionFixed + 2 * t.k) ? (n_b - kSectionFixed - 2 * t.k + 1) / 2 : 0;
+    uint32_t pos = a.wcap;  // virtual staging indices [pos, wcap) hold the words written so far
+    uint32_t x = kStateLo;
+    bool stored = (limit_words == 0);
+    if (full < rounds && !stored) {  // the partial last round comes first
+      const uint32_t i0 = full * kRound + kPerLane * lane;
+      const uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
+      uint32_t s0 = psym0, s1 = psym1;
+      if (REDUCE && valid > 0) {
         uint32_t w[NW];
+        Group gr;
         load_words<E>(src, blk0 + i0, valid, w);
         split_group<E>(w, gr);
-        if (valid < 8) {
-          uint64_t keep = (1ull << (8 * valid)) - 1;
-          uint64_t v = ((uint64_t)gr.sym[1] << 32 | gr.sym[0]) & keep;
-          gr.sym[0] = (uint32_t)v;
-          gr.sym[1] = (uint32_t)(v >> 32);
+        s0 = gr.sym[0];
+        s1 = gr.sym[1];
+      }
+      const uint32_t sy[2] = {s0, s1};
+      uint4 e[8];
+#pragma unroll
+      for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(sy, tt)];
+#pragma unroll
+      for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step<SMALL, false>(x, e[tt], (uint32_t)tt < valid, pos, stage16, ovf, lo);
+      if (a.wcap - pos >= limit_words) stored = true;
+    }
+    if constexpr (SMALL) {
+      for (int gi = 3; gi >= 0; --gi) {
+#pragma unroll
+        for (int rr = 15; rr >= 0; --rr) {
+          const int r = 16 * gi + rr;
+          if (r < (int)full && !stored) {
+            const uint32_t s0 = S.v3[2 * rr], s1 = S.v3[2 * rr + 1];
+            uint4 e[8];
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt) e[tt] = enc[(s0 >> (8 * tt)) & 0xFFu];
+#pragma unroll
+            for (int tt = 0; tt < 4; ++tt) e[4 + tt] = enc[(s1 >> (8 * tt)) & 0xFFu];
+#pragma unroll
+            for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step<true, true>(x, e[tt], true, pos, stage16, ovf, lo);
+            if (a.wcap - pos >= limit_words) stored = true;
+          }
+        }
+        if (gi > 0) shift_up(S);
+      }
+    } else {
+      // re-read the block backwards, one round ahead
+      uint32_t wa[NW], wbuf[NW];
+      if (full > 0) load_full<E>(src, blk0 + (full - 1) * kRound + kPerLane * lane, wa);
+      int r = (int)full - 1;
+      for (; r >= 1 && !stored; r -= 2) {
+        load_full<E>(src, blk0 + (uint32_t)(r - 1) * kRound + kPerLane * lane, wbuf);
+        Group gr;
+        split_group<E>(wa, gr);
+        uint4 e[8];
+#pragma unroll
+        for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
+#pragma unroll
+        for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step<false, true>(x, e[tt], true, pos, stage16, ovf, lo);
+        if (a.wcap - pos >= limit_words) stored = true;
+        if (stored) break;
+        const uint32_t rn = r >= 2 ? (uint32_t)(r - 2) : 0u;
+        load_full<E>(src, blk0 + rn * kRound + kPerLane * lane, wa);
+        split_group<E>(wbuf, gr);
+#pragma unroll
+        for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
+#pragma unroll
+        for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step<false, true>(x, e[tt], true, pos, stage16, ovf, lo);
+        if (a.wcap - pos >= limit_words) stored = true;
+      }
+      if (r == 0 && !stored) {  // wa holds round 0
+        Group gr;
+        split_group<E>(wa, gr);
+        uint4 e[8];
+#pragma unroll
+        for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
+#pragma unroll
+        for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step<false, true>(x, e[tt], true, pos, stage16, ovf, lo);
+        if (a.wcap - pos >= limit_words) stored = true;
+      }
+    }
+    pos = uniform(pos);
+    const uint32_t n_words = a.wcap - pos;
+    const uint64_t img = kSectionFixed + 2ull * t.k + 2ull * n_words;
+    const uint64_t sec_len = stored ? pad16(n_b) : pad16(img);
+
+    // ---- output offset: single-pass scan over the stream's blocks ----
+    const uint64_t excl = lookback(a.status, b, first_block, sec_len / 16, a.ticket + 1);
+    uint8_t *sec = sout + g.coded_off + 16 * excl;
+    if (lane == 0)
+      *(uint32_t *)(sout + kHeaderBytes + 4 * lb) = (stored ? kStoredBit : 0u) | (uint32_t)(excl + sec_len / 16);
+
+    if (!stored) {
+      const uint32_t hdr = kSectionFixed + 2 * t.k;
+      // header bytes: states | bitmap | f[k]
+      auto put_header = [&](uint16_t *h16) {
+        h16[2 * lane] = (uint16_t)x;
+        h16[2 * lane + 1] = (uint16_t)(x >> 16);
+        if (lane < 16) {
+          uint32_t word = 0;
+          for (uint32_t bit = 0; bit < 16; ++bit) {
+            uint32_t sy = 16 * lane + bit;
+            word |= (uint32_t)((t.present[sy & 3] >> (sy >> 2)) & 1u) << bit;
+          }
+          h16[128 + lane] = (uint16_t)word;
+        }
+        uint32_t rk = t.rank0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (t.f[q]) h16[144 + rk++] = (uint16_t)t.f[q];
+      };
+      if (!SMALL || pos >= lo) {
+        // the whole image is contiguous in LDS: header right before the words
+        const uint32_t A = kStageHead + 2 * (pos - lo) - hdr;
+        put_header((uint16_t *)(stage + A));
+        __syncthreads();
+        const uint32_t *s32 = (const uint32_t *)(stage + (A & ~3u));
+        const uint32_t sh = A & 3u;
+        for (uint32_t u = lane; u < sec_len / 16; u += 64) {
+          const uint32_t *q = s32 + 4 * u;
+          uint4 o;
+          o.x = __builtin_amdgcn_alignbyte(q[1], q[0], sh);
+          o.y = __builtin_amdgcn_alignbyte(q[2], q[1], sh);
+          o.z = __builtin_amdgcn_alignbyte(q[3], q[2], sh);
+          o.w = __builtin_amdgcn_alignbyte(q[4], q[3], sh);
+          ((uint4 *)sec)[u] = o;
+        }
+      } else {
+        // rare: words spilled to the overflow slot; gather header (LDS),
+        // spilled words (global, read back coherently) and LDS words
+        put_header((uint16_t *)stage);
+        __threadfence_block();
+        __syncthreads();
+        for (uint32_t u = lane; u < sec_len / 16; u += 64) {
+          uint32_t o[4] = {0, 0, 0, 0};
+#pragma unroll
+          for (uint32_t hw = 0; hw < 8; ++hw) {
+            const uint32_t ob = 16 * u + 2 * hw;
+            uint32_t v16 = 0;
+            if (ob < hdr) {
+              v16 = ((const uint16_t *)stage)[ob / 2];
+            } else if ((ob - hdr) / 2 < n_words) {
+              const uint32_t v = pos + (ob - hdr) / 2;
+              if (v >= lo) {
+                v16 = stage16[v - lo];
+              } else {
+                const uint32_t dw = __hip_atomic_load((const uint32_t *)ovf + (v >> 1), __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT);
+                v16 = (dw >> (16 * (v & 1))) & 0xFFFFu;
+              }
+            }
+            o[hw >> 1] |= v16 << (16 * (hw & 1));
+          }
+          ((uint4 *)sec)[u] = make_uint4(o[0], o[1], o[2], o[3]);
         }
       }
-      *(uint2 *)(sec + i0) = make_uint2(gr.sym[0], gr.sym[1]);
+    } else {
+      // STORED: the block's symbol bytes, zero-padded to 16
+      const uint32_t padded = (uint32_t)pad16(n_b);
+      auto put_stored = [&](uint32_t r, uint32_t s0, uint32_t s1) {
+        const uint32_t i0 = r * kRound + kPerLane * lane;
+        const uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
+        if (i0 >= padded) return;
+        if (valid < 8) {
+          uint64_t keep = valid ? (~0ull >> (64 - 8 * valid)) : 0ull;
+          uint64_t v = ((uint64_t)s1 << 32 | s0) & keep;
+          s0 = (uint32_t)v;
+          s1 = (uint32_t)(v >> 32);
+        }
+        *(uint2 *)(sec + i0) = make_uint2(s0, s1);
+      };
+      {  // the coding pass consumed the register copy of the symbols: re-read the block
+        for (uint32_t r = 0; r < rounds; ++r) {
+          const uint32_t i0 = r * kRound + kPerLane * lane;
+          const uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
+          uint32_t s0 = 0, s1 = 0;
+          if (valid > 0) {
+            uint32_t w[NW];
+            Group gr;
+            load_words<E>(src, blk0 + i0, valid, w);
+            split_group<E>(w, gr);
+            s0 = gr.sym[0];
+            s1 = gr.sym[1];
+          }
+          put_stored(r, s0, s1);
+        }
+      }
     }
-  }
 
-  if (last_in_chunk) {
-    const uint64_t total = g.coded_off + 16 * (excl + sec_len / 16);
-    if (lane == 0) {
-      uint32_t h[8];
-      h[0] = kMagic;
-      h[1] = kVersion | ((uint32_t)DT << 8) | (kProbBits << 16);
-      h[2] = a.block_elems;
-      h[3] = g.n_blocks;
-      h[4] = (uint32_t)chunk_n;
-      h[5] = (uint32_t)(chunk_n >> 32);
-      h[6] = (uint32_t)total;
-      h[7] = (uint32_t)(total >> 32);
-      uint4 *hp = (uint4 *)sout;
-      hp[0] = make_uint4(h[0], h[1], h[2], h[3]);
-      hp[1] = make_uint4(h[4], h[5], h[6], h[7]);
-      if (a.sizes != nullptr) a.sizes[chunk] = total;
+    if (last_in_chunk) {
+      const uint64_t total = g.coded_off + 16 * (excl + sec_len / 16);
+      if (lane == 0) {
+        uint32_t hh[8];
+        hh[0] = kMagic;
+        hh[1] = kVersion | ((uint32_t)DT << 8) | (kProbBits << 16);
+        hh[2] = a.block_elems;
+        hh[3] = g.n_blocks;
+        hh[4] = (uint32_t)chunk_n;
+        hh[5] = (uint32_t)(chunk_n >> 32);
+        hh[6] = (uint32_t)total;
+        hh[7] = (uint32_t)(total >> 32);
+        uint4 *hp = (uint4 *)sout;
+        hp[0] = make_uint4(hh[0], hh[1], hh[2], hh[3]);
+        hp[1] = make_uint4(hh[4], hh[5], hh[6], hh[7]);
+        if (a.sizes != nullptr) a.sizes[chunk] = total;
+      }
+      // zero padding after the directory
+      uint64_t db = kHeaderBytes + 4ull * g.n_blocks + lane;
+      if (lane < 16 && db < g.raw_off) sout[db] = 0;
     }
-    // zero padding after the directory
-    uint64_t db = kHeaderBytes + 4ull * g.n_blocks + lane;
-    if (lane < 16 && db < g.raw_off) sout[db] = 0;
-  }
-  if (a.flags != nullptr) {
-    __threadfence_system();
-    publish_chunk(&a.chunk_cnt[2 * chunk + 1], g.n_blocks, &a.flags[2 * chunk + 1], a.epoch);
+    if (a.flags != nullptr) {
+      __threadfence_system();
+      publish_chunk(&a.chunk_cnt[2 * chunk + 1], g.n_blocks, &a.flags[2 * chunk + 1], a.epoch);
+    }
+    __syncthreads();
   }
 }
 
 // ---------------------------------------------------------------------------
 // decode_kernel
+//
+// Words of a coded block are staged through a 4 KB LDS ring in 1 KB chunks
+// read with one 16-byte load per lane: a chunk is loaded as soon as the ring
+// has room and written to LDS only when the decoder is about to need it, so
+// the serial decode chain only ever waits on LDS.  The raw plane of the next
+// round is loaded one round ahead.
 // ---------------------------------------------------------------------------
+constexpr uint32_t kRingBytes = 4096;
+constexpr uint32_t kChunkBytes = 1024;
+
+template <bool FULL>
+__device__ inline uint32_t decode_step_ring(uint32_t &x, bool valid, const uint32_t *lut, const uint8_t *ring,
+                                            uint32_t wb, uint32_t &p, uint32_t w_avail, bool &bad) {
+  uint32_t s = 0;
+  if (FULL || valid) {
+    uint32_t e = lut[x & (kM - 1)];
+    s = e >> 24;
+    x = __umul24(e & 0xFFFu, x >> kProbBits) + ((e >> 12) & 0x7FFu);
+  }
+  bool need = (FULL || valid) && x < kStateLo;
+  uint64_t m = __ballot(need);
+  if (need) {
+    uint32_t idx = p + mbcnt(m);
+    uint32_t w = *(const uint16_t *)(ring + ((wb + 2 * idx) & (kRingBytes - 1)));
+    bad |= idx >= w_avail;
+    x = (x << 16) | w;
+  }
+  p += (uint32_t)__popcll(m);
+  return s;
+}
+
+// Ring bookkeeping of one coded block (all members wave-uniform).
+struct Ring {
+  uint32_t written;  // section bytes [written - 4096, written) are in the ring
+  uint32_t len;      // section length
+  bool pend;         // a chunk is loaded into registers, not yet in LDS
+  uint4 pv;
+};
+
+// Before a round: make sure the next 1 KB of words is in LDS, and start
+// loading the following chunk as soon as the ring has room for it.
+__device__ inline void ring_maintain(Ring &rg, uint8_t *ring, const uint8_t *sec, uint32_t cur) {
+  const uint32_t lane = lane_id();
+  if (rg.pend && rg.written < cur + kChunkBytes) {
+    *(uint4 *)(ring + ((rg.written + 16 * lane) & (kRingBytes - 1))) = rg.pv;
+    rg.written += kChunkBytes;
+    rg.pend = false;
+    __syncthreads();
+  }
+  if (!rg.pend && rg.written < rg.len && rg.written - cur <= kRingBytes - kChunkBytes) {
+    const uint32_t o = rg.written + 16 * lane;
+    rg.pv = o + 16 <= rg.len ? *(const uint4 *)(sec + o) : make_uint4(0, 0, 0, 0);
+    rg.pend = true;
+  }
+}
+
+template <int E>
+__device__ inline void load_raw_full(const uint8_t *plane, uint64_t first, uint32_t raw[6]) {
+  const uint2 *q = (const uint2 *)(plane + (uint64_t)(E - 1) * first);
+  uint2 a = q[0];
+  raw[0] = a.x;
+  raw[1] = a.y;
+  if (E == 4) {
+    uint2 b = q[1], c = q[2];
+    raw[2] = b.x;
+    raw[3] = b.y;
+    raw[4] = c.x;
+    raw[5] = c.y;
+  }
+}
+
 template <int DT>
 __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
   constexpr int E = (DT == 2) ? 4 : 2;
   constexpr int NW = 4 * (E / 2);
   __shared__ uint32_t lut[kM];
+  __shared__ __align__(16) uint8_t ring[kRingBytes];
   __shared__ uint16_t cum_s[256], f_s[256];
   const uint32_t lane = lane_id();
   const uint8_t *s = a.in;
@@ -773,11 +1113,11 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
     if (blockIdx.x == 0 && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
     return;
   }
-  if (blockIdx.x == 0 && lane == 0 && nb > 0) {
-    uint64_t endall = 16ull * (ld32(s + kHeaderBytes + 4 * (nb - 1)) & ~kStoredBit);
+  if (blockIdx.x == 0 && lane == 0) {
+    uint64_t endall = nb ? 16ull * (ld32(s + kHeaderBytes + 4 * (nb - 1)) & ~kStoredBit) : 0;
     if (g.coded_off + endall != total) report(a.dstatus, UZIP_ECORRUPT);
   }
-  if (blockIdx.x == 0 && lane == 0 && nb == 0 && total != g.coded_off) report(a.dstatus, UZIP_ECORRUPT);
+  const uint8_t *raw_plane = s + g.raw_off;
 
   for (uint32_t b = blockIdx.x; b < nb; b += gridDim.x) {
     const uint32_t d = ld32(s + kHeaderBytes + 4 * b);
@@ -788,31 +1128,20 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
     const uint32_t rounds = (n_b + kRound - 1) / kRound;
     bool bad = !(end >= start && g.coded_off + end <= total);
     const uint8_t *sec = s + g.coded_off + start;
-    const uint64_t len = bad ? 0 : end - start;
+    const uint32_t len = bad ? 0 : (uint32_t)(end - start);
     const bool stored = d >> 31;
     if (!bad && stored && len < n_b) bad = true;
-    uint32_t k = 0, x = kStateLo, p = 0, w_avail = 0;
-    const uint16_t *words = nullptr;
-    if (!bad && !stored) {
-      if (len < kSectionFixed || !build_lut(sec, len, lut, cum_s, f_s, k)) {
-        bad = true;
-      } else {
-        x = ((const uint32_t *)sec)[lane];
-        if (__any(x < kStateLo || x >= 0x80000000u)) bad = true;
-        words = (const uint16_t *)(sec + kSectionFixed + 2 * k);
-        w_avail = (uint32_t)((len - kSectionFixed - 2 * k) / 2);
-      }
-    }
     if (bad) {
       if (lane == 0) report(a.dstatus, UZIP_ECORRUPT);
       continue;
     }
-    for (uint32_t r = 0; r < rounds; ++r) {
-      uint32_t i0 = r * kRound + kPerLane * lane;
-      uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
-      uint32_t sym[2] = {0, 0};
-      if (stored) {
-        if (valid >= 8) {
+    if (stored) {
+      for (uint32_t r = 0; r < rounds; ++r) {
+        uint32_t i0 = r * kRound + kPerLane * lane;
+        uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
+        if (valid == 0) continue;
+        uint32_t sym[2] = {0, 0};
+        if (valid == 8) {
           uint2 v = *(const uint2 *)(sec + i0);
           sym[0] = v.x;
           sym[1] = v.y;
@@ -821,21 +1150,97 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
           for (uint32_t q = 0; q < 8; ++q)
             if (q < valid) sym[q >> 2] |= (uint32_t)sec[i0 + q] << (8 * (q & 3));
         }
-      } else {
-#pragma unroll
-        for (uint32_t t = 0; t < kPerLane; ++t) {
-          uint32_t sy = decode_step(x, t < valid, lut, words, p, w_avail, bad);
-          sym[t >> 2] |= sy << (8 * (t & 3));
-        }
+        uint32_t raw[6];
+        load_raw<E>(raw_plane, blk0 + i0, valid, raw);
+        uint32_t w[NW];
+        merge_group<E>(sym, raw, w);
+        store_words<E>(a.out, blk0 + i0, valid, w);
       }
-      if (valid == 0) continue;
-      uint32_t raw[6];
-      load_raw<E>(s + g.raw_off, blk0 + i0, valid, raw);
-      uint32_t w[NW];
-      merge_group<E>(sym, raw, w);
-      store_words<E>(a.out, blk0 + i0, valid, w);
+      continue;
     }
-    if (!stored && x != kStateLo) bad = true;
+    uint32_t k = 0;
+    if (!build_lut(sec, len, lut, cum_s, f_s, k)) {
+      if (lane == 0) report(a.dstatus, UZIP_ECORRUPT);
+      continue;
+    }
+    k = uniform(k);
+    uint32_t x = ((const uint32_t *)sec)[lane];
+    bad = __any(x < kStateLo || x >= 0x80000000u);
+    const uint32_t wb = kSectionFixed + 2 * k;  // section offset of word 0
+    const uint32_t w_avail = (len - wb) / 2;
+    Ring rg;
+    rg.len = len;
+    rg.written = wb & ~15u;
+    rg.pend = false;
+    rg.pv = make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      if (rg.written < len) {
+        uint32_t o = rg.written + 16 * lane;
+        uint4 v = o + 16 <= len ? *(const uint4 *)(sec + o) : make_uint4(0, 0, 0, 0);
+        *(uint4 *)(ring + (o & (kRingBytes - 1))) = v;
+        rg.written += kChunkBytes;
+      }
+    }
+    __syncthreads();
+    uint32_t p = 0;
+    const uint32_t full = n_b / kRound;
+    uint8_t *outp = a.out + blk0 * E;
+    const uint8_t *rawp = raw_plane + blk0 * (E - 1);
+    uint32_t rawA[6] = {0, 0, 0, 0, 0, 0}, rawB[6] = {0, 0, 0, 0, 0, 0};
+    if (full > 0) load_raw_full<E>(rawp, kPerLane * lane, rawA);
+    uint32_t r = 0;
+    // full rounds, two per iteration with ping-pong raw registers: every
+    // load is issued a round before its use and no register is copied
+    for (; r + 2 <= full; r += 2) {
+      ring_maintain(rg, ring, sec, wb + 2 * p);
+      load_raw_full<E>(rawp, (r + 1) * kRound + kPerLane * lane, rawB);
+      uint32_t sym[2] = {0, 0};
+#pragma unroll
+      for (uint32_t t = 0; t < kPerLane; ++t)
+        sym[t >> 2] |= decode_step_ring<true>(x, true, lut, ring, wb, p, w_avail, bad) << (8 * (t & 3));
+      uint32_t w[NW];
+      merge_group<E>(sym, rawA, w);
+      store_words<E>(outp, r * kRound + kPerLane * lane, 8, w);
+
+      ring_maintain(rg, ring, sec, wb + 2 * p);
+      const uint32_t rn = (r + 2 < full) ? r + 2 : r + 1;  // always a full round: no branch around the load
+      load_raw_full<E>(rawp, rn * kRound + kPerLane * lane, rawA);
+      sym[0] = sym[1] = 0;
+#pragma unroll
+      for (uint32_t t = 0; t < kPerLane; ++t)
+        sym[t >> 2] |= decode_step_ring<true>(x, true, lut, ring, wb, p, w_avail, bad) << (8 * (t & 3));
+      merge_group<E>(sym, rawB, w);
+      store_words<E>(outp, (r + 1) * kRound + kPerLane * lane, 8, w);
+    }
+    if (r < full) {  // odd number of full rounds: rawA holds round r
+      ring_maintain(rg, ring, sec, wb + 2 * p);
+      uint32_t sym[2] = {0, 0};
+#pragma unroll
+      for (uint32_t t = 0; t < kPerLane; ++t)
+        sym[t >> 2] |= decode_step_ring<true>(x, true, lut, ring, wb, p, w_avail, bad) << (8 * (t & 3));
+      uint32_t w[NW];
+      merge_group<E>(sym, rawA, w);
+      store_words<E>(outp, r * kRound + kPerLane * lane, 8, w);
+      ++r;
+    }
+    if (r < rounds) {  // partial last round
+      ring_maintain(rg, ring, sec, wb + 2 * p);
+      const uint32_t i0 = r * kRound + kPerLane * lane;
+      const uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
+      uint32_t sym[2] = {0, 0};
+#pragma unroll
+      for (uint32_t t = 0; t < kPerLane; ++t)
+        sym[t >> 2] |= decode_step_ring<false>(x, t < valid, lut, ring, wb, p, w_avail, bad) << (8 * (t & 3));
+      if (valid > 0) {
+        uint32_t raw[6];
+        load_raw<E>(raw_plane, blk0 + i0, valid, raw);
+        uint32_t w[NW];
+        merge_group<E>(sym, raw, w);
+        store_words<E>(a.out, blk0 + i0, valid, w);
+      }
+    }
+    if (x != kStateLo) bad = true;
     if (__any(bad) && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
     __syncthreads();
   }
@@ -860,6 +1265,18 @@ __global__ void empty_stream_kernel(uint8_t *out, uint32_t dt, uint32_t block_el
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
+// encode_kernel instantiations: index = dt * 4 + reduce * 2 + small
+const void *encode_kernel_ptr(int k) {
+  static const void *const tab[12] = {
+      (const void *)encode_kernel<0, false, false>, (const void *)encode_kernel<0, false, true>,
+      (const void *)encode_kernel<0, true, false>,  (const void *)encode_kernel<0, true, false>,
+      (const void *)encode_kernel<1, false, false>, (const void *)encode_kernel<1, false, true>,
+      (const void *)encode_kernel<1, true, false>,  (const void *)encode_kernel<1, true, false>,
+      (const void *)encode_kernel<2, false, false>, (const void *)encode_kernel<2, false, true>,
+      (const void *)encode_kernel<2, true, false>,  (const void *)encode_kernel<2, true, false>};
+  return tab[k];
+}
+
 struct DeviceInfo {
   int cus = 0;
   bool gfx950 = false;
@@ -880,12 +1297,8 @@ uzip_status device_info(DeviceInfo &out) {
     g_info[dev].cus = prop.multiProcessorCount;
     g_info[dev].gfx950 = strncmp(prop.gcnArchName, "gfx950", 6) == 0;
     const int lds_max = 160 * 1024;
-    (void)hipFuncSetAttribute((const void *)encode_kernel<0, false>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
-    (void)hipFuncSetAttribute((const void *)encode_kernel<1, false>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
-    (void)hipFuncSetAttribute((const void *)encode_kernel<2, false>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
-    (void)hipFuncSetAttribute((const void *)encode_kernel<0, true>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
-    (void)hipFuncSetAttribute((const void *)encode_kernel<1, true>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
-    (void)hipFuncSetAttribute((const void *)encode_kernel<2, true>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
+    for (int k = 0; k < 12; ++k)
+      (void)hipFuncSetAttribute(encode_kernel_ptr(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
   });
   if (err != hipSuccess) return UZIP_EHIP;
   out = g_info[dev];
@@ -905,54 +1318,75 @@ uint64_t max_size(uint32_t E, uint64_t n, uint32_t block_elems) {
   return g.coded_off + full * pad16(block_elems) + (tail ? pad16(tail) : 0);
 }
 
-// LDS bytes of encode_kernel
-uint32_t encode_lds(uint32_t block_elems, uint32_t wcap, int n_in, uint32_t &pass2_off) {
-  uint32_t pass1 = kHistBytes + (n_in > 0 ? n_in * kLutBytes + 1024 : 0);
-  uint32_t pass2 = kStageHead + 2 * wcap + kStageTail;
-  pass2_off = kEncTableBytes;
-  uint32_t region = pass1 > pass2 ? pass1 : pass2;
-  (void)block_elems;
-  return kEncTableBytes + region;
+constexpr uint32_t kSmallMaxElems = kRegRounds * kRound;  // symbols fit the register store
+constexpr uint32_t kSmallStageWords = 7424;                // LDS staging words, small blocks
+constexpr uint32_t kMaxSlots = 2048;                        // persistent workgroups (small blocks)
+
+bool small_path(uint32_t block_elems) { return block_elems <= kSmallMaxElems; }
+uint32_t word_cap(uint32_t block_elems) { return block_elems / 2 + kRound + 8; }
+uint32_t stage_words(uint32_t block_elems) {
+  const uint32_t w = word_cap(block_elems);
+  return small_path(block_elems) && w > kSmallStageWords ? kSmallStageWords : w;
+}
+uint32_t slot_words(uint32_t block_elems) {
+  const uint32_t over = word_cap(block_elems) - stage_words(block_elems);
+  return (over + 127u) & ~127u;
+}
+uint64_t n_slots(uint64_t n_blocks, uint32_t block_elems) {
+  return small_path(block_elems) ? (n_blocks < kMaxSlots ? n_blocks : kMaxSlots) : 0;
 }
 
-uint32_t word_cap(uint32_t block_elems) { return block_elems / 2 + kRound + 8; }
+// LDS bytes of encode_kernel
+uint32_t encode_lds(uint32_t block_elems, int n_in, bool small) {
+  const uint32_t pass1 = kHistBytes + (n_in > 0 ? n_in * kLutBytes + 1024 : 0);
+  const uint32_t pass2 = kStageHead + 2 * (small ? stage_words(block_elems) : word_cap(block_elems)) + kStageTail;
+  return kEncTableBytes + (pass1 > pass2 ? pass1 : pass2);
+}
 
 struct EncodeWs {
-  uint64_t status_off, cnt_off, y_off, total;
+  uint64_t status_off, cnt_off, slot_off, y_off, total;
 };
 
-EncodeWs encode_ws(uint64_t n_blocks, uint64_t n_chunks, uint64_t ybytes) {
+// workspace: ticket + error word | look-back status per block | chunk
+// counters | overflow slots (small blocks) | reduced tensor (large-block
+// reduce without a caller buffer).  [0, slot_off) is cleared per call.
+EncodeWs encode_ws(uint64_t n_blocks, uint64_t n_chunks, uint32_t block_elems, uint64_t ybytes, bool reduce = false) {
   EncodeWs w;
   w.status_off = 256;
   w.cnt_off = pad256(w.status_off + 8 * n_blocks);
-  w.y_off = pad256(w.cnt_off + 8 * n_chunks);
+  w.slot_off = pad256(w.cnt_off + 8 * n_chunks);
+  w.y_off = pad256(w.slot_off + (reduce ? 0 : 2ull * n_slots(n_blocks, block_elems) * slot_words(block_elems)));
   w.total = pad256(w.y_off + ybytes);
   return w;
 }
 
 uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws, const EncodeWs &w,
-                          hipStream_t stream) {
+                          const DeviceInfo &info, hipStream_t stream) {
+  const bool small = !reduce && small_path(a.block_elems);
   a.ticket = (uint32_t *)ws;
   a.status = (uint64_t *)(ws + w.status_off);
   a.chunk_cnt = (uint32_t *)(ws + w.cnt_off);
+  a.slots = (uint16_t *)(ws + w.slot_off);
+  a.slot_words = slot_words(a.block_elems);
   a.wcap = word_cap(a.block_elems);
-  uint32_t lds = encode_lds(a.block_elems, a.wcap, reduce ? a.n_in : 0, a.pass2_off);
+  a.lds_words = small ? stage_words(a.block_elems) : a.wcap;
+  a.pass2_off = kEncTableBytes;
+  const uint32_t lds = encode_lds(a.block_elems, reduce ? a.n_in : 0, small);
   if (lds > 160 * 1024) return UZIP_EINVAL;
-  uint64_t clear_words = w.y_off / 4;
-  hipLaunchKernelGGL(clear_kernel, dim3((unsigned)((clear_words + 255) / 256 < 4096 ? (clear_words + 255) / 256 : 4096)),
-                     dim3(256), 0, stream, (uint32_t *)ws, clear_words);
+  const void *fn = encode_kernel_ptr((int)dt * 4 + (reduce ? 2 : 0) + (small ? 1 : 0));
+  int occ = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, 64, lds) != hipSuccess || occ < 1) occ = 1;
+  uint64_t grid = (uint64_t)info.cus * (uint64_t)occ;
+  if (grid > a.n_blocks) grid = a.n_blocks;
+  if (small && grid > n_slots(a.n_blocks, a.block_elems)) grid = n_slots(a.n_blocks, a.block_elems);
+  if (grid == 0) grid = 1;
+  const uint64_t clear_words = w.slot_off / 4;
+  const uint64_t cgrid = (clear_words + 255) / 256 < 4096 ? (clear_words + 255) / 256 : 4096;
+  hipLaunchKernelGGL(clear_kernel, dim3((unsigned)cgrid), dim3(256), 0, stream, (uint32_t *)ws, clear_words);
   if (hipGetLastError() != hipSuccess) return UZIP_EHIP;
-  dim3 grid(a.n_blocks), block(64);
-  if (!reduce) {
-    if (dt == UZIP_BF16) hipLaunchKernelGGL((encode_kernel<0, false>), grid, block, lds, stream, a);
-    if (dt == UZIP_FP16) hipLaunchKernelGGL((encode_kernel<1, false>), grid, block, lds, stream, a);
-    if (dt == UZIP_FP32) hipLaunchKernelGGL((encode_kernel<2, false>), grid, block, lds, stream, a);
-  } else {
-    if (dt == UZIP_BF16) hipLaunchKernelGGL((encode_kernel<0, true>), grid, block, lds, stream, a);
-    if (dt == UZIP_FP16) hipLaunchKernelGGL((encode_kernel<1, true>), grid, block, lds, stream, a);
-    if (dt == UZIP_FP32) hipLaunchKernelGGL((encode_kernel<2, true>), grid, block, lds, stream, a);
-  }
-  return hipGetLastError() == hipSuccess ? UZIP_OK : UZIP_EHIP;
+  void *args[] = {&a};
+  if (hipLaunchKernel(fn, dim3((unsigned)grid), dim3(64), args, lds, stream) != hipSuccess) return UZIP_EHIP;
+  return UZIP_OK;
 }
 
 }  // namespace
@@ -970,20 +1404,20 @@ size_t uzip_workspace_size(int op, uzip_dtype dtype, uint64_t n_elems, uint32_t 
   const uint64_t nb = (n_elems + be - 1) / be;
   switch (op) {
     case UZIP_OP_COMPRESS:
-      return (size_t)encode_ws(nb, 1, 0).total;
+      return (size_t)encode_ws(nb, 1, be, 0).total;
     case UZIP_OP_DECOMPRESS:
       return 0;
     case UZIP_OP_CHUNKED: {
       if (aux == 0 || aux % block_bytes) return 0;
       const uint64_t ce = aux / E;
       const uint64_t chunks = (n_elems + ce - 1) / ce;
-      return (size_t)encode_ws(chunks * (ce / be), chunks, 0).total;
+      return (size_t)encode_ws(chunks * (ce / be), chunks, be, 0).total;
     }
     case UZIP_OP_REDUCE: {
       const uint64_t n_in = aux & 0xFFFFu;
       if (n_in < 1 || n_in > kMaxInputs) return 0;
       const uint64_t y = (aux & UZIP_WS_NO_OUT_RAW) ? n_elems * E : 0;
-      return (size_t)encode_ws(nb, 1, y).total;
+      return (size_t)encode_ws(nb, 1, be, y, true).total;
     }
     default:
       return 0;
@@ -1008,7 +1442,7 @@ uzip_status uzip_compress(const void *d_in, uint64_t n_elems, uzip_dtype dtype, 
                        d_out_size);
     return hipGetLastError() == hipSuccess ? UZIP_OK : UZIP_EHIP;
   }
-  EncodeWs w = encode_ws(nb, 1, 0);
+  EncodeWs w = encode_ws(nb, 1, be, 0);
   if (d_ws == nullptr || !aligned16(d_ws) || ws_bytes < w.total) return UZIP_ENOSPC;
   EncodeArgs a;
   memset(&a, 0, sizeof(a));
@@ -1021,7 +1455,7 @@ uzip_status uzip_compress(const void *d_in, uint64_t n_elems, uzip_dtype dtype, 
   a.out = (uint8_t *)d_out;
   a.slot_bytes = 0;
   a.sizes = d_out_size;
-  return launch_encode(a, dtype, false, (uint8_t *)d_ws, w, stream);
+  return launch_encode(a, dtype, false, (uint8_t *)d_ws, w, info, stream);
 }
 
 uzip_status uzip_compress_chunked(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint32_t block_bytes,
@@ -1044,7 +1478,7 @@ uzip_status uzip_compress_chunked(const void *d_in, uint64_t n_elems, uzip_dtype
   DeviceInfo info;
   uzip_status st = device_info(info);
   if (st != UZIP_OK) return st;
-  EncodeWs w = encode_ws(chunks * (ce / be), chunks, 0);
+  EncodeWs w = encode_ws(chunks * (ce / be), chunks, be, 0);
   if (d_ws == nullptr || !aligned16(d_ws) || ws_bytes < w.total) return UZIP_ENOSPC;
   EncodeArgs a;
   memset(&a, 0, sizeof(a));
@@ -1059,7 +1493,7 @@ uzip_status uzip_compress_chunked(const void *d_in, uint64_t n_elems, uzip_dtype
   a.sizes = chunk_sizes;
   a.flags = flags;
   a.epoch = epoch;
-  return launch_encode(a, dtype, false, (uint8_t *)d_ws, w, stream);
+  return launch_encode(a, dtype, false, (uint8_t *)d_ws, w, info, stream);
 }
 
 uzip_status uzip_decompress(const void *d_in, size_t in_bytes, uzip_dtype dtype, uint64_t n_elems, void *d_out,
@@ -1112,7 +1546,8 @@ uzip_status uzip_reduce_fused(const void *const *d_in, const size_t *in_bytes, i
                        d_out_size);
     return hipGetLastError() == hipSuccess ? UZIP_OK : UZIP_EHIP;
   }
-  EncodeWs w = encode_ws(nb, 1, d_out_raw ? 0 : n_elems * E);
+  const bool need_y = d_out_raw == nullptr;
+  EncodeWs w = encode_ws(nb, 1, be, need_y ? n_elems * E : 0, true);
   if (d_ws == nullptr || !aligned16(d_ws) || ws_bytes < w.total) return UZIP_ENOSPC;
   EncodeArgs a;
   memset(&a, 0, sizeof(a));
@@ -1129,9 +1564,10 @@ uzip_status uzip_reduce_fused(const void *const *d_in, const size_t *in_bytes, i
     a.in_bytes[i] = in_bytes[i];
   }
   a.local_raw = (const uint8_t *)d_local_raw;
-  a.ybuf = d_out_raw ? (uint8_t *)d_out_raw : (uint8_t *)d_ws + w.y_off;
+  a.yout = (uint8_t *)d_out_raw;
+  a.ybuf = d_out_raw ? (uint8_t *)d_out_raw : (need_y ? (uint8_t *)d_ws + w.y_off : nullptr);
   a.dstatus = d_status;
-  return launch_encode(a, dtype, true, (uint8_t *)d_ws, w, stream);
+  return launch_encode(a, dtype, true, (uint8_t *)d_ws, w, info, stream);
 }
 
 const char *uzip_status_str(uzip_status status) {

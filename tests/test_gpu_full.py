@@ -1,0 +1,135 @@
+"""GPU parity at the full sizes of the five measured configurations.
+
+Every stream the GPU writes is compared byte for byte with the CPU oracle's
+stream for the same seeded input (whole streams: the oracle compresses a
+GiB in seconds), and every stream is decoded on the GPU back to the input.
+The launch configuration is the one bench.py times (the same entry points
+and block/chunk sizes).
+"""
+import sys
+import time
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import ref
+import workloads as W
+
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
+
+EB = {"bf16": 2, "fp16": 2, "fp32": 4}
+NP_BITS = {"bf16": np.int16, "fp16": np.int16, "fp32": np.int32}
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def uz():
+    import paper_2604_17172_amd as m
+    return m
+
+
+def to_dev(x, dtype):
+    return torch.from_numpy(np.ascontiguousarray(x).view(NP_BITS[dtype])).cuda()
+
+
+def first_diff(a, b):
+    n = min(a.size, b.size)
+    d = np.nonzero(a[:n] != b[:n])[0]
+    return int(d[0]) if d.size else n
+
+
+def check_whole(uz, x, dtype, bb, label):
+    say(f"[full] {label}: dtype={dtype} n={x.size} block={bb}")
+    t0 = time.time()
+    want = ref.compress(x, dtype, bb)
+    say(f"[full] {label}: oracle {time.time() - t0:.1f}s, ratio {want.size / (EB[dtype] * x.size):.4f}")
+    xt = to_dev(x, dtype)
+    out, size = uz.compress(xt, bb, dtype=dtype)
+    torch.cuda.synchronize()
+    got = out[:int(size.item())].cpu().numpy()
+    assert got.size == want.size and np.array_equal(got, want), \
+        f"{label}: stream differs (sizes {got.size}/{want.size}, first diff at {first_diff(got, want)})"
+    y, status = uz.decompress(out, dtype, x.size)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    assert torch.equal(y, xt), f"{label}: round trip not lossless"
+
+
+def check_chunked(uz, x, dtype, bb, cb, label):
+    say(f"[full] {label}: chunked dtype={dtype} n={x.size} block={bb} chunk={cb}")
+    xt = to_dev(x, dtype)
+    flags = torch.zeros(2 * ((x.size * EB[dtype] + cb - 1) // cb), dtype=torch.int32).pin_memory()
+    out, slot, sizes, _ = uz.compress_chunked(xt, bb, cb, dtype=dtype, epoch=11, flags=flags)
+    torch.cuda.synchronize()
+    assert bool((flags == 11).all())
+    buf = out.cpu().numpy()
+    sz = sizes.cpu().numpy()
+    ce = cb // EB[dtype]
+    t0 = time.time()
+    for c in range(sz.size):
+        w = ref.compress(x[c * ce:(c + 1) * ce], dtype, bb)
+        assert sz[c] == w.size, f"{label}: chunk {c} size {sz[c]} != {w.size}"
+        assert np.array_equal(buf[c * slot:c * slot + w.size], w), f"{label}: chunk {c} differs"
+    say(f"[full] {label}: {sz.size} chunks equal to the oracle ({time.time() - t0:.1f}s)")
+    # every chunk decodes back to its slice
+    y = torch.empty_like(xt)
+    for c in range(sz.size):
+        n_c = min(ce, x.size - c * ce)
+        yc, st = uz.decompress(out[c * slot:(c + 1) * slot], dtype, n_c, out=y[c * ce:c * ce + n_c])
+        assert int(st.item()) == 0
+    torch.cuda.synchronize()
+    assert torch.equal(y, xt)
+
+
+def test_normal_bf16_4MiB(uz):
+    check_whole(uz, W.normal_bf16(), "bf16", 65536, "normal_bf16_4MiB")
+
+
+def test_weight_sync_1GiB_whole_stream(uz):
+    check_whole(uz, W.weight_sync(), "bf16", 65536, "weight_sync_bf16_1GiB")
+
+
+def test_weight_sync_1GiB_split_send_producer(uz):
+    check_chunked(uz, W.weight_sync(), "bf16", 65536, 4 << 20, "weight_sync_bf16_1GiB")
+
+
+def test_grad_fp32_1GiB(uz):
+    check_whole(uz, W.grad_fp32(), "fp32", 262144, "grad_fp32_1GiB")
+
+
+def test_grad_fp16_512MiB(uz):
+    check_whole(uz, W.grad_fp16(), "fp16", 262144, "grad_fp16_512MiB")
+
+
+def test_kv_cache_2GiB_chunked(uz):
+    check_chunked(uz, W.kv_cache(), "bf16", 65536, 1 << 20, "kv_cache_bf16_2GiB")
+
+
+def test_reduce_8x16MiB(uz):
+    xs = W.reduce_slices()
+    n = xs[0].size
+    say(f"[full] reduce_8x_bf16_16MiB: n={n}")
+    t0 = time.time()
+    streams = [ref.compress(v, "bf16", 65536) for v in xs]
+    want_s, want_y = ref.reduce(streams, "bf16", n, 65536)
+    say(f"[full] reduce oracle {time.time() - t0:.1f}s")
+    dstreams = [torch.from_numpy(s).cuda() for s in streams]
+    out, size, raw, status = uz.reduce_fused(dstreams, "bf16", n, 65536)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    got = out[:int(size.item())].cpu().numpy()
+    assert np.array_equal(got, want_s), f"reduce stream differs at {first_diff(got, want_s)}"
+    assert np.array_equal(raw.cpu().numpy().view(np.uint16), want_y)
+    # the GPU's own compressed shares give the same result
+    gstreams = []
+    for v in xs:
+        o, sz = uz.compress(to_dev(v, "bf16"), 65536, dtype="bf16")
+        gstreams.append(o[:int(sz.item())].clone())
+    out2, size2, _, st2 = uz.reduce_fused(gstreams, "bf16", n, 65536, want_raw=False)
+    torch.cuda.synchronize()
+    assert int(st2.item()) == 0 and np.array_equal(out2[:int(size2.item())].cpu().numpy(), want_s)

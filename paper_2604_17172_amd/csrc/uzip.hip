@@ -39,6 +39,7 @@ using namespace uzip;
 namespace {
 
 constexpr int kMaxInputs = 16;
+constexpr uint32_t kTrashBytes = 256;  // encoder: one 4-byte slot per lane for non-emitted words
 constexpr uint32_t kMinBlockBytes = 4096, kMaxBlockBytes = 262144;
 
 struct EncodeArgs {
@@ -464,32 +465,66 @@ __device__ __forceinline__ void shift_up(SymRegs &S) {
 
 // One encoder sub-step of every lane (rANS coding function with 16-bit
 // renormalisation).  Emitted words go to virtual staging index
-// pos - cnt + rank: index v >= lo lives in LDS at lds[v - lo], smaller
-// indices in the workgroup's overflow slot in global memory.
-template <bool OVF, bool FULL>
-__device__ __forceinline__ void enc_step(uint32_t &x, const uint4 e, bool valid, uint32_t &pos, uint16_t *lds,
-                                         uint16_t *ovf, uint32_t lo) {
+// pos - cnt + rank, compacted across the wave with ballot + mbcnt.
+//
+// enc_step_lds: the whole step lands in the LDS staging area (index v lives
+// at lds[v - lo]); branch-free: every lane stores, lanes that emit nothing
+// store into their own trash slot.
+template <bool FULL>
+__device__ __forceinline__ void enc_step_lds(uint32_t &x, const uint4 e, bool valid, uint32_t &pos,
+                                             __attribute__((address_space(3))) uint16_t *lds_rel,
+                                             __attribute__((address_space(3))) uint16_t *trash) {
   const bool emit = (FULL || valid) && x >= e.y;
   const uint64_t m = __ballot(emit);
-  const uint32_t cnt = (uint32_t)__popcll(m);
-  const uint32_t base = pos - cnt;
-  if (!OVF || base >= lo) {
-    if (emit) {
-      lds[base - lo + mbcnt(m)] = (uint16_t)x;
-      x >>= 16;
-    }
-  } else if (emit) {
+  const uint32_t base = pos - (uint32_t)__popcll(m);
+  const uint32_t v = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, base));
+  __attribute__((address_space(3))) uint16_t *dst = emit ? lds_rel + v : trash;
+  *dst = (uint16_t)x;
+  x = emit ? x >> 16 : x;
+  pos = base;
+  if (FULL || valid) {
+    const uint32_t q = __umulhi(x, e.x) >> (e.z >> 24);
+    x = x + __umul24(q, e.z) + e.w;
+  }
+}
+
+// enc_step_ovf: a step that may reach below the LDS part; indices below lo
+// go to the workgroup's overflow slot in global memory.
+template <bool FULL>
+__device__ __forceinline__ void enc_step_ovf(uint32_t &x, const uint4 e, bool valid, uint32_t &pos,
+                                          __attribute__((address_space(3))) uint16_t *lds_rel, uint16_t *ovf,
+                                          uint32_t lo) {
+  const bool emit = (FULL || valid) && x >= e.y;
+  const uint64_t m = __ballot(emit);
+  const uint32_t base = pos - (uint32_t)__popcll(m);
+  if (emit) {
     const uint32_t v = base + mbcnt(m);
     if (v >= lo)
-      lds[v - lo] = (uint16_t)x;
+      lds_rel[v] = (uint16_t)x;
     else
-      ovf[v] = (uint16_t)x;
+      __builtin_nontemporal_store((uint16_t)x, ovf + v);
     x >>= 16;
   }
   pos = base;
   if (FULL || valid) {
     const uint32_t q = __umulhi(x, e.x) >> (e.z >> 24);
     x = x + __umul24(q, e.z) + e.w;
+  }
+}
+
+// One round of 8 sub-steps, backwards; picks the LDS-only form when even 512
+// emitted words cannot reach the overflow part.
+template <bool OVF, bool FULL>
+__device__ __forceinline__ void enc_round(uint32_t &x, const uint4 (&e)[8], uint32_t valid, uint32_t &pos,
+                                          __attribute__((address_space(3))) uint16_t *lds_rel,
+                                          __attribute__((address_space(3))) uint16_t *trash, uint16_t *ovf,
+                                          uint32_t lo) {
+  if (!OVF || pos >= lo + kRound) {
+#pragma unroll
+    for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step_lds<FULL>(x, e[tt], (uint32_t)tt < valid, pos, lds_rel, trash);
+  } else {
+#pragma unroll
+    for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step_ovf<FULL>(x, e[tt], (uint32_t)tt < valid, pos, lds_rel, ovf, lo);
   }
 }
 
@@ -529,11 +564,12 @@ __device__ __forceinline__ void hist_add8(uint32_t *h, const Group &g, uint32_t 
 //   and LDS holds the whole staging area.
 // ---------------------------------------------------------------------------
 template <int DT, bool REDUCE, bool SMALL>
-__global__ void __launch_bounds__(64) encode_kernel(EncodeArgs a) {
+__device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   constexpr int E = (DT == 2) ? 4 : 2;
   constexpr int NW = 4 * (E / 2);
-  constexpr int D = 4;  // pass-1 load pipeline depth (rounds)
-  extern __shared__ __align__(16) uint8_t smem[];
+  constexpr int D = (E == 2) ? 8 : 4;  // pass-1 load pipeline depth (rounds)
+  extern __shared__ __align__(16) uint8_t smem_base[];
+  uint8_t *smem = smem_base + kTrashBytes;  // [trash | encoder table | histogram / staging]
   uint4 *enc = (uint4 *)smem;
   uint32_t *hist = (uint32_t *)(smem + kEncTableBytes);
   uint8_t *stage = smem + a.pass2_off;
@@ -541,6 +577,11 @@ __global__ void __launch_bounds__(64) encode_kernel(EncodeArgs a) {
   const uint32_t lane = lane_id();
   uint16_t *ovf = SMALL ? a.slots + (uint64_t)blockIdx.x * a.slot_words : nullptr;
   const uint32_t lo = SMALL ? a.wcap - a.lds_words : 0;  // virtual index of stage16[0]
+  typedef __attribute__((address_space(3))) uint16_t lds16_t;
+  // LDS pointer such that lds_rel[v] is virtual staging index v (v >= lo)
+  lds16_t *lds_rel = (lds16_t *)(stage16) - lo;
+  // one private 4-byte slot per lane for words that are not emitted
+  lds16_t *trash = (lds16_t *)smem_base + 2 * lane;
 
   while (true) {
     uint32_t b = 0;
@@ -819,8 +860,7 @@ __global__ void __launch_bounds__(64) encode_kernel(EncodeArgs a) {
       uint4 e[8];
 #pragma unroll
       for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(sy, tt)];
-#pragma unroll
-      for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step<SMALL, false>(x, e[tt], (uint32_t)tt < valid, pos, stage16, ovf, lo);
+      enc_round<SMALL, false>(x, e, valid, pos, lds_rel, trash, ovf, lo);
       if (a.wcap - pos >= limit_words) stored = true;
     }
     if constexpr (SMALL) {
@@ -835,8 +875,7 @@ __global__ void __launch_bounds__(64) encode_kernel(EncodeArgs a) {
             for (int tt = 0; tt < 4; ++tt) e[tt] = enc[(s0 >> (8 * tt)) & 0xFFu];
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) e[4 + tt] = enc[(s1 >> (8 * tt)) & 0xFFu];
-#pragma unroll
-            for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step<true, true>(x, e[tt], true, pos, stage16, ovf, lo);
+            enc_round<true, true>(x, e, 8, pos, lds_rel, trash, ovf, lo);
             if (a.wcap - pos >= limit_words) stored = true;
           }
         }
@@ -854,8 +893,7 @@ __global__ void __launch_bounds__(64) encode_kernel(EncodeArgs a) {
         uint4 e[8];
 #pragma unroll
         for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
-#pragma unroll
-        for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step<false, true>(x, e[tt], true, pos, stage16, ovf, lo);
+        enc_round<false, true>(x, e, 8, pos, lds_rel, trash, ovf, lo);
         if (a.wcap - pos >= limit_words) stored = true;
         if (stored) break;
         const uint32_t rn = r >= 2 ? (uint32_t)(r - 2) : 0u;
@@ -863,8 +901,7 @@ __global__ void __launch_bounds__(64) encode_kernel(EncodeArgs a) {
         split_group<E>(wbuf, gr);
 #pragma unroll
         for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
-#pragma unroll
-        for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step<false, true>(x, e[tt], true, pos, stage16, ovf, lo);
+        enc_round<false, true>(x, e, 8, pos, lds_rel, trash, ovf, lo);
         if (a.wcap - pos >= limit_words) stored = true;
       }
       if (r == 0 && !stored) {  // wa holds round 0
@@ -873,8 +910,7 @@ __global__ void __launch_bounds__(64) encode_kernel(EncodeArgs a) {
         uint4 e[8];
 #pragma unroll
         for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
-#pragma unroll
-        for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step<false, true>(x, e[tt], true, pos, stage16, ovf, lo);
+        enc_round<false, true>(x, e, 8, pos, lds_rel, trash, ovf, lo);
         if (a.wcap - pos >= limit_words) stored = true;
       }
     }
@@ -1013,6 +1049,17 @@ __global__ void __launch_bounds__(64) encode_kernel(EncodeArgs a) {
     }
     __syncthreads();
   }
+}
+
+// Compress kernels keep two waves per SIMD (the LDS budget allows eight
+// workgroups per CU); the fused reduce holds many more per-input states.
+template <int DT, bool REDUCE, bool SMALL>
+__global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) encode_kernel(EncodeArgs a) {
+  encode_body<DT, false, SMALL>(a);
+}
+template <int DT>
+__global__ void __launch_bounds__(64) reduce_kernel(EncodeArgs a) {
+  encode_body<DT, true, false>(a);
 }
 
 // ---------------------------------------------------------------------------
@@ -1269,11 +1316,11 @@ __global__ void empty_stream_kernel(uint8_t *out, uint32_t dt, uint32_t block_el
 const void *encode_kernel_ptr(int k) {
   static const void *const tab[12] = {
       (const void *)encode_kernel<0, false, false>, (const void *)encode_kernel<0, false, true>,
-      (const void *)encode_kernel<0, true, false>,  (const void *)encode_kernel<0, true, false>,
+      (const void *)reduce_kernel<0>,               (const void *)reduce_kernel<0>,
       (const void *)encode_kernel<1, false, false>, (const void *)encode_kernel<1, false, true>,
-      (const void *)encode_kernel<1, true, false>,  (const void *)encode_kernel<1, true, false>,
+      (const void *)reduce_kernel<1>,               (const void *)reduce_kernel<1>,
       (const void *)encode_kernel<2, false, false>, (const void *)encode_kernel<2, false, true>,
-      (const void *)encode_kernel<2, true, false>,  (const void *)encode_kernel<2, true, false>};
+      (const void *)reduce_kernel<2>,               (const void *)reduce_kernel<2>};
   return tab[k];
 }
 
@@ -1340,7 +1387,7 @@ uint64_t n_slots(uint64_t n_blocks, uint32_t block_elems) {
 uint32_t encode_lds(uint32_t block_elems, int n_in, bool small) {
   const uint32_t pass1 = kHistBytes + (n_in > 0 ? n_in * kLutBytes + 1024 : 0);
   const uint32_t pass2 = kStageHead + 2 * (small ? stage_words(block_elems) : word_cap(block_elems)) + kStageTail;
-  return kEncTableBytes + (pass1 > pass2 ? pass1 : pass2);
+  return kTrashBytes + kEncTableBytes + (pass1 > pass2 ? pass1 : pass2);
 }
 
 struct EncodeWs {

@@ -488,44 +488,22 @@ __device__ __forceinline__ void enc_step_lds(uint32_t &x, const uint4 e, bool va
   }
 }
 
-// enc_step_ovf: a step that may reach below the LDS part; indices below lo
-// go to the workgroup's overflow slot in global memory.
+// One round of 8 sub-steps, backwards.
 template <bool FULL>
-__device__ __forceinline__ void enc_step_ovf(uint32_t &x, const uint4 e, bool valid, uint32_t &pos,
-                                          __attribute__((address_space(3))) uint16_t *lds_rel, uint16_t *ovf,
-                                          uint32_t lo) {
-  const bool emit = (FULL || valid) && x >= e.y;
-  const uint64_t m = __ballot(emit);
-  const uint32_t base = pos - (uint32_t)__popcll(m);
-  if (emit) {
-    const uint32_t v = base + mbcnt(m);
-    if (v >= lo)
-      lds_rel[v] = (uint16_t)x;
-    else
-      __builtin_nontemporal_store((uint16_t)x, ovf + v);
-    x >>= 16;
-  }
-  pos = base;
-  if (FULL || valid) {
-    const uint32_t q = __umulhi(x, e.x) >> (e.z >> 24);
-    x = x + __umul24(q, e.z) + e.w;
-  }
-}
-
-// One round of 8 sub-steps, backwards; picks the LDS-only form when even 512
-// emitted words cannot reach the overflow part.
-template <bool OVF, bool FULL>
 __device__ __forceinline__ void enc_round(uint32_t &x, const uint4 (&e)[8], uint32_t valid, uint32_t &pos,
                                           __attribute__((address_space(3))) uint16_t *lds_rel,
-                                          __attribute__((address_space(3))) uint16_t *trash, uint16_t *ovf,
-                                          uint32_t lo) {
-  if (!OVF || pos >= lo + kRound) {
+                                          __attribute__((address_space(3))) uint16_t *trash) {
 #pragma unroll
-    for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step_lds<FULL>(x, e[tt], (uint32_t)tt < valid, pos, lds_rel, trash);
-  } else {
-#pragma unroll
-    for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step_ovf<FULL>(x, e[tt], (uint32_t)tt < valid, pos, lds_rel, ovf, lo);
-  }
+  for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step_lds<FULL>(x, e[tt], (uint32_t)tt < valid, pos, lds_rel, trash);
+}
+
+// The LDS staging window holds virtual indices [lo, lo + cap).  Before a
+// round that could write below it, move the words written so far,
+// [pos, lo + cap), to the same indices of the workgroup's overflow slot in
+// global memory and slide the window down to end at pos.
+__device__ __forceinline__ void spill_window(const __attribute__((address_space(3))) uint16_t *lds_rel, uint16_t *ovf,
+                                          uint32_t pos, uint32_t top) {
+  for (uint32_t v = pos + lane_id(); v < top; v += 64) __builtin_nontemporal_store(lds_rel[v], ovf + v);
 }
 
 template <int E>
@@ -576,10 +554,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   uint16_t *stage16 = (uint16_t *)(stage + kStageHead);
   const uint32_t lane = lane_id();
   uint16_t *ovf = SMALL ? a.slots + (uint64_t)blockIdx.x * a.slot_words : nullptr;
-  const uint32_t lo = SMALL ? a.wcap - a.lds_words : 0;  // virtual index of stage16[0]
   typedef __attribute__((address_space(3))) uint16_t lds16_t;
-  // LDS pointer such that lds_rel[v] is virtual staging index v (v >= lo)
-  lds16_t *lds_rel = (lds16_t *)(stage16) - lo;
   // one private 4-byte slot per lane for words that are not emitted
   lds16_t *trash = (lds16_t *)smem_base + 2 * lane;
 
@@ -650,14 +625,11 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
               S.v3[2 * rr + 1] = gr.sym[1];
               store_raw_full<E>(raw_plane, blk0 + r * kRound + kPerLane * lane, gr);
               hist_add8(h, gr, 8);
-            } else if (r == full && full < rounds) {
-              partial_round();
-              S.v3[2 * rr] = psym0;
-              S.v3[2 * rr + 1] = psym1;
             }
           }
           if (gi < 3) shift_down(S);
         }
+        if (full < rounds) partial_round();  // its symbols stay in psym0/psym1
       } else {
         if (full > 0) {
           uint32_t r = 0;
@@ -839,9 +811,13 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
 
     // ---- pass 2: rANS over the block, backwards; words staged ----
     for (uint32_t i = lane; i < kStageTail / 4; i += 64)
-      ((uint32_t *)(stage + kStageHead + 2 * (a.wcap - lo)))[i] = 0;
+      ((uint32_t *)(stage + kStageHead + 2 * a.lds_words))[i] = 0;
     const uint32_t limit_words = (n_b > kSectionFixed + 2 * t.k) ? (n_b - kSectionFixed - 2 * t.k + 1) / 2 : 0;
     uint32_t pos = a.wcap;  // virtual staging indices [pos, wcap) hold the words written so far
+    // LDS window over virtual indices [lo, lo + lds_words); lds_rel[v] is index v
+    uint32_t lo = a.wcap - a.lds_words;
+    lds16_t *lds_rel = (lds16_t *)stage16 - lo;
+    uint32_t spilled = a.wcap;  // indices [spilled, wcap) live in the overflow slot
     uint32_t x = kStateLo;
     bool stored = (limit_words == 0);
     if (full < rounds && !stored) {  // the partial last round comes first
@@ -860,7 +836,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
       uint4 e[8];
 #pragma unroll
       for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(sy, tt)];
-      enc_round<SMALL, false>(x, e, valid, pos, lds_rel, trash, ovf, lo);
+      enc_round<false>(x, e, valid, pos, lds_rel, trash);
       if (a.wcap - pos >= limit_words) stored = true;
     }
     if constexpr (SMALL) {
@@ -869,13 +845,19 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         for (int rr = 15; rr >= 0; --rr) {
           const int r = 16 * gi + rr;
           if (r < (int)full && !stored) {
+            if (pos < lo + kRound) {  // rare: slide the LDS window down
+              spill_window(lds_rel, ovf, pos, spilled);
+              spilled = pos;
+              lo = pos > a.lds_words ? pos - a.lds_words : 0;
+              lds_rel = (lds16_t *)stage16 - lo;
+            }
             const uint32_t s0 = S.v3[2 * rr], s1 = S.v3[2 * rr + 1];
             uint4 e[8];
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) e[tt] = enc[(s0 >> (8 * tt)) & 0xFFu];
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) e[4 + tt] = enc[(s1 >> (8 * tt)) & 0xFFu];
-            enc_round<true, true>(x, e, 8, pos, lds_rel, trash, ovf, lo);
+            enc_round<true>(x, e, 8, pos, lds_rel, trash);
             if (a.wcap - pos >= limit_words) stored = true;
           }
         }
@@ -893,7 +875,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         uint4 e[8];
 #pragma unroll
         for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
-        enc_round<false, true>(x, e, 8, pos, lds_rel, trash, ovf, lo);
+        enc_round<true>(x, e, 8, pos, lds_rel, trash);
         if (a.wcap - pos >= limit_words) stored = true;
         if (stored) break;
         const uint32_t rn = r >= 2 ? (uint32_t)(r - 2) : 0u;
@@ -901,7 +883,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         split_group<E>(wbuf, gr);
 #pragma unroll
         for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
-        enc_round<false, true>(x, e, 8, pos, lds_rel, trash, ovf, lo);
+        enc_round<true>(x, e, 8, pos, lds_rel, trash);
         if (a.wcap - pos >= limit_words) stored = true;
       }
       if (r == 0 && !stored) {  // wa holds round 0
@@ -910,7 +892,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         uint4 e[8];
 #pragma unroll
         for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
-        enc_round<false, true>(x, e, 8, pos, lds_rel, trash, ovf, lo);
+        enc_round<true>(x, e, 8, pos, lds_rel, trash);
         if (a.wcap - pos >= limit_words) stored = true;
       }
     }
@@ -944,7 +926,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         for (int q = 0; q < 4; ++q)
           if (t.f[q]) h16[144 + rk++] = (uint16_t)t.f[q];
       };
-      if (!SMALL || pos >= lo) {
+      if (!SMALL || spilled == a.wcap) {
         // the whole image is contiguous in LDS: header right before the words
         const uint32_t A = kStageHead + 2 * (pos - lo) - hdr;
         put_header((uint16_t *)(stage + A));
@@ -961,8 +943,9 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
           ((uint4 *)sec)[u] = o;
         }
       } else {
-        // rare: words spilled to the overflow slot; gather header (LDS),
-        // spilled words (global, read back coherently) and LDS words
+        // rare: words [spilled, wcap) went to the overflow slot; gather the
+        // header (LDS), the LDS words [pos, spilled) and the spilled words
+        // (global, read back with device-coherent loads)
         put_header((uint16_t *)stage);
         __threadfence_block();
         __syncthreads();
@@ -976,7 +959,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
               v16 = ((const uint16_t *)stage)[ob / 2];
             } else if ((ob - hdr) / 2 < n_words) {
               const uint32_t v = pos + (ob - hdr) / 2;
-              if (v >= lo) {
+              if (v < spilled) {
                 v16 = stage16[v - lo];
               } else {
                 const uint32_t dw = __hip_atomic_load((const uint32_t *)ovf + (v >> 1), __ATOMIC_RELAXED,
@@ -1375,10 +1358,7 @@ uint32_t stage_words(uint32_t block_elems) {
   const uint32_t w = word_cap(block_elems);
   return small_path(block_elems) && w > kSmallStageWords ? kSmallStageWords : w;
 }
-uint32_t slot_words(uint32_t block_elems) {
-  const uint32_t over = word_cap(block_elems) - stage_words(block_elems);
-  return (over + 127u) & ~127u;
-}
+uint32_t slot_words(uint32_t block_elems) { return (word_cap(block_elems) + 127u) & ~127u; }
 uint64_t n_slots(uint64_t n_blocks, uint32_t block_elems) {
   return small_path(block_elems) ? (n_blocks < kMaxSlots ? n_blocks : kMaxSlots) : 0;
 }

@@ -284,3 +284,20 @@ def test_reduce_rejects_mismatched_inputs(uz):
     out, size, raw, status = uz.reduce_fused([dev(s1), dev(s2)], "bf16", 50_000, 65536)
     torch.cuda.synchronize()
     assert int(status.item()) == uz.ECORRUPT
+
+
+@pytest.mark.parametrize("dtype,spread", [("bf16", 64), ("bf16", 200), ("fp16", 30)])
+def test_high_entropy_blocks_spill_staging(uz, dtype, spread):
+    """Exponents spread over many values: a 64 KiB block codes to more words
+    than the encoder's LDS staging window holds (it spills to the
+    workgroup's overflow slot) while the block still stays CODED (spread 64)
+    or turns STORED part way (spread 200)."""
+    rng = np.random.default_rng(spread)
+    n = 5 * 32768 + 999
+    if dtype == "bf16":
+        e = rng.integers(127 - spread // 2, 127 + spread // 2, n)
+        x = ((e << 7) | rng.integers(0, 128, n) | (rng.integers(0, 2, n) << 15)).astype(np.uint16)
+    else:
+        e = rng.integers(1, spread + 1, n)
+        x = ((e << 10) | rng.integers(0, 1024, n) | (rng.integers(0, 2, n) << 15)).astype(np.uint16)
+    check_roundtrip(uz, x, dtype, 65536, f"spread {spread}")

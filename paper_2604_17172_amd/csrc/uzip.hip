@@ -517,6 +517,30 @@ __device__ __forceinline__ void load_full(const uint8_t *base, uint64_t first, u
   }
 }
 
+// Full groups addressed as a wave-uniform round base (kept in scalar
+// registers) plus a 32-bit lane offset: round r of a block starts at
+// elements blk0 + 512 r; lane j owns 16 (E = 2) or 32 (E = 4) bytes of it.
+template <int E>
+__device__ __forceinline__ void load_round(const uint8_t *round_base, uint32_t w[4 * (E / 2)]) {
+  const uint4 *p = (const uint4 *)round_base + (E / 2) * lane_id();
+  uint4 a = p[0];
+  w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
+  if (E == 4) {
+    uint4 b = p[1];
+    w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
+  }
+}
+
+template <int E>
+__device__ __forceinline__ void store_raw_round(uint8_t *raw_round_base, const Group &g) {
+  uint2 *q = (uint2 *)raw_round_base + (E - 1) * lane_id();
+  q[0] = make_uint2(g.raw[0], g.raw[1]);
+  if (E == 4) {
+    q[1] = make_uint2(g.raw[2], g.raw[3]);
+    q[2] = make_uint2(g.raw[4], g.raw[5]);
+  }
+}
+
 template <int E>
 __device__ __forceinline__ void store_raw_full(uint8_t *plane, uint64_t first, const Group &g) {
   uint2 *q = (uint2 *)(plane + (uint64_t)(E - 1) * first);
@@ -578,6 +602,8 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     const bool last_in_chunk = (lb + 1 == g.n_blocks);
     const uint8_t *src = REDUCE ? a.ybuf : a.in + chunk_first * E;  // pass-2 source (large blocks)
     uint8_t *raw_plane = sout + g.raw_off;
+    const uint8_t *src_blk = src + blk0 * E;           // wave-uniform
+    uint8_t *raw_blk = raw_plane + blk0 * (E - 1);      // wave-uniform
     uint32_t *h = hist + (lane & (kHistReplicas - 1)) * kHistStride;
     SymRegs S;
 
@@ -606,28 +632,36 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
       if (full > 0) {
 #pragma unroll
         for (int u = 0; u < D; ++u)
-          load_full<E>(src, blk0 + (u < (int)full ? u : full - 1) * kRound + kPerLane * lane, buf[u]);
+          load_round<E>(src_blk + (uint64_t)(u < (int)full ? u : full - 1) * kRound * E, buf[u]);
       }
       if constexpr (SMALL) {
-        for (uint32_t gi = 0; gi < 4; ++gi) {
+        // Fully unrolled and free of value-carrying branches: loads, the
+        // split and the register writes run for all 64 rounds (addresses
+        // clamped to a real round), only the side effects are guarded.  A
+        // prefetch buffer that crossed a branch join would be copied right
+        // after its load, and the copy would wait for the load.
+        if (full > 0) {
 #pragma unroll
-          for (int rr = 0; rr < 16; ++rr) {
-            const uint32_t r = 16 * gi + rr;
-            if (r < full) {
+          for (uint32_t gi = 0; gi < 4; ++gi) {
+#pragma unroll
+            for (int rr = 0; rr < 16; ++rr) {
+              const uint32_t r = 16 * gi + rr;
               uint32_t w[NW];
 #pragma unroll
               for (int q = 0; q < NW; ++q) w[q] = buf[rr % D][q];
               const uint32_t rn = (r + D < full) ? r + D : full - 1;
-              load_full<E>(src, blk0 + rn * kRound + kPerLane * lane, buf[rr % D]);
+              load_round<E>(src_blk + (uint64_t)rn * kRound * E, buf[rr % D]);
               Group gr;
               split_group<E>(w, gr);
               S.v3[2 * rr] = gr.sym[0];
               S.v3[2 * rr + 1] = gr.sym[1];
-              store_raw_full<E>(raw_plane, blk0 + r * kRound + kPerLane * lane, gr);
-              hist_add8(h, gr, 8);
+              if (r < full) {
+                store_raw_round<E>(raw_blk + (uint64_t)r * kRound * (E - 1), gr);
+                hist_add8(h, gr, 8);
+              }
             }
+            if (gi < 3) shift_down(S);
           }
-          if (gi < 3) shift_down(S);
         }
         if (full < rounds) partial_round();  // its symbols stay in psym0/psym1
       } else {
@@ -640,10 +674,10 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
 #pragma unroll
               for (int q = 0; q < NW; ++q) w[q] = buf[u][q];
               const uint32_t rn = (r + u + D < full) ? r + u + D : full - 1;
-              load_full<E>(src, blk0 + rn * kRound + kPerLane * lane, buf[u]);
+              load_round<E>(src_blk + (uint64_t)rn * kRound * E, buf[u]);
               Group gr;
               split_group<E>(w, gr);
-              store_raw_full<E>(raw_plane, blk0 + (r + u) * kRound + kPerLane * lane, gr);
+              store_raw_round<E>(raw_blk + (uint64_t)(r + u) * kRound * (E - 1), gr);
               hist_add8(h, gr, 8);
             }
           }
@@ -652,7 +686,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
             if (r + u < full) {
               Group gr;
               split_group<E>(buf[u], gr);
-              store_raw_full<E>(raw_plane, blk0 + (r + u) * kRound + kPerLane * lane, gr);
+              store_raw_round<E>(raw_blk + (uint64_t)(r + u) * kRound * (E - 1), gr);
               hist_add8(h, gr, 8);
             }
           }
@@ -866,10 +900,10 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     } else {
       // re-read the block backwards, one round ahead
       uint32_t wa[NW], wbuf[NW];
-      if (full > 0) load_full<E>(src, blk0 + (full - 1) * kRound + kPerLane * lane, wa);
+      if (full > 0) load_round<E>(src_blk + (uint64_t)(full - 1) * kRound * E, wa);
       int r = (int)full - 1;
       for (; r >= 1 && !stored; r -= 2) {
-        load_full<E>(src, blk0 + (uint32_t)(r - 1) * kRound + kPerLane * lane, wbuf);
+        load_round<E>(src_blk + (uint64_t)(r - 1) * kRound * E, wbuf);
         Group gr;
         split_group<E>(wa, gr);
         uint4 e[8];
@@ -879,7 +913,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         if (a.wcap - pos >= limit_words) stored = true;
         if (stored) break;
         const uint32_t rn = r >= 2 ? (uint32_t)(r - 2) : 0u;
-        load_full<E>(src, blk0 + rn * kRound + kPerLane * lane, wa);
+        load_round<E>(src_blk + (uint64_t)rn * kRound * E, wa);
         split_group<E>(wbuf, gr);
 #pragma unroll
         for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];

@@ -96,11 +96,12 @@ def main() -> int:
     out = torch.empty(cap, dtype=torch.uint8, device=dev)
     ws = torch.empty(uz.uzip_workspace_size(uz.OP_COMPRESS, uz.BF16, n, bb), dtype=torch.uint8, device=dev)
     y = torch.empty_like(x)
+    dws = torch.empty(uz.uzip_workspace_size(uz.OP_DECOMPRESS, uz.BF16, n, bb), dtype=torch.uint8, device=dev)
 
     size = status = None
     for _ in range(args.warmup):
         _, size = uz.compress(x, bb, dtype="bf16", out=out, ws=ws)
-        _, status = uz.decompress(out, "bf16", n, out=y)
+        _, status = uz.decompress(out, "bf16", n, out=y, ws=dws)
     torch.cuda.synchronize()
     total = int(size.item())
     if int(status.item()) != 0 or not torch.equal(x, y):
@@ -116,7 +117,7 @@ def main() -> int:
         e[0].record(stream)
         uz.compress(x, bb, dtype="bf16", out=out, ws=ws)
         e[1].record(stream)
-        uz.decompress(out, "bf16", n, out=y)
+        uz.decompress(out, "bf16", n, out=y, ws=dws)
         e[2].record(stream)
         evs.append(e)
     torch.cuda.synchronize()

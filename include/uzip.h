@@ -107,7 +107,9 @@ uzip_status uzip_compress(const void *d_in, uint64_t n_elems, uzip_dtype dtype,
  *   d_out, out_cap: n_elems values, out_cap >= n_elems * element size.
  *   d_status:       device u32, set to UZIP_ECORRUPT if the stream is
  *                   corrupt or does not match (may be NULL).
- *   d_ws, ws_bytes: not used by this version (pass NULL, 0).
+ *   d_ws, ws_bytes: device workspace of uzip_workspace_size(
+ *                   UZIP_OP_DECOMPRESS, ...) bytes (256: the counter that
+ *                   hands blocks to workgroups), 16-byte aligned.
  * Errors: EINVAL, ENOSPC, EHIP, EUNSUPPORTED. */
 uzip_status uzip_decompress(const void *d_in, size_t in_bytes, uzip_dtype dtype,
                             uint64_t n_elems, void *d_out, size_t out_cap,

@@ -147,15 +147,19 @@ def compress(x: torch.Tensor, block_bytes: int = 65536, dtype=None, out: torch.T
 
 
 def decompress(s: torch.Tensor, dtype, n_elems: int, out: torch.Tensor | None = None,
-               in_bytes: int | None = None, stream=None):
+               in_bytes: int | None = None, ws: torch.Tensor | None = None, stream=None):
     """Decompress a stream.  Returns (bit-pattern tensor, device u32 status)."""
     dt = dtype_code(dtype)
     if out is None:
         out = torch.empty(max(n_elems, 1), dtype=_BITS[dt], device=s.device)[:n_elems]
     status = torch.zeros(1, dtype=torch.int32, device=s.device)
     nbytes = s.numel() * s.element_size() if in_bytes is None else in_bytes
+    wsb = uzip_workspace_size(OP_DECOMPRESS, dt, n_elems, 65536, 0)
+    if ws is None:
+        ws = _dev_empty(wsb, s.device)
     _check(uzip_decompress(s.data_ptr(), nbytes, dt, n_elems, out.data_ptr() if n_elems else None,
-                           n_elems * _ELEM[dt], status.data_ptr(), None, 0, _stream(stream)), "uzip_decompress")
+                           n_elems * _ELEM[dt], status.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream)),
+           "uzip_decompress")
     return out, status
 
 

@@ -73,6 +73,8 @@ struct EncodeArgs {
   uint32_t lds_words;       // staging words held in LDS
 };
 
+constexpr size_t kDecodeWsBytes = 256;   // the block ticket
+
 struct DecodeArgs {
   const uint8_t *in;
   uint64_t in_bytes;
@@ -80,6 +82,7 @@ struct DecodeArgs {
   uint32_t dtype;
   uint8_t *out;
   uint32_t *dstatus;
+  uint32_t *ticket;  // workspace: next block to decode
 };
 
 // first error wins
@@ -1091,26 +1094,30 @@ __global__ void __launch_bounds__(64) reduce_kernel(EncodeArgs a) {
 constexpr uint32_t kRingBytes = 4096;
 constexpr uint32_t kChunkBytes = 1024;
 
+// One decode sub-step of every lane (inverse of the coding function, then
+// 16-bit renormalisation).  Branch-free: every lane reads the ring at its
+// would-be word index; lanes that need no word keep their state.  Indices
+// past the section's words stay inside the ring and are caught once per
+// block by p <= w_avail.
 template <bool FULL>
-__device__ inline uint32_t decode_step_ring(uint32_t &x, bool valid, const uint32_t *lut, const uint8_t *ring,
-                                            uint32_t wb, uint32_t &p, uint32_t w_avail, bool &bad) {
+__device__ __forceinline__ uint32_t decode_step_ring(uint32_t &x, bool valid, const uint32_t *lut,
+                                                     const uint8_t *ring, uint32_t wb, uint32_t &p) {
   uint32_t s = 0;
   if (FULL || valid) {
-    uint32_t e = lut[x & (kM - 1)];
+    const uint32_t e = lut[x & (kM - 1)];
     s = e >> 24;
     x = __umul24(e & 0xFFFu, x >> kProbBits) + ((e >> 12) & 0x7FFu);
   }
-  bool need = (FULL || valid) && x < kStateLo;
-  uint64_t m = __ballot(need);
-  if (need) {
-    uint32_t idx = p + mbcnt(m);
-    uint32_t w = *(const uint16_t *)(ring + ((wb + 2 * idx) & (kRingBytes - 1)));
-    bad |= idx >= w_avail;
-    x = (x << 16) | w;
-  }
+  const bool need = (FULL || valid) && x < kStateLo;
+  const uint64_t m = __ballot(need);
+  const uint32_t idx = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, p));
+  uint32_t w = *(const uint16_t *)(ring + ((wb + 2 * idx) & (kRingBytes - 1)));
+  asm volatile("" : "+v"(w));  // keep the read unconditional: no exec-mask branch around it
+  x = need ? ((x << 16) | w) : x;
   p += (uint32_t)__popcll(m);
   return s;
 }
+
 
 // Ring bookkeeping of one coded block (all members wave-uniform).
 struct Ring {
@@ -1158,7 +1165,8 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
   constexpr int NW = 4 * (E / 2);
   __shared__ uint32_t lut[kM];
   __shared__ __align__(16) uint8_t ring[kRingBytes];
-  __shared__ uint16_t cum_s[256], f_s[256];
+  // the table-build scratch (cum, f) lives in the ring before the ring fills
+  uint16_t *cum_s = (uint16_t *)ring, *f_s = (uint16_t *)ring + 256;
   const uint32_t lane = lane_id();
   const uint8_t *s = a.in;
   if (a.in_bytes < kHeaderBytes) {
@@ -1183,7 +1191,11 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
   }
   const uint8_t *raw_plane = s + g.raw_off;
 
-  for (uint32_t b = blockIdx.x; b < nb; b += gridDim.x) {
+  while (true) {
+    uint32_t b = 0;
+    if (lane == 0) b = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    b = uniform(b);
+    if (b >= nb) break;
     const uint32_t d = ld32(s + kHeaderBytes + 4 * b);
     const uint64_t start = b ? 16ull * (ld32(s + kHeaderBytes + 4 * (b - 1)) & ~kStoredBit) : 0;
     const uint64_t end = 16ull * (d & ~kStoredBit);
@@ -1262,7 +1274,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
       uint32_t sym[2] = {0, 0};
 #pragma unroll
       for (uint32_t t = 0; t < kPerLane; ++t)
-        sym[t >> 2] |= decode_step_ring<true>(x, true, lut, ring, wb, p, w_avail, bad) << (8 * (t & 3));
+        sym[t >> 2] |= decode_step_ring<true>(x, true, lut, ring, wb, p) << (8 * (t & 3));
       uint32_t w[NW];
       merge_group<E>(sym, rawA, w);
       store_words<E>(outp, r * kRound + kPerLane * lane, 8, w);
@@ -1273,7 +1285,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
       sym[0] = sym[1] = 0;
 #pragma unroll
       for (uint32_t t = 0; t < kPerLane; ++t)
-        sym[t >> 2] |= decode_step_ring<true>(x, true, lut, ring, wb, p, w_avail, bad) << (8 * (t & 3));
+        sym[t >> 2] |= decode_step_ring<true>(x, true, lut, ring, wb, p) << (8 * (t & 3));
       merge_group<E>(sym, rawB, w);
       store_words<E>(outp, (r + 1) * kRound + kPerLane * lane, 8, w);
     }
@@ -1282,7 +1294,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
       uint32_t sym[2] = {0, 0};
 #pragma unroll
       for (uint32_t t = 0; t < kPerLane; ++t)
-        sym[t >> 2] |= decode_step_ring<true>(x, true, lut, ring, wb, p, w_avail, bad) << (8 * (t & 3));
+        sym[t >> 2] |= decode_step_ring<true>(x, true, lut, ring, wb, p) << (8 * (t & 3));
       uint32_t w[NW];
       merge_group<E>(sym, rawA, w);
       store_words<E>(outp, r * kRound + kPerLane * lane, 8, w);
@@ -1295,7 +1307,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
       uint32_t sym[2] = {0, 0};
 #pragma unroll
       for (uint32_t t = 0; t < kPerLane; ++t)
-        sym[t >> 2] |= decode_step_ring<false>(x, t < valid, lut, ring, wb, p, w_avail, bad) << (8 * (t & 3));
+        sym[t >> 2] |= decode_step_ring<false>(x, t < valid, lut, ring, wb, p) << (8 * (t & 3));
       if (valid > 0) {
         uint32_t raw[6];
         load_raw<E>(raw_plane, blk0 + i0, valid, raw);
@@ -1304,7 +1316,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
         store_words<E>(a.out, blk0 + i0, valid, w);
       }
     }
-    if (x != kStateLo) bad = true;
+    if (x != kStateLo || p > w_avail) bad = true;
     if (__any(bad) && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
     __syncthreads();
   }
@@ -1467,7 +1479,7 @@ size_t uzip_workspace_size(int op, uzip_dtype dtype, uint64_t n_elems, uint32_t 
     case UZIP_OP_COMPRESS:
       return (size_t)encode_ws(nb, 1, be, 0).total;
     case UZIP_OP_DECOMPRESS:
-      return 0;
+      return kDecodeWsBytes;
     case UZIP_OP_CHUNKED: {
       if (aux == 0 || aux % block_bytes) return 0;
       const uint64_t ce = aux / E;
@@ -1559,11 +1571,10 @@ uzip_status uzip_compress_chunked(const void *d_in, uint64_t n_elems, uzip_dtype
 
 uzip_status uzip_decompress(const void *d_in, size_t in_bytes, uzip_dtype dtype, uint64_t n_elems, void *d_out,
                             size_t out_cap, uint32_t *d_status, void *d_ws, size_t ws_bytes, hipStream_t stream) {
-  (void)d_ws;
-  (void)ws_bytes;
   if (!valid_dtype(dtype) || d_in == nullptr || !aligned16(d_in)) return UZIP_EINVAL;
   if (n_elems > 0 && (d_out == nullptr || !aligned16(d_out))) return UZIP_EINVAL;
   if (out_cap < n_elems * elem_bytes(dtype)) return UZIP_ENOSPC;
+  if (d_ws == nullptr || !aligned16(d_ws) || ws_bytes < kDecodeWsBytes) return UZIP_EINVAL;
   DeviceInfo info;
   uzip_status st = device_info(info);
   if (st != UZIP_OK) return st;
@@ -1574,15 +1585,22 @@ uzip_status uzip_decompress(const void *d_in, size_t in_bytes, uzip_dtype dtype,
   a.dtype = (uint32_t)dtype;
   a.out = (uint8_t *)d_out;
   a.dstatus = d_status;
-  // grid-stride: enough waves to fill the device, never more than the smallest block size allows
+  a.ticket = (uint32_t *)d_ws;
+  // resident waves take blocks by ticket until none are left
   const uint64_t most = (n_elems + (kMinBlockBytes / elem_bytes(dtype)) - 1) / (kMinBlockBytes / elem_bytes(dtype));
-  uint64_t grid = (uint64_t)info.cus * 16;
+  const void *fn = dtype == UZIP_BF16   ? (const void *)decode_kernel<0>
+                   : dtype == UZIP_FP16 ? (const void *)decode_kernel<1>
+                                        : (const void *)decode_kernel<2>;
+  int occ = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, 64, 0) != hipSuccess || occ < 1) occ = 1;
+  uint64_t grid = (uint64_t)info.cus * (uint64_t)occ;
   if (grid > most) grid = most;
   if (grid == 0) grid = 1;
-  if (dtype == UZIP_BF16) hipLaunchKernelGGL(decode_kernel<0>, dim3((unsigned)grid), dim3(64), 0, stream, a);
-  if (dtype == UZIP_FP16) hipLaunchKernelGGL(decode_kernel<1>, dim3((unsigned)grid), dim3(64), 0, stream, a);
-  if (dtype == UZIP_FP32) hipLaunchKernelGGL(decode_kernel<2>, dim3((unsigned)grid), dim3(64), 0, stream, a);
-  return hipGetLastError() == hipSuccess ? UZIP_OK : UZIP_EHIP;
+  hipLaunchKernelGGL(clear_kernel, dim3(1), dim3(64), 0, stream, a.ticket, (uint64_t)1);
+  if (hipGetLastError() != hipSuccess) return UZIP_EHIP;
+  void *args[] = {&a};
+  if (hipLaunchKernel(fn, dim3((unsigned)grid), dim3(64), args, 0, stream) != hipSuccess) return UZIP_EHIP;
+  return UZIP_OK;
 }
 
 uzip_status uzip_reduce_fused(const void *const *d_in, const size_t *in_bytes, int n_in, const void *d_local_raw,

@@ -1092,56 +1092,93 @@ __global__ void __launch_bounds__(64) reduce_kernel(EncodeArgs a) {
 // round is loaded one round ahead.
 // ---------------------------------------------------------------------------
 constexpr uint32_t kRingBytes = 4096;
+constexpr uint32_t kRingMirror = 128;  // ring[0, 128) repeated past the end: one step's reads never wrap
 constexpr uint32_t kChunkBytes = 1024;
 
 // One decode sub-step of every lane (inverse of the coding function, then
-// 16-bit renormalisation).  Branch-free: every lane reads the ring at its
-// would-be word index; lanes that need no word keep their state.  Indices
-// past the section's words stay inside the ring and are caught once per
-// block by p <= w_avail.
+// 16-bit renormalisation).  Returns the lane's table entry (its symbol in the
+// top byte; 0 for a lane without an element).  Branch-free: every lane reads
+// the ring at its would-be word position rb + 2 * rank (rb: ring offset of
+// the next unread word, uniform); lanes that need no word keep their state.
+// Positions past the section's words stay inside the ring and are caught
+// once per block by p <= w_avail.
 template <bool FULL>
 __device__ __forceinline__ uint32_t decode_step_ring(uint32_t &x, bool valid, const uint32_t *lut,
-                                                     const uint8_t *ring, uint32_t wb, uint32_t &p) {
-  uint32_t s = 0;
+                                                     const uint8_t *ring, uint32_t &rb, uint32_t &p) {
+  uint32_t e = 0;
   if (FULL || valid) {
-    const uint32_t e = lut[x & (kM - 1)];
-    s = e >> 24;
+    e = lut[x & (kM - 1)];
     x = __umul24(e & 0xFFFu, x >> kProbBits) + ((e >> 12) & 0x7FFu);
   }
   const bool need = (FULL || valid) && x < kStateLo;
   const uint64_t m = __ballot(need);
-  const uint32_t idx = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, p));
-  uint32_t w = *(const uint16_t *)(ring + ((wb + 2 * idx) & (kRingBytes - 1)));
+  const uint32_t rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+  uint32_t w = *(const uint16_t *)(ring + rb + 2 * rank);
   asm volatile("" : "+v"(w));  // keep the read unconditional: no exec-mask branch around it
   x = need ? ((x << 16) | w) : x;
-  p += (uint32_t)__popcll(m);
-  return s;
+  const uint32_t c = (uint32_t)__popcll(m);
+  p += c;
+  rb = (rb + 2 * c) & (kRingBytes - 1);
+  return e;
+}
+
+// 16 bytes of section words into the ring at pos and, for the first 128
+// bytes, into the mirror (the other lanes store to pos twice: no branch)
+__device__ __forceinline__ void ring_put(uint8_t *ring, uint32_t pos, uint4 v) {
+  *(uint4 *)(ring + pos) = v;
+  *(uint4 *)(ring + (pos < kRingMirror ? kRingBytes + pos : pos)) = v;
+}
+
+// Eight decoded elements of one lane from their table entries (symbols in
+// the top bytes) and raw bytes: the inverse of the byte-plane split.
+template <int E>
+__device__ inline void merge_entries(const uint32_t e[8], const uint32_t raw[6], uint32_t w[4 * (E / 2)]) {
+  if (E == 2) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      // [raw, sym, raw, sym] of elements 2j, 2j + 1, then rotate each half back
+      const uint32_t t = __builtin_amdgcn_perm(e[2 * j], raw[j >> 1], (j & 1) ? 0x07030702u : 0x07010700u);
+      w[j] = rotr16x2(__builtin_amdgcn_perm(e[2 * j + 1], t, 0x07020100u));
+    }
+  } else {
+    uint32_t sym[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint32_t lo = __builtin_amdgcn_perm(e[4 * h + 1], e[4 * h], 0x07070703u);
+      const uint32_t hi = __builtin_amdgcn_perm(e[4 * h + 3], e[4 * h + 2], 0x07030303u);
+      sym[h] = __builtin_amdgcn_perm(hi, lo, 0x07060100u);
+    }
+    merge32(sym, raw, w);
+  }
 }
 
 
 // Ring bookkeeping of one coded block (all members wave-uniform).
 struct Ring {
   uint32_t written;  // section bytes [written - 4096, written) are in the ring
-  uint32_t len;      // section length
-  bool pend;         // a chunk is loaded into registers, not yet in LDS
-  uint4 pv;
+  uint32_t len;      // section length (a multiple of 16)
+  uint4 pv;          // this lane's 16 bytes of the chunk at `written`, loaded a round ahead
 };
 
-// Before a round: make sure the next 1 KB of words is in LDS, and start
-// loading the following chunk as soon as the ring has room for it.
-__device__ inline void ring_maintain(Ring &rg, uint8_t *ring, const uint8_t *sec, uint32_t cur) {
+// 16 bytes of this lane's part of the chunk at section offset o (clamped to
+// the section: a chunk past the end is never decoded from)
+__device__ __forceinline__ uint4 ring_fetch(const uint8_t *sec, uint32_t o, uint32_t len) {
+  return *(const uint4 *)(sec + (o + 16 <= len ? o : len - 16));
+}
+
+// Before a round: make sure the next 1 KB of words (from section offset cur)
+// is in LDS, then load the following chunk for the next round.  Every round
+// stores the loaded chunk at its ring position and loads the chunk at
+// `written` again, also when neither has moved (a repeat store of the same
+// bytes; a cache hit): every path through a round then issues the same
+// memory operations, so no wait for them lands inside the decode chain.
+// The store never overwrites unread words: written < cur + 2048 always.
+__device__ __forceinline__ void ring_maintain(Ring &rg, uint8_t *ring, const uint8_t *sec, uint32_t cur) {
   const uint32_t lane = lane_id();
-  if (rg.pend && rg.written < cur + kChunkBytes) {
-    *(uint4 *)(ring + ((rg.written + 16 * lane) & (kRingBytes - 1))) = rg.pv;
-    rg.written += kChunkBytes;
-    rg.pend = false;
-    __syncthreads();
-  }
-  if (!rg.pend && rg.written < rg.len && rg.written - cur <= kRingBytes - kChunkBytes) {
-    const uint32_t o = rg.written + 16 * lane;
-    rg.pv = o + 16 <= rg.len ? *(const uint4 *)(sec + o) : make_uint4(0, 0, 0, 0);
-    rg.pend = true;
-  }
+  ring_put(ring, (rg.written + 16 * lane) & (kRingBytes - 1), rg.pv);
+  asm volatile("" ::: "memory");  // the ring stores stay before the round's ring reads
+  rg.written += rg.written < cur + kChunkBytes ? kChunkBytes : 0;
+  rg.pv = ring_fetch(sec, rg.written + 16 * lane, rg.len);
 }
 
 template <int E>
@@ -1164,7 +1201,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
   constexpr int E = (DT == 2) ? 4 : 2;
   constexpr int NW = 4 * (E / 2);
   __shared__ uint32_t lut[kM];
-  __shared__ __align__(16) uint8_t ring[kRingBytes];
+  __shared__ __align__(16) uint8_t ring[kRingBytes + kRingMirror];
   // the table-build scratch (cum, f) lives in the ring before the ring fills
   uint16_t *cum_s = (uint16_t *)ring, *f_s = (uint16_t *)ring + 256;
   const uint32_t lane = lane_id();
@@ -1241,62 +1278,60 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
     }
     k = uniform(k);
     uint32_t x = ((const uint32_t *)sec)[lane];
-    bad = __any(x < kStateLo || x >= 0x80000000u);
+    const uint32_t x0 = x;  // checked at the end of the block: no wait for it here
     const uint32_t wb = kSectionFixed + 2 * k;  // section offset of word 0
     const uint32_t w_avail = (len - wb) / 2;
     Ring rg;
     rg.len = len;
     rg.written = wb & ~15u;
-    rg.pend = false;
-    rg.pv = make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      if (rg.written < len) {
-        uint32_t o = rg.written + 16 * lane;
-        uint4 v = o + 16 <= len ? *(const uint4 *)(sec + o) : make_uint4(0, 0, 0, 0);
-        *(uint4 *)(ring + (o & (kRingBytes - 1))) = v;
-        rg.written += kChunkBytes;
-      }
+      const uint32_t o = rg.written + 16 * lane;
+      ring_put(ring, o & (kRingBytes - 1), ring_fetch(sec, o, len));
+      rg.written += kChunkBytes;
     }
+    rg.pv = ring_fetch(sec, rg.written + 16 * lane, len);
     __syncthreads();
-    uint32_t p = 0;
+    uint32_t p = 0, rb = wb & (kRingBytes - 1);
     const uint32_t full = n_b / kRound;
     uint8_t *outp = a.out + blk0 * E;
     const uint8_t *rawp = raw_plane + blk0 * (E - 1);
     uint32_t rawA[6] = {0, 0, 0, 0, 0, 0}, rawB[6] = {0, 0, 0, 0, 0, 0};
-    if (full > 0) load_raw_full<E>(rawp, kPerLane * lane, rawA);
+    // round 0's raw bytes; with no full round a dummy load of the stream
+    // header, so that the loop below is always entered with the same loads
+    // in flight and waits only for what it uses
+    load_raw_full<E>(full > 0 ? rawp : s, full > 0 ? kPerLane * lane : 0, rawA);
+    // one more memory operation in flight, standing in for the store that
+    // ends every round, so that both ways into the loop match
+    const uint32_t pad_load = *(const uint32_t *)(s + 4 * lane);
     uint32_t r = 0;
     // full rounds, two per iteration with ping-pong raw registers: every
     // load is issued a round before its use and no register is copied
     for (; r + 2 <= full; r += 2) {
       ring_maintain(rg, ring, sec, wb + 2 * p);
       load_raw_full<E>(rawp, (r + 1) * kRound + kPerLane * lane, rawB);
-      uint32_t sym[2] = {0, 0};
+      uint32_t e[kPerLane];
 #pragma unroll
-      for (uint32_t t = 0; t < kPerLane; ++t)
-        sym[t >> 2] |= decode_step_ring<true>(x, true, lut, ring, wb, p) << (8 * (t & 3));
+      for (uint32_t t = 0; t < kPerLane; ++t) e[t] = decode_step_ring<true>(x, true, lut, ring, rb, p);
       uint32_t w[NW];
-      merge_group<E>(sym, rawA, w);
+      merge_entries<E>(e, rawA, w);
       store_words<E>(outp, r * kRound + kPerLane * lane, 8, w);
 
       ring_maintain(rg, ring, sec, wb + 2 * p);
       const uint32_t rn = (r + 2 < full) ? r + 2 : r + 1;  // always a full round: no branch around the load
       load_raw_full<E>(rawp, rn * kRound + kPerLane * lane, rawA);
-      sym[0] = sym[1] = 0;
 #pragma unroll
-      for (uint32_t t = 0; t < kPerLane; ++t)
-        sym[t >> 2] |= decode_step_ring<true>(x, true, lut, ring, wb, p) << (8 * (t & 3));
-      merge_group<E>(sym, rawB, w);
+      for (uint32_t t = 0; t < kPerLane; ++t) e[t] = decode_step_ring<true>(x, true, lut, ring, rb, p);
+      merge_entries<E>(e, rawB, w);
       store_words<E>(outp, (r + 1) * kRound + kPerLane * lane, 8, w);
     }
     if (r < full) {  // odd number of full rounds: rawA holds round r
       ring_maintain(rg, ring, sec, wb + 2 * p);
-      uint32_t sym[2] = {0, 0};
+      uint32_t e[kPerLane];
 #pragma unroll
-      for (uint32_t t = 0; t < kPerLane; ++t)
-        sym[t >> 2] |= decode_step_ring<true>(x, true, lut, ring, wb, p) << (8 * (t & 3));
+      for (uint32_t t = 0; t < kPerLane; ++t) e[t] = decode_step_ring<true>(x, true, lut, ring, rb, p);
       uint32_t w[NW];
-      merge_group<E>(sym, rawA, w);
+      merge_entries<E>(e, rawA, w);
       store_words<E>(outp, r * kRound + kPerLane * lane, 8, w);
       ++r;
     }
@@ -1304,19 +1339,19 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
       ring_maintain(rg, ring, sec, wb + 2 * p);
       const uint32_t i0 = r * kRound + kPerLane * lane;
       const uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
-      uint32_t sym[2] = {0, 0};
+      uint32_t e[kPerLane];
 #pragma unroll
-      for (uint32_t t = 0; t < kPerLane; ++t)
-        sym[t >> 2] |= decode_step_ring<false>(x, t < valid, lut, ring, wb, p) << (8 * (t & 3));
+      for (uint32_t t = 0; t < kPerLane; ++t) e[t] = decode_step_ring<false>(x, t < valid, lut, ring, rb, p);
       if (valid > 0) {
         uint32_t raw[6];
         load_raw<E>(raw_plane, blk0 + i0, valid, raw);
         uint32_t w[NW];
-        merge_group<E>(sym, raw, w);
+        merge_entries<E>(e, raw, w);
         store_words<E>(a.out, blk0 + i0, valid, w);
       }
     }
-    if (x != kStateLo || p > w_avail) bad = true;
+    asm volatile("" ::"v"(pad_load));
+    if (x != kStateLo || p > w_avail || x0 < kStateLo || x0 >= 0x80000000u) bad = true;
     if (__any(bad) && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
     __syncthreads();
   }

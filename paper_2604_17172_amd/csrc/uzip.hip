@@ -139,20 +139,48 @@ __device__ inline void split_group(const uint32_t w[4 * (E / 2)], Group &g) {
 }
 
 // raw plane bytes of a group: 8 (E = 2) or 24 (E = 4) bytes at plane + (E-1) first
-template <int E>
+// Stores of stream bytes.  SYS (split-send producer): system-coherent
+// stores, written through to memory, so that a block only has to wait for
+// its own stores before it counts itself done, instead of writing back the
+// whole L2 (a consumer outside this GPU reads the chunk once its flag is set).
+template <bool SYS>
+__device__ __forceinline__ void out8(uint8_t *p, uint8_t v) {
+  if (SYS) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  else *p = v;
+}
+template <bool SYS>
+__device__ __forceinline__ void out32(uint32_t *p, uint32_t v) {
+  if (SYS) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  else *p = v;
+}
+template <bool SYS>
+__device__ __forceinline__ void out64(uint8_t *p, uint32_t lo, uint32_t hi) {
+  if (SYS) __hip_atomic_store((uint64_t *)p, (uint64_t)hi << 32 | lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  else *(uint2 *)p = make_uint2(lo, hi);
+}
+template <bool SYS>
+__device__ __forceinline__ void out128(uint8_t *p, uint4 v) {
+  if (SYS) {
+    out64<true>(p, v.x, v.y);
+    out64<true>(p + 8, v.z, v.w);
+  } else {
+    *(uint4 *)p = v;
+  }
+}
+
+template <int E, bool SYS = false>
 __device__ inline void store_raw(uint8_t *plane, uint64_t first, uint32_t valid, const Group &g) {
   uint8_t *p = plane + (uint64_t)(E - 1) * first;
   if (valid >= 8) {
-    uint2 *q = (uint2 *)p;
-    q[0] = make_uint2(g.raw[0], g.raw[1]);
+    out64<SYS>(p, g.raw[0], g.raw[1]);
     if (E == 4) {
-      q[1] = make_uint2(g.raw[2], g.raw[3]);
-      q[2] = make_uint2(g.raw[4], g.raw[5]);
+      out64<SYS>(p + 8, g.raw[2], g.raw[3]);
+      out64<SYS>(p + 16, g.raw[4], g.raw[5]);
     }
   } else {
 #pragma unroll
     for (uint32_t b = 0; b < 8 * (E - 1); ++b)
-      if (b < (E - 1) * valid) p[b] = (uint8_t)(g.raw[b >> 2] >> (8 * (b & 3)));
+      if (b < (E - 1) * valid) out8<SYS>(p + b, (uint8_t)(g.raw[b >> 2] >> (8 * (b & 3))));
   }
 }
 
@@ -410,11 +438,15 @@ __device__ uint64_t lookback(uint64_t *status, uint32_t b, uint32_t first, uint6
 }
 
 // Counter of finished blocks of a chunk; the last one publishes the flag.
+// The block's stream bytes were written with system-coherent stores
+// (write-through), so waiting for them to complete is what orders them
+// before the count; the count is a system-scope atomic at the memory, so the
+// block that completes it stores the flag after every block's bytes are in
+// memory.
 __device__ void publish_chunk(uint32_t *cnt, uint32_t need, uint32_t *flag, uint32_t epoch) {
-  if (lane_id() == 0) {
-    uint32_t old = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_SYSTEM);
-    if (old + 1 == need) __hip_atomic_store(flag, epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
-  }
+  __builtin_amdgcn_s_waitcnt(0);
+  if (lane_id() == 0 && __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) + 1 == need)
+    __hip_atomic_store(flag, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
 // Fused reduce, pass 1 helpers: per-input state of the block being reduced.
@@ -534,13 +566,13 @@ __device__ __forceinline__ void load_round(const uint8_t *round_base, uint32_t w
   }
 }
 
-template <int E>
+template <int E, bool SYS>
 __device__ __forceinline__ void store_raw_round(uint8_t *raw_round_base, const Group &g) {
-  uint2 *q = (uint2 *)raw_round_base + (E - 1) * lane_id();
-  q[0] = make_uint2(g.raw[0], g.raw[1]);
+  uint8_t *q = raw_round_base + 8 * (E - 1) * lane_id();
+  out64<SYS>(q, g.raw[0], g.raw[1]);
   if (E == 4) {
-    q[1] = make_uint2(g.raw[2], g.raw[3]);
-    q[2] = make_uint2(g.raw[4], g.raw[5]);
+    out64<SYS>(q + 8, g.raw[2], g.raw[3]);
+    out64<SYS>(q + 16, g.raw[4], g.raw[5]);
   }
 }
 
@@ -568,7 +600,7 @@ __device__ __forceinline__ void hist_add8(uint32_t *h, const Group &g, uint32_t 
 //   workgroup's overflow slot.  Otherwise the coding pass re-reads the block
 //   and LDS holds the whole staging area.
 // ---------------------------------------------------------------------------
-template <int DT, bool REDUCE, bool SMALL>
+template <int DT, bool REDUCE, bool SMALL, bool SYS>
 __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   constexpr int E = (DT == 2) ? 4 : 2;
   constexpr int NW = 4 * (E / 2);
@@ -625,7 +657,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
           uint32_t w[NW];
           load_words<E>(src, blk0 + i0, valid, w);
           split_group<E>(w, gr);
-          store_raw<E>(raw_plane, blk0 + i0, valid, gr);
+          store_raw<E, SYS>(raw_plane, blk0 + i0, valid, gr);
           hist_add8(h, gr, valid);
         }
         psym0 = gr.sym[0];
@@ -659,7 +691,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
               S.v3[2 * rr] = gr.sym[0];
               S.v3[2 * rr + 1] = gr.sym[1];
               if (r < full) {
-                store_raw_round<E>(raw_blk + (uint64_t)r * kRound * (E - 1), gr);
+                store_raw_round<E, SYS>(raw_blk + (uint64_t)r * kRound * (E - 1), gr);
                 hist_add8(h, gr, 8);
               }
             }
@@ -680,7 +712,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
               load_round<E>(src_blk + (uint64_t)rn * kRound * E, buf[u]);
               Group gr;
               split_group<E>(w, gr);
-              store_raw_round<E>(raw_blk + (uint64_t)(r + u) * kRound * (E - 1), gr);
+              store_raw_round<E, SYS>(raw_blk + (uint64_t)(r + u) * kRound * (E - 1), gr);
               hist_add8(h, gr, 8);
             }
           }
@@ -689,7 +721,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
             if (r + u < full) {
               Group gr;
               split_group<E>(buf[u], gr);
-              store_raw_round<E>(raw_blk + (uint64_t)(r + u) * kRound * (E - 1), gr);
+              store_raw_round<E, SYS>(raw_blk + (uint64_t)(r + u) * kRound * (E - 1), gr);
               hist_add8(h, gr, 8);
             }
           }
@@ -819,7 +851,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
             gr.sym[0] = (uint32_t)v;
             gr.sym[1] = (uint32_t)(v >> 32);
           }
-          store_raw<E>(raw_plane, blk0 + i0, valid, gr);
+          store_raw<E, SYS>(raw_plane, blk0 + i0, valid, gr);
           hist_add8(h, gr, valid);
         }
       }
@@ -832,11 +864,10 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     if (last_in_chunk && lane < 16) {
       // zero padding after the raw plane (pad16 of (E-1) n bytes)
       uint64_t rb = g.raw_off + (uint64_t)(E - 1) * chunk_n + lane;
-      if (rb < g.coded_off) sout[rb] = 0;
+      if (rb < g.coded_off) out8<SYS>(sout + rb, 0);
     }
     __syncthreads();
     if (a.flags != nullptr) {
-      __threadfence_system();
       publish_chunk(&a.chunk_cnt[2 * chunk], g.n_blocks, &a.flags[2 * chunk], a.epoch);
     }
 
@@ -942,7 +973,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     const uint64_t excl = lookback(a.status, b, first_block, sec_len / 16, a.ticket + 1);
     uint8_t *sec = sout + g.coded_off + 16 * excl;
     if (lane == 0)
-      *(uint32_t *)(sout + kHeaderBytes + 4 * lb) = (stored ? kStoredBit : 0u) | (uint32_t)(excl + sec_len / 16);
+      out32<SYS>((uint32_t *)(sout + kHeaderBytes + 4 * lb), (stored ? kStoredBit : 0u) | (uint32_t)(excl + sec_len / 16));
 
     if (!stored) {
       const uint32_t hdr = kSectionFixed + 2 * t.k;
@@ -977,7 +1008,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
           o.y = __builtin_amdgcn_alignbyte(q[2], q[1], sh);
           o.z = __builtin_amdgcn_alignbyte(q[3], q[2], sh);
           o.w = __builtin_amdgcn_alignbyte(q[4], q[3], sh);
-          ((uint4 *)sec)[u] = o;
+          out128<SYS>(sec + 16 * u, o);
         }
       } else {
         // rare: words [spilled, wcap) went to the overflow slot; gather the
@@ -1006,7 +1037,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
             }
             o[hw >> 1] |= v16 << (16 * (hw & 1));
           }
-          ((uint4 *)sec)[u] = make_uint4(o[0], o[1], o[2], o[3]);
+          out128<SYS>(sec + 16 * u, make_uint4(o[0], o[1], o[2], o[3]));
         }
       }
     } else {
@@ -1022,7 +1053,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
           s0 = (uint32_t)v;
           s1 = (uint32_t)(v >> 32);
         }
-        *(uint2 *)(sec + i0) = make_uint2(s0, s1);
+        out64<SYS>(sec + i0, s0, s1);
       };
       {  // the coding pass consumed the register copy of the symbols: re-read the block
         for (uint32_t r = 0; r < rounds; ++r) {
@@ -1055,16 +1086,18 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         hh[6] = (uint32_t)total;
         hh[7] = (uint32_t)(total >> 32);
         uint4 *hp = (uint4 *)sout;
-        hp[0] = make_uint4(hh[0], hh[1], hh[2], hh[3]);
-        hp[1] = make_uint4(hh[4], hh[5], hh[6], hh[7]);
-        if (a.sizes != nullptr) a.sizes[chunk] = total;
+        out128<SYS>((uint8_t *)hp, make_uint4(hh[0], hh[1], hh[2], hh[3]));
+        out128<SYS>((uint8_t *)(hp + 1), make_uint4(hh[4], hh[5], hh[6], hh[7]));
+        if (a.sizes != nullptr) {
+          if (SYS) __hip_atomic_store(&a.sizes[chunk], total, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          else a.sizes[chunk] = total;
+        }
       }
       // zero padding after the directory
       uint64_t db = kHeaderBytes + 4ull * g.n_blocks + lane;
-      if (lane < 16 && db < g.raw_off) sout[db] = 0;
+      if (lane < 16 && db < g.raw_off) out8<SYS>(sout + db, 0);
     }
     if (a.flags != nullptr) {
-      __threadfence_system();
       publish_chunk(&a.chunk_cnt[2 * chunk + 1], g.n_blocks, &a.flags[2 * chunk + 1], a.epoch);
     }
     __syncthreads();
@@ -1073,13 +1106,13 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
 
 // Compress kernels keep two waves per SIMD (the LDS budget allows eight
 // workgroups per CU); the fused reduce holds many more per-input states.
-template <int DT, bool REDUCE, bool SMALL>
+template <int DT, bool SMALL, bool SYS>
 __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) encode_kernel(EncodeArgs a) {
-  encode_body<DT, false, SMALL>(a);
+  encode_body<DT, false, SMALL, SYS>(a);
 }
 template <int DT>
 __global__ void __launch_bounds__(64) reduce_kernel(EncodeArgs a) {
-  encode_body<DT, true, false>(a);
+  encode_body<DT, true, false, false>(a);
 }
 
 // ---------------------------------------------------------------------------
@@ -1376,16 +1409,23 @@ __global__ void empty_stream_kernel(uint8_t *out, uint32_t dt, uint32_t block_el
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
-// encode_kernel instantiations: index = dt * 4 + reduce * 2 + small
+// encoder kernels: index = dt * 4 + kind, kind 0/1 = compress large/small
+// blocks, 2/3 = split-send producer large/small blocks; fused reduce apart
+constexpr int kEncodeKernels = 12;
 const void *encode_kernel_ptr(int k) {
-  static const void *const tab[12] = {
-      (const void *)encode_kernel<0, false, false>, (const void *)encode_kernel<0, false, true>,
-      (const void *)reduce_kernel<0>,               (const void *)reduce_kernel<0>,
-      (const void *)encode_kernel<1, false, false>, (const void *)encode_kernel<1, false, true>,
-      (const void *)reduce_kernel<1>,               (const void *)reduce_kernel<1>,
-      (const void *)encode_kernel<2, false, false>, (const void *)encode_kernel<2, false, true>,
-      (const void *)reduce_kernel<2>,               (const void *)reduce_kernel<2>};
+  static const void *const tab[kEncodeKernels] = {
+      (const void *)encode_kernel<0, false, false>, (const void *)encode_kernel<0, true, false>,
+      (const void *)encode_kernel<0, false, true>,  (const void *)encode_kernel<0, true, true>,
+      (const void *)encode_kernel<1, false, false>, (const void *)encode_kernel<1, true, false>,
+      (const void *)encode_kernel<1, false, true>,  (const void *)encode_kernel<1, true, true>,
+      (const void *)encode_kernel<2, false, false>, (const void *)encode_kernel<2, true, false>,
+      (const void *)encode_kernel<2, false, true>,  (const void *)encode_kernel<2, true, true>};
   return tab[k];
+}
+const void *reduce_kernel_ptr(int dt) {
+  static const void *const tab[3] = {(const void *)reduce_kernel<0>, (const void *)reduce_kernel<1>,
+                                     (const void *)reduce_kernel<2>};
+  return tab[dt];
 }
 
 struct DeviceInfo {
@@ -1408,8 +1448,10 @@ uzip_status device_info(DeviceInfo &out) {
     g_info[dev].cus = prop.multiProcessorCount;
     g_info[dev].gfx950 = strncmp(prop.gcnArchName, "gfx950", 6) == 0;
     const int lds_max = 160 * 1024;
-    for (int k = 0; k < 12; ++k)
+    for (int k = 0; k < kEncodeKernels; ++k)
       (void)hipFuncSetAttribute(encode_kernel_ptr(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
+    for (int k = 0; k < 3; ++k)
+      (void)hipFuncSetAttribute(reduce_kernel_ptr(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
   });
   if (err != hipSuccess) return UZIP_EHIP;
   out = g_info[dev];
@@ -1481,7 +1523,8 @@ uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws
   a.pass2_off = kEncTableBytes;
   const uint32_t lds = encode_lds(a.block_elems, reduce ? a.n_in : 0, small);
   if (lds > 160 * 1024) return UZIP_EINVAL;
-  const void *fn = encode_kernel_ptr((int)dt * 4 + (reduce ? 2 : 0) + (small ? 1 : 0));
+  const void *fn = reduce ? reduce_kernel_ptr((int)dt)
+                          : encode_kernel_ptr((int)dt * 4 + (a.flags != nullptr ? 2 : 0) + (small ? 1 : 0));
   int occ = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, 64, lds) != hipSuccess || occ < 1) occ = 1;
   uint64_t grid = (uint64_t)info.cus * (uint64_t)occ;

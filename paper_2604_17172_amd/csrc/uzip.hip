@@ -19,11 +19,18 @@
 //                   single-pass scan with decoupled look-back over blocks
 //                   taken in ticket order; the section is then stored with
 //                   16-byte writes straight into the final stream.
-//   decode_kernel   grid-stride over blocks; each block's offset is read
-//                   from the directory, its decode table (2048 x u32) is
-//                   built in LDS and the 64 states decode forwards.
-//   encode_kernel<REDUCE>  pass 1 decodes block b of every input in lock
-//                   step round by round and adds in binary32 in input order.
+//   decode_kernel   resident waves take blocks by ticket; each block's
+//                   offset is read from the directory, its decode table
+//                   (2048 x u32) is built in LDS, its words are staged
+//                   through an LDS ring and the 64 states decode forwards.
+//   reduce_decode_kernel + encode_kernel (fused reduce)  one workgroup per
+//                   output block decodes block b of up to eight inputs in
+//                   parallel waves, round by round, and a further wave adds
+//                   them in binary32 in input order and splits the rounded
+//                   result (raw plane, histogram); the coding pass of
+//                   encode_kernel then runs over the reduced tensor.
+//   split-send producer  encode_kernel with write-through stores and
+//                   per-chunk completion counters.
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -60,13 +67,8 @@ struct EncodeArgs {
   uint64_t *status;         // workspace: look-back status per block
   uint32_t *chunk_cnt;      // workspace: [2 * chunks] completion counters
   // fused reduce only
-  int n_in;
-  const uint8_t *ins[kMaxInputs];
-  uint64_t in_bytes[kMaxInputs];
-  const uint8_t *local_raw;
-  uint8_t *ybuf;            // reduced tensor re-read by pass 2 (large blocks)
-  uint8_t *yout;            // caller's copy of the reduced tensor (may be null)
-  uint32_t *dstatus;
+  const uint8_t *ybuf;      // the reduced tensor: source of both passes
+  const uint32_t *hist_in;  // [n_blocks][256] symbol histograms of the reduced tensor
   // small-block path: per-workgroup overflow slots for the staged words
   uint16_t *slots;
   uint32_t slot_words;
@@ -231,6 +233,14 @@ __device__ inline void store_words(uint8_t *base, uint64_t first, uint32_t valid
   }
 }
 
+// LDS traffic of one wave is processed in order: between its own stores and
+// loads only the compiler has to be kept from reordering (no workgroup
+// barrier, so the table build also runs in one wave of a larger group).
+__device__ __forceinline__ void wave_lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
 // ---------------------------------------------------------------------------
 // Decode side: table of one coded block -> 2048-entry lookup table in LDS.
 // Entry for slot: f | (slot - cum) << 12 | sym << 24.
@@ -271,7 +281,7 @@ __device__ bool build_lut(const uint8_t *sec, uint64_t sec_len, uint32_t *lut, u
     f_s[4 * lane + q] = (uint16_t)f[q];
     c += f[q];
   }
-  __syncthreads();
+  wave_lds_fence();
   // lane fills slots 32 lane .. 32 lane + 31: find the owner of the first one
   uint32_t slot = 32 * lane;
   uint32_t lo = 0, hi = 255;  // largest s with cum[s] <= slot
@@ -292,35 +302,9 @@ __device__ bool build_lut(const uint8_t *sec, uint64_t sec_len, uint32_t *lut, u
     }
     lut[slot] = fs | ((slot - c0) << 12) | (s << 24);
   }
-  __syncthreads();
+  wave_lds_fence();
   k_out = k;
   return true;
-}
-
-// One decode sub-step of one lane; returns the symbol.
-__device__ inline uint32_t decode_step(uint32_t &x, bool valid, const uint32_t *lut, const uint16_t *words,
-                                       uint32_t &p, uint32_t w_avail, bool &bad) {
-  uint32_t s = 0;
-  if (valid) {
-    uint32_t e = lut[x & (kM - 1)];
-    uint32_t f = e & 0xFFFu;
-    uint32_t bias = (e >> 12) & 0x7FFu;
-    s = e >> 24;
-    x = __umul24(f, x >> kProbBits) + bias;
-  }
-  bool need = valid && x < kStateLo;
-  uint64_t m = __ballot(need);
-  if (need) {
-    uint32_t idx = p + mbcnt(m);
-    uint32_t w = 0;
-    if (idx < w_avail)
-      w = words[idx];
-    else
-      bad = true;
-    x = (x << 16) | w;
-  }
-  p += (uint32_t)__popcll(m);
-  return s;
 }
 
 // ---------------------------------------------------------------------------
@@ -448,15 +432,6 @@ __device__ void publish_chunk(uint32_t *cnt, uint32_t need, uint32_t *flag, uint
   if (lane_id() == 0 && __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) + 1 == need)
     __hip_atomic_store(flag, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
-
-// Fused reduce, pass 1 helpers: per-input state of the block being reduced.
-struct InBlock {
-  const uint8_t *sec;
-  const uint16_t *words;
-  const uint8_t *raw_plane;
-  uint32_t w_avail;
-  uint32_t stored;
-};
 
 template <int DT>
 __device__ inline float to_f32(uint32_t w) {
@@ -729,136 +704,9 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         if (full < rounds) partial_round();
       }
     } else {
-      // fused reduce: decode block b of every input, add in order, round
-      uint32_t *luts = (uint32_t *)(smem + kEncTableBytes + kHistBytes);
-      uint16_t *cum_s = (uint16_t *)(smem + kEncTableBytes + kHistBytes + a.n_in * kLutBytes);
-      uint16_t *f_s = cum_s + 256;
-      InBlock ib[kMaxInputs];
-      uint32_t x[kMaxInputs], p[kMaxInputs];
-      bool bad = false;
-#pragma unroll
-      for (int i = 0; i < kMaxInputs; ++i) {
-        x[i] = kStateLo;
-        p[i] = 0;
-        ib[i].sec = nullptr;
-        ib[i].words = nullptr;
-        ib[i].raw_plane = nullptr;
-        ib[i].w_avail = 0;
-        ib[i].stored = 1;
-        if (i < a.n_in) {
-          const uint8_t *s = a.ins[i];
-          const uint64_t total = ld64(s + 24);
-          const uint32_t be = ld32(s + 8), nb = ld32(s + 12);
-          bool ok = a.in_bytes[i] >= kHeaderBytes && ld32(s) == kMagic && s[4] == kVersion && s[5] == DT &&
-                    s[6] == kProbBits && s[7] == 0 && be == a.block_elems && nb == g.n_blocks &&
-                    ld64(s + 16) == chunk_n && total <= a.in_bytes[i] && total >= g.coded_off;
-          uint64_t start = 0, end = 0;
-          uint32_t d = 0;
-          if (ok) {
-            d = ld32(s + kHeaderBytes + 4 * lb);
-            start = lb ? 16ull * (ld32(s + kHeaderBytes + 4 * (lb - 1)) & ~kStoredBit) : 0;
-            end = 16ull * (d & ~kStoredBit);
-            ok = end >= start && g.coded_off + end <= total;
-          }
-          if (ok) {
-            ib[i].sec = s + g.coded_off + start;
-            ib[i].raw_plane = s + g.raw_off;
-            ib[i].stored = d >> 31;
-            if (ib[i].stored) {
-              ok = end - start >= n_b;
-            } else {
-              uint32_t k = 0;
-              ok = build_lut(ib[i].sec, end - start, luts + i * kM, cum_s, f_s, k);
-              if (ok) {
-                k = uniform(k);
-                x[i] = ((const uint32_t *)ib[i].sec)[lane];
-                ok = !__any(x[i] < kStateLo || x[i] >= 0x80000000u);
-                ib[i].words = (const uint16_t *)(ib[i].sec + kSectionFixed + 2 * k);
-                ib[i].w_avail = (uint32_t)((end - start - kSectionFixed - 2 * k) / 2);
-              }
-            }
-          }
-          if (!ok) {
-            bad = true;
-            ib[i].stored = 1;
-            ib[i].sec = nullptr;
-          }
-        }
-      }
-      __syncthreads();
-      for (uint32_t r = 0; r < rounds; ++r) {
-        uint32_t i0 = r * kRound + kPerLane * lane;
-        uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
-        float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-#pragma unroll
-        for (int i = 0; i < kMaxInputs; ++i) {
-          if (i < a.n_in) {
-            uint32_t sym[2] = {0, 0};
-            if (ib[i].stored) {
-              if (ib[i].sec != nullptr && valid > 0) {
-#pragma unroll
-                for (uint32_t q = 0; q < 8; ++q)
-                  if (q < valid) sym[q >> 2] |= (uint32_t)ib[i].sec[i0 + q] << (8 * (q & 3));
-              }
-            } else {
-#pragma unroll
-              for (uint32_t t = 0; t < kPerLane; ++t) {
-                uint32_t s = decode_step(x[i], t < valid, luts + i * kM, ib[i].words, p[i], ib[i].w_avail, bad);
-                sym[t >> 2] |= s << (8 * (t & 3));
-              }
-            }
-            uint32_t raw[6] = {0, 0, 0, 0, 0, 0};
-            if (valid > 0 && ib[i].raw_plane != nullptr) load_raw<E>(ib[i].raw_plane, blk0 + i0, valid, raw);
-            uint32_t w[NW];
-            merge_group<E>(sym, raw, w);
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-              uint32_t wq = (E == 2) ? ((w[q >> 1] >> (16 * (q & 1))) & 0xFFFFu) : w[q];
-              float v = to_f32<DT>(wq);
-              acc[q] = (i == 0) ? v : acc[q] + v;
-            }
-          }
-        }
-        Group gr;
-        gr.sym[0] = gr.sym[1] = 0;
-        if (valid > 0) {
-          if (a.local_raw != nullptr) {
-            uint32_t w[NW];
-            load_words<E>(a.local_raw, blk0 + i0, valid, w);
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-              uint32_t wq = (E == 2) ? ((w[q >> 1] >> (16 * (q & 1))) & 0xFFFFu) : w[q];
-              acc[q] = acc[q] + to_f32<DT>(wq);
-            }
-          }
-          uint32_t w[NW];
-#pragma unroll
-          for (int q = 0; q < NW; ++q) w[q] = 0;
-#pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            uint32_t y = from_f32<DT>(acc[q]);
-            if (E == 2)
-              w[q >> 1] |= y << (16 * (q & 1));
-            else
-              w[q] = y;
-          }
-          if (a.yout != nullptr) store_words<E>(a.yout, blk0 + i0, valid, w);
-          if (a.ybuf != a.yout) store_words<E>(a.ybuf, blk0 + i0, valid, w);
-          split_group<E>(w, gr);
-          if (valid < 8) {
-            uint64_t keep = (1ull << (8 * valid)) - 1;
-            uint64_t v = ((uint64_t)gr.sym[1] << 32 | gr.sym[0]) & keep;
-            gr.sym[0] = (uint32_t)v;
-            gr.sym[1] = (uint32_t)(v >> 32);
-          }
-          store_raw<E, SYS>(raw_plane, blk0 + i0, valid, gr);
-          hist_add8(h, gr, valid);
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < kMaxInputs; ++i)
-        if (i < a.n_in && !ib[i].stored && x[i] != kStateLo) bad = true;
-      if (__any(bad) && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
+      // fused reduce: the decode-reduce kernel left the reduced tensor (the
+      // source of the coding pass), the raw plane and this block's histogram
+      for (uint32_t sy = lane; sy < 256; sy += 64) hist[sy] = a.hist_in[(uint64_t)b * 256 + sy];
     }
 
     if (last_in_chunk && lane < 16) {
@@ -1390,6 +1238,236 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// reduce_decode_kernel: the decode and reduce half of the fused reduce
+// (section 3.4).  One workgroup per output block, one wave per input of a
+// group of up to 8 inputs plus one reducing wave.  Input wave i decodes block
+// b of its stream round by round into an LDS slab (its own lookup table and
+// word ring, as in decode_kernel); after every round the reducing wave adds
+// the slabs in input order in fp32, continuing the partial sums of earlier
+// groups.  The group that finishes the sum adds the local contribution,
+// rounds to the element type and writes the reduced tensor, the raw plane
+// of the output stream and the block's symbol histogram; encode_kernel then
+// codes the reduced tensor from there.  Slabs are double-buffered, so one
+// barrier per round suffices.
+// ---------------------------------------------------------------------------
+constexpr int kReduceGroup = 8;
+constexpr uint32_t kDecLds = kLutBytes + kRingBytes + kRingMirror;  // per decoding wave
+
+struct ReduceArgs {
+  const uint8_t *ins[kReduceGroup];
+  uint64_t in_bytes[kReduceGroup];
+  int n_in;              // inputs of this group
+  int first;             // this group starts the sums
+  int last;              // this group ends them
+  const float *acc_in;   // partial sums of the groups before (first == 0)
+  float *acc_out;        // partial sums for the next group (last == 0)
+  const uint8_t *local_raw;
+  uint64_t n;
+  uint32_t block_elems;
+  uint8_t *out_raw_plane;  // raw plane of the output stream
+  uint8_t *ybuf;           // reduced tensor, read again by the coding pass
+  uint8_t *yout;           // caller's copy of it (may be null or ybuf)
+  uint32_t *hist_out;      // [n_blocks][256]
+  uint32_t *dstatus;
+};
+
+uint32_t reduce_lds(int n_in, uint32_t E) { return n_in * (kDecLds + 2 * kRound * E) + kHistBytes; }
+
+template <int DT>
+__global__ void __launch_bounds__(64 * (kReduceGroup + 1)) reduce_decode_kernel(ReduceArgs a) {
+  constexpr int E = (DT == 2) ? 4 : 2;
+  constexpr int NW = 4 * (E / 2);
+  extern __shared__ __align__(16) uint8_t smem_base[];
+  const uint32_t wave = threadIdx.x >> 6;
+  const uint32_t lane = lane_id();
+  const int n_in = a.n_in;
+  const bool decoder = (int)wave < n_in;
+  uint8_t *slabs = smem_base + n_in * kDecLds;  // [2][n_in][512 elements]
+  constexpr uint32_t kSlab = kRound * E;
+  uint32_t *hist = (uint32_t *)(slabs + 2 * n_in * kSlab);
+  const uint32_t be = a.block_elems;
+  const uint32_t b = blockIdx.x;
+  const uint64_t blk0 = (uint64_t)b * be;
+  const uint32_t n_b = (uint32_t)((a.n - blk0) < be ? (a.n - blk0) : be);
+  const uint32_t rounds = (n_b + kRound - 1) / kRound;
+  const uint32_t full = n_b / kRound;
+
+  // ---- decoding waves: block b of input `wave` ----
+  uint32_t *lut = (uint32_t *)(smem_base + wave * kDecLds);
+  uint8_t *ring = smem_base + wave * kDecLds + kLutBytes;
+  enum : uint32_t { kBad = 0, kStored = 1, kCoded = 2 };
+  uint32_t mode = kBad;
+  const uint8_t *sec = nullptr, *raw_plane = nullptr;
+  uint32_t x = kStateLo, x0 = kStateLo, p = 0, rb = 0, wb = 0, w_avail = 0;
+  Ring rg;
+  rg.written = 0;
+  rg.len = 16;
+  rg.pv = make_uint4(0, 0, 0, 0);
+  if (decoder) {
+    const uint8_t *s = a.ins[wave];
+    bool ok = a.in_bytes[wave] >= kHeaderBytes;
+    uint64_t total = 0;
+    Geom g = make_geom(a.n, be, E);
+    if (ok) {
+      total = ld64(s + 24);
+      ok = ld32(s) == kMagic && s[4] == kVersion && s[5] == DT && s[6] == kProbBits && s[7] == 0 &&
+           ld32(s + 8) == be && ld32(s + 12) == g.n_blocks && ld64(s + 16) == a.n && total <= a.in_bytes[wave] &&
+           total >= g.coded_off;
+    }
+    uint64_t start = 0, end = 0;
+    uint32_t d = 0;
+    if (ok) {
+      d = ld32(s + kHeaderBytes + 4 * b);
+      start = b ? 16ull * (ld32(s + kHeaderBytes + 4 * (b - 1)) & ~kStoredBit) : 0;
+      end = 16ull * (d & ~kStoredBit);
+      ok = end >= start && g.coded_off + end <= total;
+    }
+    if (ok) {
+      sec = s + g.coded_off + start;
+      raw_plane = s + g.raw_off;
+      const uint32_t len = (uint32_t)(end - start);
+      if (d >> 31) {
+        ok = len >= n_b;
+        mode = kStored;
+      } else {
+        uint32_t k = 0;
+        ok = build_lut(sec, len, lut, (uint16_t *)ring, (uint16_t *)ring + 256, k);
+        if (ok) {
+          mode = kCoded;
+          k = uniform(k);
+          x = x0 = ((const uint32_t *)sec)[lane];
+          wb = kSectionFixed + 2 * k;
+          w_avail = (len - wb) / 2;
+          rb = wb & (kRingBytes - 1);
+          rg.len = len;
+          rg.written = wb & ~15u;
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            const uint32_t o = rg.written + 16 * lane;
+            ring_put(ring, o & (kRingBytes - 1), ring_fetch(sec, o, len));
+            rg.written += kChunkBytes;
+          }
+          rg.pv = ring_fetch(sec, rg.written + 16 * lane, len);
+        }
+      }
+    }
+    if (!ok) {
+      mode = kBad;
+      if (lane == 0) report(a.dstatus, UZIP_ECORRUPT);
+    }
+  } else {
+    for (uint32_t i = lane; i < kHistReplicas * kHistStride; i += 64) hist[i] = 0;
+  }
+  uint32_t *h = hist + (lane & (kHistReplicas - 1)) * kHistStride;
+  __syncthreads();
+
+  for (uint32_t r = 0; r < rounds; ++r) {
+    uint8_t *slab = slabs + (r & 1) * n_in * kSlab;
+    const uint32_t i0 = r * kRound + kPerLane * lane;
+    const uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
+    if (decoder) {
+      uint32_t w[NW];
+#pragma unroll
+      for (int q = 0; q < NW; ++q) w[q] = 0;
+      if (mode == kCoded) {
+        ring_maintain(rg, ring, sec, wb + 2 * p);
+        uint32_t e[kPerLane];
+        if (r < full) {
+#pragma unroll
+          for (uint32_t t = 0; t < kPerLane; ++t) e[t] = decode_step_ring<true>(x, true, lut, ring, rb, p);
+        } else {
+#pragma unroll
+          for (uint32_t t = 0; t < kPerLane; ++t) e[t] = decode_step_ring<false>(x, t < valid, lut, ring, rb, p);
+        }
+        uint32_t raw[6] = {0, 0, 0, 0, 0, 0};
+        load_raw<E>(raw_plane, blk0 + i0, valid, raw);
+        merge_entries<E>(e, raw, w);
+      } else if (mode == kStored && valid > 0) {
+        uint32_t sym[2] = {0, 0};
+#pragma unroll
+        for (uint32_t q = 0; q < 8; ++q)
+          if (q < valid) sym[q >> 2] |= (uint32_t)sec[i0 + q] << (8 * (q & 3));
+        uint32_t raw[6] = {0, 0, 0, 0, 0, 0};
+        load_raw<E>(raw_plane, blk0 + i0, valid, raw);
+        merge_group<E>(sym, raw, w);
+      }
+      uint4 *dst = (uint4 *)(slab + wave * kSlab + kPerLane * E * lane);
+      dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
+      if (E == 4) dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
+    }
+    __syncthreads();
+    if (!decoder && valid > 0) {
+      float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      if (!a.first) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[q] = (uint32_t)q < valid ? a.acc_in[blk0 + i0 + q] : 0.f;
+      }
+      for (int i = 0; i < n_in; ++i) {
+        const uint4 *src = (const uint4 *)(slabs + (r & 1) * n_in * kSlab + i * kSlab + kPerLane * E * lane);
+        uint32_t w[NW];
+        const uint4 v0 = src[0];
+        w[0] = v0.x, w[1] = v0.y, w[2] = v0.z, w[3] = v0.w;
+        if (E == 4) {
+          const uint4 v1 = src[1];
+          w[4] = v1.x, w[5] = v1.y, w[6] = v1.z, w[7] = v1.w;
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const uint32_t wq = (E == 2) ? ((w[q >> 1] >> (16 * (q & 1))) & 0xFFFFu) : w[q];
+          const float v = to_f32<DT>(wq);
+          acc[q] = (a.first && i == 0) ? v : acc[q] + v;
+        }
+      }
+      if (a.last) {
+        if (a.local_raw != nullptr) {
+          uint32_t w[NW];
+          load_words<E>(a.local_raw, blk0 + i0, valid, w);
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const uint32_t wq = (E == 2) ? ((w[q >> 1] >> (16 * (q & 1))) & 0xFFFFu) : w[q];
+            acc[q] = acc[q] + to_f32<DT>(wq);
+          }
+        }
+        uint32_t w[NW];
+#pragma unroll
+        for (int q = 0; q < NW; ++q) w[q] = 0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const uint32_t y = from_f32<DT>(acc[q]);
+          if (E == 2)
+            w[q >> 1] |= y << (16 * (q & 1));
+          else
+            w[q] = y;
+        }
+        store_words<E>(a.ybuf, blk0 + i0, valid, w);
+        if (a.yout != nullptr && a.yout != a.ybuf) store_words<E>(a.yout, blk0 + i0, valid, w);
+        Group gr;
+        split_group<E>(w, gr);
+        store_raw<E>(a.out_raw_plane, blk0 + i0, valid, gr);
+        hist_add8(h, gr, valid);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          if ((uint32_t)q < valid) a.acc_out[blk0 + i0 + q] = acc[q];
+      }
+    }
+  }
+  __syncthreads();
+  if (decoder && mode == kCoded) {
+    const bool bad = x != kStateLo || p > w_avail || x0 < kStateLo || x0 >= 0x80000000u;
+    if (__any(bad) && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
+  }
+  if (!decoder && a.last) {
+    for (uint32_t sy = lane; sy < 256; sy += 64) {
+      uint32_t c = 0;
+#pragma unroll
+      for (uint32_t rep = 0; rep < kHistReplicas; ++rep) c += hist[rep * kHistStride + sy];
+      a.hist_out[(uint64_t)b * 256 + sy] = c;
+    }
+  }
+}
+
 // zero the ticket, the look-back status words and the chunk counters
 __global__ void clear_kernel(uint32_t *p, uint64_t words) {
   for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < words; i += (uint64_t)gridDim.x * blockDim.x)
@@ -1452,6 +1530,9 @@ uzip_status device_info(DeviceInfo &out) {
       (void)hipFuncSetAttribute(encode_kernel_ptr(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
     for (int k = 0; k < 3; ++k)
       (void)hipFuncSetAttribute(reduce_kernel_ptr(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
+    (void)hipFuncSetAttribute((const void *)reduce_decode_kernel<0>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
+    (void)hipFuncSetAttribute((const void *)reduce_decode_kernel<1>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
+    (void)hipFuncSetAttribute((const void *)reduce_decode_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
   });
   if (err != hipSuccess) return UZIP_EHIP;
   out = g_info[dev];
@@ -1487,8 +1568,8 @@ uint64_t n_slots(uint64_t n_blocks, uint32_t block_elems) {
 }
 
 // LDS bytes of encode_kernel
-uint32_t encode_lds(uint32_t block_elems, int n_in, bool small) {
-  const uint32_t pass1 = kHistBytes + (n_in > 0 ? n_in * kLutBytes + 1024 : 0);
+uint32_t encode_lds(uint32_t block_elems, bool small) {
+  const uint32_t pass1 = kHistBytes;
   const uint32_t pass2 = kStageHead + 2 * (small ? stage_words(block_elems) : word_cap(block_elems)) + kStageTail;
   return kTrashBytes + kEncTableBytes + (pass1 > pass2 ? pass1 : pass2);
 }
@@ -1510,6 +1591,22 @@ EncodeWs encode_ws(uint64_t n_blocks, uint64_t n_chunks, uint32_t block_elems, u
   return w;
 }
 
+// Fused reduce workspace: the coding pass's (status words, the reduced
+// tensor if the caller keeps no copy), the per-block histograms, and fp32
+// partial sums when the inputs come in more than one group.
+struct ReduceWs {
+  EncodeWs enc;
+  uint64_t hist_off, acc_off, total;
+};
+ReduceWs reduce_ws(uint64_t n_blocks, uint32_t block_elems, uint64_t n, uint32_t E, int n_in, bool need_y) {
+  ReduceWs w;
+  w.enc = encode_ws(n_blocks, 1, block_elems, need_y ? n * E : 0, true);
+  w.hist_off = w.enc.total;
+  w.acc_off = pad256(w.hist_off + 1024 * n_blocks);
+  w.total = pad256(w.acc_off + (n_in > kReduceGroup ? 4 * n : 0));
+  return w;
+}
+
 uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws, const EncodeWs &w,
                           const DeviceInfo &info, hipStream_t stream) {
   const bool small = !reduce && small_path(a.block_elems);
@@ -1521,7 +1618,7 @@ uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws
   a.wcap = word_cap(a.block_elems);
   a.lds_words = small ? stage_words(a.block_elems) : a.wcap;
   a.pass2_off = kEncTableBytes;
-  const uint32_t lds = encode_lds(a.block_elems, reduce ? a.n_in : 0, small);
+  const uint32_t lds = encode_lds(a.block_elems, small);
   if (lds > 160 * 1024) return UZIP_EINVAL;
   const void *fn = reduce ? reduce_kernel_ptr((int)dt)
                           : encode_kernel_ptr((int)dt * 4 + (a.flags != nullptr ? 2 : 0) + (small ? 1 : 0));
@@ -1567,8 +1664,7 @@ size_t uzip_workspace_size(int op, uzip_dtype dtype, uint64_t n_elems, uint32_t 
     case UZIP_OP_REDUCE: {
       const uint64_t n_in = aux & 0xFFFFu;
       if (n_in < 1 || n_in > kMaxInputs) return 0;
-      const uint64_t y = (aux & UZIP_WS_NO_OUT_RAW) ? n_elems * E : 0;
-      return (size_t)encode_ws(nb, 1, be, y, true).total;
+      return (size_t)reduce_ws(nb, be, n_elems, E, (int)n_in, (aux & UZIP_WS_NO_OUT_RAW) != 0).total;
     }
     default:
       return 0;
@@ -1704,8 +1800,43 @@ uzip_status uzip_reduce_fused(const void *const *d_in, const size_t *in_bytes, i
     return hipGetLastError() == hipSuccess ? UZIP_OK : UZIP_EHIP;
   }
   const bool need_y = d_out_raw == nullptr;
-  EncodeWs w = encode_ws(nb, 1, be, need_y ? n_elems * E : 0, true);
+  const ReduceWs w = reduce_ws(nb, be, n_elems, E, n_in, need_y);
   if (d_ws == nullptr || !aligned16(d_ws) || ws_bytes < w.total) return UZIP_ENOSPC;
+  uint8_t *ws = (uint8_t *)d_ws;
+  uint8_t *ybuf = d_out_raw ? (uint8_t *)d_out_raw : ws + w.enc.y_off;
+  const Geom g = make_geom(n_elems, be, E);
+  // decode + reduce, inputs in groups of up to kReduceGroup
+  const int groups = (n_in + kReduceGroup - 1) / kReduceGroup;
+  const void *dfn = dtype == UZIP_BF16   ? (const void *)reduce_decode_kernel<0>
+                    : dtype == UZIP_FP16 ? (const void *)reduce_decode_kernel<1>
+                                         : (const void *)reduce_decode_kernel<2>;
+  for (int gi = 0; gi < groups; ++gi) {
+    ReduceArgs r;
+    memset(&r, 0, sizeof(r));
+    const int i0 = gi * kReduceGroup;
+    r.n_in = n_in - i0 < kReduceGroup ? n_in - i0 : kReduceGroup;
+    for (int i = 0; i < r.n_in; ++i) {
+      r.ins[i] = (const uint8_t *)d_in[i0 + i];
+      r.in_bytes[i] = in_bytes[i0 + i];
+    }
+    r.first = gi == 0;
+    r.last = gi == groups - 1;
+    r.acc_in = (const float *)(ws + w.acc_off);
+    r.acc_out = (float *)(ws + w.acc_off);
+    r.local_raw = (const uint8_t *)d_local_raw;
+    r.n = n_elems;
+    r.block_elems = be;
+    r.out_raw_plane = (uint8_t *)d_out + g.raw_off;
+    r.ybuf = ybuf;
+    r.yout = (uint8_t *)d_out_raw;
+    r.hist_out = (uint32_t *)(ws + w.hist_off);
+    r.dstatus = d_status;
+    const uint32_t lds = reduce_lds(r.n_in, E);
+    void *args[] = {&r};
+    if (hipLaunchKernel(dfn, dim3((unsigned)nb), dim3(64 * (r.n_in + 1)), args, lds, stream) != hipSuccess)
+      return UZIP_EHIP;
+  }
+  // coding pass over the reduced tensor
   EncodeArgs a;
   memset(&a, 0, sizeof(a));
   a.n = n_elems;
@@ -1715,16 +1846,9 @@ uzip_status uzip_reduce_fused(const void *const *d_in, const size_t *in_bytes, i
   a.n_blocks = (uint32_t)nb;
   a.out = (uint8_t *)d_out;
   a.sizes = d_out_size;
-  a.n_in = n_in;
-  for (int i = 0; i < n_in; ++i) {
-    a.ins[i] = (const uint8_t *)d_in[i];
-    a.in_bytes[i] = in_bytes[i];
-  }
-  a.local_raw = (const uint8_t *)d_local_raw;
-  a.yout = (uint8_t *)d_out_raw;
-  a.ybuf = d_out_raw ? (uint8_t *)d_out_raw : (need_y ? (uint8_t *)d_ws + w.y_off : nullptr);
-  a.dstatus = d_status;
-  return launch_encode(a, dtype, true, (uint8_t *)d_ws, w, info, stream);
+  a.ybuf = ybuf;
+  a.hist_in = (const uint32_t *)(ws + w.hist_off);
+  return launch_encode(a, dtype, true, ws, w.enc, info, stream);
 }
 
 const char *uzip_status_str(uzip_status status) {

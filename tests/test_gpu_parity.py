@@ -231,6 +231,23 @@ def test_reduce_sixteen_inputs_with_stored_blocks(uz):
     assert np.array_equal(host_bits(raw, "bf16"), want_y)
 
 
+def test_reduce_two_uneven_input_groups(uz):
+    """Eleven inputs: decoded in a group of eight and a group of three; the
+    fp32 partial sums carry over between the groups in input order."""
+    n = 90_001
+    say("[parity] reduce n_in=11")
+    xs = [special_words("fp16", n, seed=400 + i) for i in range(11)]
+    streams = [ref.compress(v, "fp16", 65536) for v in xs]
+    local = special_words("fp16", n, seed=78)
+    out, size, raw, status = uz.reduce_fused([dev(s) for s in streams], "fp16", n, 65536,
+                                             local=to_dev_bits(local, "fp16"))
+    torch.cuda.synchronize()
+    want_s, want_y = ref.reduce(streams, "fp16", n, 65536, local=local)
+    assert int(status.item()) == 0
+    assert np.array_equal(out[:int(size.item())].cpu().numpy(), want_s)
+    assert np.array_equal(host_bits(raw, "fp16"), want_y)
+
+
 def test_reduce_eight_slices_share(uz):
     """Eight bf16 shares [tokens x 8192] with per-token scales (64 tokens)."""
     xs = W.reduce_slices(n_in=8, tokens=64, hidden=8192, seed=5)

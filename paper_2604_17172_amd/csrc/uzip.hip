@@ -366,7 +366,10 @@ __device__ void build_enc_table(const uint32_t *hist, uint32_t n_b, uint4 *enc, 
       } else {
         // floor(x / f) = mulhi(x, m) >> (l - 1), m = ceil(2^(31+l) / f),
         // exact for x < 2^31 (division by invariant integers)
-        uint32_t m = (uint32_t)(((1ull << (31 + l)) + f - 1) / f);
+        // 2^(31+l) / f in binary64 is correctly rounded and a non-integer
+        // quotient is at least 1/f from the next integer, far more than half
+        // an ulp (< 2^-20), so the ceiling of the rounded quotient is exact
+        uint32_t m = (uint32_t)ceil((double)(1ull << (31 + l)) / (double)f);
         e = make_uint4(m, f << 20, (kM - f) | ((l - 1) << 24), cum);
       }
       enc[4 * lane + q] = e;
@@ -617,6 +620,10 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     uint32_t *h = hist + (lane & (kHistReplicas - 1)) * kHistStride;
     SymRegs S;
 
+    // The first pass (memory-bound) runs at raised wave priority, the rest
+    // at normal: a SIMD's two waves then overlap streaming with coding
+    // instead of the older wave winning both.
+    __builtin_amdgcn_s_setprio(1);
     // ---- pass 1: split, raw plane to its final place, histogram ----
     for (uint32_t i = lane; i < kHistReplicas * kHistStride; i += 64) hist[i] = 0;
     __syncthreads();
@@ -719,6 +726,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
       publish_chunk(&a.chunk_cnt[2 * chunk], g.n_blocks, &a.flags[2 * chunk], a.epoch);
     }
 
+    __builtin_amdgcn_s_setprio(0);
     // ---- table ----
     Table t;
     build_enc_table(hist, n_b, enc, t);
@@ -1062,6 +1070,32 @@ __device__ __forceinline__ void ring_maintain(Ring &rg, uint8_t *ring, const uin
   rg.pv = ring_fetch(sec, rg.written + 16 * lane, rg.len);
 }
 
+// The decoder's ring: a chunk is fetched two rounds before it is stored, by
+// two alternating register slots, so that a new chunk's memory latency is
+// covered by two rounds of decoding instead of one.  Every round stores its
+// slot's chunk and fetches the next chunk if the ring will have room for it
+// when it is stored (front < cur + 3 chunks), else re-fetches the newest
+// chunk (a repeat store of the same bytes): with at most one chunk consumed
+// per round, the chunk at front - 1 KiB is always the newest one that is not
+// overwritten, the stored frontier stays at least 1 KiB ahead of the words
+// a round reads, and a store never overwrites unread words.
+struct Ring2 {
+  uint32_t len;         // section length (a multiple of 16)
+  uint32_t front;       // section offset of the next chunk to fetch
+  uint32_t pos[2];      // section offsets of the chunks in pv[0], pv[1]
+  uint4 pv[2];
+};
+
+template <int X>
+__device__ __forceinline__ void ring2_round(Ring2 &rg, uint8_t *ring, const uint8_t *sec, uint32_t cur) {
+  const uint32_t lane = lane_id();
+  ring_put(ring, (rg.pos[X] + 16 * lane) & (kRingBytes - 1), rg.pv[X]);
+  asm volatile("" ::: "memory");  // the ring stores stay before the round's ring reads
+  rg.front += rg.front < cur + 3 * kChunkBytes ? kChunkBytes : 0;
+  rg.pos[X] = rg.front - kChunkBytes;
+  rg.pv[X] = ring_fetch(sec, rg.pos[X] + 16 * lane, rg.len);
+}
+
 template <int E>
 __device__ inline void load_raw_full(const uint8_t *plane, uint64_t first, uint32_t raw[6]) {
   const uint2 *q = (const uint2 *)(plane + (uint64_t)(E - 1) * first);
@@ -1162,16 +1196,19 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
     const uint32_t x0 = x;  // checked at the end of the block: no wait for it here
     const uint32_t wb = kSectionFixed + 2 * k;  // section offset of word 0
     const uint32_t w_avail = (len - wb) / 2;
-    Ring rg;
+    Ring2 rg;
     rg.len = len;
-    rg.written = wb & ~15u;
+    {
+      const uint32_t base = wb & ~15u;
+      uint4 v[3];
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const uint32_t o = rg.written + 16 * lane;
-      ring_put(ring, o & (kRingBytes - 1), ring_fetch(sec, o, len));
-      rg.written += kChunkBytes;
+      for (int c = 0; c < 3; ++c) v[c] = ring_fetch(sec, base + c * kChunkBytes + 16 * lane, len);
+#pragma unroll
+      for (int c = 0; c < 3; ++c) ring_put(ring, (base + c * kChunkBytes + 16 * lane) & (kRingBytes - 1), v[c]);
+      rg.front = base + 3 * kChunkBytes;
+      rg.pos[0] = rg.pos[1] = base + 2 * kChunkBytes;
+      rg.pv[0] = rg.pv[1] = v[2];
     }
-    rg.pv = ring_fetch(sec, rg.written + 16 * lane, len);
     __syncthreads();
     uint32_t p = 0, rb = wb & (kRingBytes - 1);
     const uint32_t full = n_b / kRound;
@@ -1189,7 +1226,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
     // full rounds, two per iteration with ping-pong raw registers: every
     // load is issued a round before its use and no register is copied
     for (; r + 2 <= full; r += 2) {
-      ring_maintain(rg, ring, sec, wb + 2 * p);
+      ring2_round<0>(rg, ring, sec, wb + 2 * p);
       load_raw_full<E>(rawp, (r + 1) * kRound + kPerLane * lane, rawB);
       uint32_t e[kPerLane];
 #pragma unroll
@@ -1198,7 +1235,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
       merge_entries<E>(e, rawA, w);
       store_words<E>(outp, r * kRound + kPerLane * lane, 8, w);
 
-      ring_maintain(rg, ring, sec, wb + 2 * p);
+      ring2_round<1>(rg, ring, sec, wb + 2 * p);
       const uint32_t rn = (r + 2 < full) ? r + 2 : r + 1;  // always a full round: no branch around the load
       load_raw_full<E>(rawp, rn * kRound + kPerLane * lane, rawA);
 #pragma unroll
@@ -1206,8 +1243,8 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
       merge_entries<E>(e, rawB, w);
       store_words<E>(outp, (r + 1) * kRound + kPerLane * lane, 8, w);
     }
-    if (r < full) {  // odd number of full rounds: rawA holds round r
-      ring_maintain(rg, ring, sec, wb + 2 * p);
+    if (r < full) {  // odd number of full rounds: rawA holds round r (r even)
+      ring2_round<0>(rg, ring, sec, wb + 2 * p);
       uint32_t e[kPerLane];
 #pragma unroll
       for (uint32_t t = 0; t < kPerLane; ++t) e[t] = decode_step_ring<true>(x, true, lut, ring, rb, p);
@@ -1217,7 +1254,10 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
       ++r;
     }
     if (r < rounds) {  // partial last round
-      ring_maintain(rg, ring, sec, wb + 2 * p);
+      if (r & 1)
+        ring2_round<1>(rg, ring, sec, wb + 2 * p);
+      else
+        ring2_round<0>(rg, ring, sec, wb + 2 * p);
       const uint32_t i0 = r * kRound + kPerLane * lane;
       const uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
       uint32_t e[kPerLane];

@@ -214,12 +214,20 @@ __device__ inline void merge_group(const uint32_t sym[2], const uint32_t raw[6],
     merge32(sym, raw, w);
 }
 
-template <int E>
+// Eight elements of one lane out to a tensor.  NT: full groups with
+// streaming (non-temporal) stores, for output nothing here reads back.
+template <int E, bool NT = false>
 __device__ inline void store_words(uint8_t *base, uint64_t first, uint32_t valid, const uint32_t w[4 * (E / 2)]) {
   if (valid >= 8) {
-    uint4 *p = (uint4 *)(base + first * E);
-    p[0] = make_uint4(w[0], w[1], w[2], w[3]);
-    if (E == 4) p[1] = make_uint4(w[4], w[5], w[6], w[7]);
+    typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+    v4u *p = (v4u *)(base + first * E);
+    if (NT) {
+      __builtin_nontemporal_store((v4u){w[0], w[1], w[2], w[3]}, p);
+      if (E == 4) __builtin_nontemporal_store((v4u){w[4], w[5], w[6], w[7]}, p + 1);
+    } else {
+      p[0] = (v4u){w[0], w[1], w[2], w[3]};
+      if (E == 4) p[1] = (v4u){w[4], w[5], w[6], w[7]};
+    }
   } else {
 #pragma unroll
     for (uint32_t q = 0; q < 8; ++q) {
@@ -991,7 +999,7 @@ constexpr uint32_t kChunkBytes = 1024;
 // the next unread word, uniform); lanes that need no word keep their state.
 // Positions past the section's words stay inside the ring and are caught
 // once per block by p <= w_avail.
-template <bool FULL>
+template <bool FULL, uint32_t RB = kRingBytes, bool MIRROR = true>
 __device__ __forceinline__ uint32_t decode_step_ring(uint32_t &x, bool valid, const uint32_t *lut,
                                                      const uint8_t *ring, uint32_t &rb, uint32_t &p) {
   uint32_t e = 0;
@@ -1002,12 +1010,12 @@ __device__ __forceinline__ uint32_t decode_step_ring(uint32_t &x, bool valid, co
   const bool need = (FULL || valid) && x < kStateLo;
   const uint64_t m = __ballot(need);
   const uint32_t rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-  uint32_t w = *(const uint16_t *)(ring + rb + 2 * rank);
+  uint32_t w = *(const uint16_t *)(ring + (MIRROR ? rb + 2 * rank : (rb + 2 * rank) & (RB - 1)));
   asm volatile("" : "+v"(w));  // keep the read unconditional: no exec-mask branch around it
   x = need ? ((x << 16) | w) : x;
   const uint32_t c = (uint32_t)__popcll(m);
   p += c;
-  rb = (rb + 2 * c) & (kRingBytes - 1);
+  rb = (rb + 2 * c) & (RB - 1);
   return e;
 }
 
@@ -1070,30 +1078,33 @@ __device__ __forceinline__ void ring_maintain(Ring &rg, uint8_t *ring, const uin
   rg.pv = ring_fetch(sec, rg.written + 16 * lane, rg.len);
 }
 
-// The decoder's ring: a chunk is fetched two rounds before it is stored, by
-// two alternating register slots, so that a new chunk's memory latency is
-// covered by two rounds of decoding instead of one.  Every round stores its
-// slot's chunk and fetches the next chunk if the ring will have room for it
-// when it is stored (front < cur + 3 chunks), else re-fetches the newest
-// chunk (a repeat store of the same bytes): with at most one chunk consumed
-// per round, the chunk at front - 1 KiB is always the newest one that is not
-// overwritten, the stored frontier stays at least 1 KiB ahead of the words
-// a round reads, and a store never overwrites unread words.
-struct Ring2 {
-  uint32_t len;         // section length (a multiple of 16)
-  uint32_t front;       // section offset of the next chunk to fetch
-  uint32_t pos[2];      // section offsets of the chunks in pv[0], pv[1]
-  uint4 pv[2];
+// decode_kernel's ring: 2 KB without a mirror (8 KB table + 2 KB ring =
+// 10 KB of LDS per wave, 16 waves per CU), 512-byte chunks read with one
+// 8-byte load per lane.  A half round (4 sub-steps) reads at most 512 bytes;
+// each half round stores the chunk its slot fetched a round earlier and
+// fetches the next chunk if it will fit when stored (front < cur + 1536),
+// else re-fetches the newest chunk.  Two slots alternate by half round.  The
+// stored frontier then stays at least 512 bytes ahead of the words a half
+// round reads, and a store never overwrites unread words.
+constexpr uint32_t kDecRingBytes = 2048;
+constexpr uint32_t kDecChunk = 512;
+
+struct RingD {
+  uint32_t len;
+  uint32_t front;
+  uint32_t pos[2];
+  uint2 pv[2];
 };
 
 template <int X>
-__device__ __forceinline__ void ring2_round(Ring2 &rg, uint8_t *ring, const uint8_t *sec, uint32_t cur) {
+__device__ __forceinline__ void ringd_half(RingD &rg, uint8_t *ring, const uint8_t *sec, uint32_t cur) {
   const uint32_t lane = lane_id();
-  ring_put(ring, (rg.pos[X] + 16 * lane) & (kRingBytes - 1), rg.pv[X]);
-  asm volatile("" ::: "memory");  // the ring stores stay before the round's ring reads
-  rg.front += rg.front < cur + 3 * kChunkBytes ? kChunkBytes : 0;
-  rg.pos[X] = rg.front - kChunkBytes;
-  rg.pv[X] = ring_fetch(sec, rg.pos[X] + 16 * lane, rg.len);
+  *(uint2 *)(ring + ((rg.pos[X] + 8 * lane) & (kDecRingBytes - 1))) = rg.pv[X];
+  asm volatile("" ::: "memory");  // the ring stores stay before the half round's ring reads
+  rg.front += rg.front < cur + 3 * kDecChunk ? kDecChunk : 0;
+  rg.pos[X] = rg.front - kDecChunk;
+  const uint32_t o = rg.pos[X] + 8 * lane;
+  rg.pv[X] = *(const uint2 *)(sec + (o + 8 <= rg.len ? o : rg.len - 8));
 }
 
 template <int E>
@@ -1116,7 +1127,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
   constexpr int E = (DT == 2) ? 4 : 2;
   constexpr int NW = 4 * (E / 2);
   __shared__ uint32_t lut[kM];
-  __shared__ __align__(16) uint8_t ring[kRingBytes + kRingMirror];
+  __shared__ __align__(16) uint8_t ring[kDecRingBytes];
   // the table-build scratch (cum, f) lives in the ring before the ring fills
   uint16_t *cum_s = (uint16_t *)ring, *f_s = (uint16_t *)ring + 256;
   const uint32_t lane = lane_id();
@@ -1196,21 +1207,24 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
     const uint32_t x0 = x;  // checked at the end of the block: no wait for it here
     const uint32_t wb = kSectionFixed + 2 * k;  // section offset of word 0
     const uint32_t w_avail = (len - wb) / 2;
-    Ring2 rg;
+    RingD rg;
     rg.len = len;
     {
       const uint32_t base = wb & ~15u;
-      uint4 v[3];
+      uint2 v[3];
 #pragma unroll
-      for (int c = 0; c < 3; ++c) v[c] = ring_fetch(sec, base + c * kChunkBytes + 16 * lane, len);
+      for (int c = 0; c < 3; ++c) {
+        const uint32_t o = base + c * kDecChunk + 8 * lane;
+        v[c] = *(const uint2 *)(sec + (o + 8 <= len ? o : len - 8));
+      }
 #pragma unroll
-      for (int c = 0; c < 3; ++c) ring_put(ring, (base + c * kChunkBytes + 16 * lane) & (kRingBytes - 1), v[c]);
-      rg.front = base + 3 * kChunkBytes;
-      rg.pos[0] = rg.pos[1] = base + 2 * kChunkBytes;
+      for (int c = 0; c < 3; ++c) *(uint2 *)(ring + ((base + c * kDecChunk + 8 * lane) & (kDecRingBytes - 1))) = v[c];
+      rg.front = base + 3 * kDecChunk;
+      rg.pos[0] = rg.pos[1] = base + 2 * kDecChunk;
       rg.pv[0] = rg.pv[1] = v[2];
     }
     __syncthreads();
-    uint32_t p = 0, rb = wb & (kRingBytes - 1);
+    uint32_t p = 0, rb = wb & (kDecRingBytes - 1);
     const uint32_t full = n_b / kRound;
     uint8_t *outp = a.out + blk0 * E;
     const uint8_t *rawp = raw_plane + blk0 * (E - 1);
@@ -1226,43 +1240,52 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
     // full rounds, two per iteration with ping-pong raw registers: every
     // load is issued a round before its use and no register is copied
     for (; r + 2 <= full; r += 2) {
-      ring2_round<0>(rg, ring, sec, wb + 2 * p);
+      ringd_half<0>(rg, ring, sec, wb + 2 * p);
       load_raw_full<E>(rawp, (r + 1) * kRound + kPerLane * lane, rawB);
       uint32_t e[kPerLane];
 #pragma unroll
-      for (uint32_t t = 0; t < kPerLane; ++t) e[t] = decode_step_ring<true>(x, true, lut, ring, rb, p);
+      for (uint32_t t = 0; t < kPerLane; ++t) {
+        if (t == kPerLane / 2) ringd_half<1>(rg, ring, sec, wb + 2 * p);
+        e[t] = decode_step_ring<true, kDecRingBytes, false>(x, true, lut, ring, rb, p);
+      }
       uint32_t w[NW];
       merge_entries<E>(e, rawA, w);
-      store_words<E>(outp, r * kRound + kPerLane * lane, 8, w);
+      store_words<E, true>(outp, r * kRound + kPerLane * lane, 8, w);
 
-      ring2_round<1>(rg, ring, sec, wb + 2 * p);
+      ringd_half<0>(rg, ring, sec, wb + 2 * p);
       const uint32_t rn = (r + 2 < full) ? r + 2 : r + 1;  // always a full round: no branch around the load
       load_raw_full<E>(rawp, rn * kRound + kPerLane * lane, rawA);
 #pragma unroll
-      for (uint32_t t = 0; t < kPerLane; ++t) e[t] = decode_step_ring<true>(x, true, lut, ring, rb, p);
+      for (uint32_t t = 0; t < kPerLane; ++t) {
+        if (t == kPerLane / 2) ringd_half<1>(rg, ring, sec, wb + 2 * p);
+        e[t] = decode_step_ring<true, kDecRingBytes, false>(x, true, lut, ring, rb, p);
+      }
       merge_entries<E>(e, rawB, w);
-      store_words<E>(outp, (r + 1) * kRound + kPerLane * lane, 8, w);
+      store_words<E, true>(outp, (r + 1) * kRound + kPerLane * lane, 8, w);
     }
-    if (r < full) {  // odd number of full rounds: rawA holds round r (r even)
-      ring2_round<0>(rg, ring, sec, wb + 2 * p);
+    if (r < full) {  // odd number of full rounds: rawA holds round r
+      ringd_half<0>(rg, ring, sec, wb + 2 * p);
       uint32_t e[kPerLane];
 #pragma unroll
-      for (uint32_t t = 0; t < kPerLane; ++t) e[t] = decode_step_ring<true>(x, true, lut, ring, rb, p);
+      for (uint32_t t = 0; t < kPerLane; ++t) {
+        if (t == kPerLane / 2) ringd_half<1>(rg, ring, sec, wb + 2 * p);
+        e[t] = decode_step_ring<true, kDecRingBytes, false>(x, true, lut, ring, rb, p);
+      }
       uint32_t w[NW];
       merge_entries<E>(e, rawA, w);
-      store_words<E>(outp, r * kRound + kPerLane * lane, 8, w);
+      store_words<E, true>(outp, r * kRound + kPerLane * lane, 8, w);
       ++r;
     }
     if (r < rounds) {  // partial last round
-      if (r & 1)
-        ring2_round<1>(rg, ring, sec, wb + 2 * p);
-      else
-        ring2_round<0>(rg, ring, sec, wb + 2 * p);
+      ringd_half<0>(rg, ring, sec, wb + 2 * p);
       const uint32_t i0 = r * kRound + kPerLane * lane;
       const uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
       uint32_t e[kPerLane];
 #pragma unroll
-      for (uint32_t t = 0; t < kPerLane; ++t) e[t] = decode_step_ring<false>(x, t < valid, lut, ring, rb, p);
+      for (uint32_t t = 0; t < kPerLane; ++t) {
+        if (t == kPerLane / 2) ringd_half<1>(rg, ring, sec, wb + 2 * p);
+        e[t] = decode_step_ring<false, kDecRingBytes, false>(x, t < valid, lut, ring, rb, p);
+      }
       if (valid > 0) {
         uint32_t raw[6];
         load_raw<E>(raw_plane, blk0 + i0, valid, raw);

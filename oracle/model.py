@@ -19,11 +19,43 @@ M = 1 << 11
 L = 1 << 15
 LANES, PER_LANE = 64, 8
 ROUND = LANES * PER_LANE
-EB = {"bf16": 2, "fp16": 2, "fp32": 4}
-CODE = {"bf16": 0, "fp16": 1, "fp32": 2}
+EB = {"bf16": 2, "fp16": 2, "fp32": 4, "e4m3fn": 2, "e5m2": 2}
+CODE = {"bf16": 0, "fp16": 1, "fp32": 2, "e4m3fn": 3, "e5m2": 4}
+# FP8 value fields (sign, exponent bits, fraction bits)
+FP8_FIELDS = {"e4m3fn": (4, 3), "e5m2": (5, 2)}
+
+
+def fp8_pair_planes(dtype: str, w: int) -> tuple[int, int]:
+    """Section 4.1: two FP8 values in one 16-bit unit, their exponent fields
+    taken together as the 8-bit symbol.  Written from the value fields: for
+    e4m3fn the symbol is the two exponents; for e5m2 the two exponents'
+    top four bits, the lowest exponent bit going with sign and fraction."""
+    ebits, mbits = FP8_FIELDS[dtype]
+    sym = raw = 0
+    for k in range(2):
+        v = (w >> (8 * k)) & 0xFF
+        sign, exp, frac = v >> 7, (v >> mbits) & ((1 << ebits) - 1), v & ((1 << mbits) - 1)
+        keep = ebits - 4  # exponent bits that do not fit the symbol nibble
+        sym |= (exp >> keep) << (4 * k)
+        raw |= ((sign << 3) | ((exp & ((1 << keep) - 1)) << mbits) | frac) << (4 * k)
+    return sym, raw
+
+
+def fp8_pair_value(dtype: str, sym: int, raw: int) -> int:
+    ebits, mbits = FP8_FIELDS[dtype]
+    keep = ebits - 4
+    w = 0
+    for k in range(2):
+        s4, r4 = (sym >> (4 * k)) & 15, (raw >> (4 * k)) & 15
+        exp = (s4 << keep) | ((r4 >> mbits) & ((1 << keep) - 1))
+        v = ((r4 >> 3) << 7) | (exp << mbits) | (r4 & ((1 << mbits) - 1))
+        w |= v << (8 * k)
+    return w
 
 
 def to_planes(dtype: str, w: int) -> tuple[int, int]:
+    if dtype in FP8_FIELDS:
+        return fp8_pair_planes(dtype, w)
     bits = 8 * EB[dtype]
     full = (1 << bits) - 1
     r = ((w << 1) & full) | (w >> (bits - 1))
@@ -31,6 +63,8 @@ def to_planes(dtype: str, w: int) -> tuple[int, int]:
 
 
 def from_planes(dtype: str, sym: int, raw: int) -> int:
+    if dtype in FP8_FIELDS:
+        return fp8_pair_value(dtype, sym, raw)
     bits = 8 * EB[dtype]
     full = (1 << bits) - 1
     r = (sym << (bits - 8)) | raw

@@ -19,9 +19,10 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(_HERE, "uzip_ref.c")
 LIB_PATH = os.path.join(_HERE, "_build", "libuzip_ref.so")
 
-DTYPES = {"bf16": 0, "fp16": 1, "fp32": 2}
-ELEM_BYTES = {"bf16": 2, "fp16": 2, "fp32": 4}
-BITS_DTYPE = {"bf16": np.uint16, "fp16": np.uint16, "fp32": np.uint32}
+# FP8 formats are coded in pairs: one element = a 16-bit unit of two values
+DTYPES = {"bf16": 0, "fp16": 1, "fp32": 2, "e4m3fn": 3, "e5m2": 4}
+ELEM_BYTES = {"bf16": 2, "fp16": 2, "fp32": 4, "e4m3fn": 2, "e5m2": 2}
+BITS_DTYPE = {"bf16": np.uint16, "fp16": np.uint16, "fp32": np.uint32, "e4m3fn": np.uint16, "e5m2": np.uint16}
 
 REF_EINVAL, REF_ENOSPC, REF_ECORRUPT = -1, -2, -3
 

@@ -13,6 +13,17 @@
  *   exponent field; for fp16 the 5-bit exponent and the top 3 fraction
  *   bits); the low E-1 bytes are the raw sign+fraction part, stored as-is.
  *
+ *   FP8 pairs (section 4.1: two FP8 values packed in a 16-bit unit, their
+ *   exponent fields extracted jointly into one 8-bit symbol).  Element = the
+ *   16-bit unit v0 | v1 << 8 of two consecutive values.  From each value
+ *   byte, bits 6..3 go to the symbol and bit 7 (sign) with bits 2..0 to the
+ *   raw byte: symbol = n(v0) | n(v1) << 4 with n(v) = (v >> 3) & 15, raw =
+ *   r(v0) | r(v1) << 4 with r(v) = (v >> 7) << 3 | (v & 7).  For e4m3fn the
+ *   symbol nibbles are the two 4-bit exponent fields; for e5m2 (5-bit
+ *   exponent, 2-bit fraction) they are the top four exponent bits of each
+ *   value, and the lowest exponent bit travels in the raw byte with the
+ *   sign and fraction (our reading: 2 x 5 exponent bits do not fit a byte).
+ *
  *   Localized table (section 3.3.1).  Each block of n_b symbols gets its own
  *   table from its own histogram c[256]: with k present symbols and
  *   M = 2^11, f[s] = 1 + floor(c[s](M-k)/n_b) for present s (0 otherwise);
@@ -110,7 +121,22 @@ static void store_elem(void *out, int dtype, uint64_t i, uint32_t w) {
 /* ------------------------------------------------------------------ */
 /* Step 1: split a value into symbol (exponent byte) and raw part.      */
 /* ------------------------------------------------------------------ */
+static int is_fp8(int dtype) { return dtype == REF_E4M3FN || dtype == REF_E5M2; }
+
+/* one FP8 value byte: symbol nibble (bits 6..3), raw nibble (bit 7, bits 2..0) */
+static uint32_t fp8_sym_nibble(uint32_t v) { return (v >> 3) & 15u; }
+static uint32_t fp8_raw_nibble(uint32_t v) { return ((v >> 7) << 3) | (v & 7u); }
+static uint32_t fp8_value(uint32_t sym_nibble, uint32_t raw_nibble) {
+  return ((raw_nibble >> 3) << 7) | (sym_nibble << 3) | (raw_nibble & 7u);
+}
+
 void ref_split_word(int dtype, uint32_t w, uint32_t *sym, uint32_t *raw) {
+  if (is_fp8(dtype)) {
+    uint32_t v0 = w & 0xFFu, v1 = (w >> 8) & 0xFFu;
+    *sym = fp8_sym_nibble(v0) | (fp8_sym_nibble(v1) << 4);
+    *raw = fp8_raw_nibble(v0) | (fp8_raw_nibble(v1) << 4);
+    return;
+  }
   uint32_t bits = 8u * elem_bytes(dtype);
   uint64_t mask = (bits == 32u) ? 0xFFFFFFFFull : ((1ull << bits) - 1ull);
   uint64_t v = (uint64_t)w & mask;
@@ -120,6 +146,11 @@ void ref_split_word(int dtype, uint32_t w, uint32_t *sym, uint32_t *raw) {
 }
 
 uint32_t ref_merge_word(int dtype, uint32_t sym, uint32_t raw) {
+  if (is_fp8(dtype)) {
+    uint32_t v0 = fp8_value(sym & 15u, raw & 15u);
+    uint32_t v1 = fp8_value((sym >> 4) & 15u, (raw >> 4) & 15u);
+    return v0 | (v1 << 8);
+  }
   uint32_t bits = 8u * elem_bytes(dtype);
   uint64_t mask = (bits == 32u) ? 0xFFFFFFFFull : ((1ull << bits) - 1ull);
   uint64_t rot = ((uint64_t)sym << (bits - 8u)) | (uint64_t)raw;
@@ -308,7 +339,7 @@ int64_t ref_block_section(const void *in, uint64_t n, int dtype,
 
 int64_t ref_compress(const void *in, uint64_t n, int dtype,
                      uint32_t block_bytes, uint8_t *out, uint64_t out_cap) {
-  if (dtype < 0 || dtype > 2 || !valid_block_bytes(block_bytes)) return REF_EINVAL;
+  if (dtype < 0 || dtype > 4 || !valid_block_bytes(block_bytes)) return REF_EINVAL;
   uint32_t E = elem_bytes(dtype);
   uint64_t be = block_bytes / E;
   uint64_t nb = (n + be - 1) / be;

@@ -35,10 +35,15 @@
 extern "C" {
 #endif
 
-/* dtype codes used by the stream header */
+/* dtype codes used by the stream header.  The two FP8 formats (section
+ * 4.1) are coded as pairs: one codec element is a 16-bit unit holding two
+ * consecutive FP8 values (the first in the low byte), and element counts
+ * of FP8 streams count pairs. */
 #define REF_BF16 0
 #define REF_FP16 1
 #define REF_FP32 2
+#define REF_E4M3FN 3
+#define REF_E5M2 4
 
 /* error codes (negative returns) */
 #define REF_EINVAL (-1)

@@ -22,7 +22,7 @@ import torch
 from oracle import model, ref
 import workloads as W
 
-EB = {"bf16": 2, "fp16": 2, "fp32": 4}
+EB = {"bf16": 2, "fp16": 2, "fp32": 4, "e4m3fn": 2, "e5m2": 2}
 L_STATE = 1 << 15
 M = 2048
 
@@ -332,6 +332,80 @@ def test_ratio_bounded_by_exponent_entropy():
         assert lower <= len(s) <= lower * 1.01 + 1024 * (n // be + 1)
 
 
+# ----------------------------------------------- FP8 pairs (section 4.1)
+def _fp8_value_table(fmt):
+    """Float value of every FP8 byte, decoded by torch (independent of the
+    oracle's bit handling)."""
+    b = torch.arange(256, dtype=torch.uint8)
+    t = {"e4m3fn": torch.float8_e4m3fn, "e5m2": torch.float8_e5m2}[fmt]
+    return b.view(t).to(torch.float64).numpy()
+
+
+@pytest.mark.parametrize("fmt", ["e4m3fn", "e5m2"])
+def test_fp8_pair_symbol_is_the_joint_exponent(fmt):
+    """Every 16-bit unit of two FP8 values: the symbol's nibbles locate the
+    two values' binades (the exponent fields of section 4.1; for e5m2 the
+    exponent without its lowest bit, i.e. a pair of binades), the raw byte
+    keeps the signs, and the split is a bijection."""
+    vals = _fp8_value_table(fmt)
+    bias, pair = (7, 1) if fmt == "e4m3fn" else (15, 2)   # e5m2: a nibble spans two binades
+    seen = set()
+    for w in range(1 << 16):
+        s, r = ref.split_word(fmt, w)
+        assert 0 <= s < 256 and 0 <= r < 256
+        seen.add((s, r))
+        assert ref.merge_word(fmt, s, r) == w
+        for k in range(2):
+            v = vals[(w >> (8 * k)) & 0xFF]
+            nib, rnib = (s >> (4 * k)) & 15, (r >> (4 * k)) & 15
+            if np.isnan(v) or np.isinf(v):
+                continue
+            assert (rnib >> 3) == (1 if math.copysign(1.0, v) < 0 else 0), (w, k)
+            a = abs(v)
+            if a == 0:
+                assert nib == 0
+                continue
+            lo = 2.0 ** (pair * nib - bias) if nib > 0 else 0.0
+            hi = 2.0 ** (pair * nib + pair - bias)
+            # nibble 0 holds the subnormals (and for e5m2 also the first normal binade)
+            assert lo <= a < hi, (fmt, w, k, v, nib)
+    assert len(seen) == 1 << 16
+
+
+@pytest.mark.parametrize("fmt", ["e4m3fn", "e5m2"])
+def test_fp8_ratio_bounded_by_pair_exponent_entropy(fmt):
+    """FP8 N(0,1) pairs: half the bytes stay raw; the coded part is the
+    symbols' empirical entropy per block plus the bounded rANS overhead."""
+    x = W.normal_fp8_pairs(1 << 19, fmt, seed=21)
+    n, bb = x.size, 65536
+    be = bb // 2
+    s = ref.compress(x, fmt, bb)
+    sym = np.array([ref.split_word(fmt, int(w))[0] for w in x[:1 << 16]])
+    sym = np.concatenate([sym, ((x[1 << 16:] >> 3) & 15) | (((x[1 << 16:] >> 11) & 15) << 4)])
+    Hsum = 0.0
+    for b in range(0, n, be):
+        blk = sym[b:b + be]
+        p = np.bincount(blk, minlength=256) / blk.size
+        Hsum += -blk.size * float(np.sum(p[p > 0] * np.log2(p[p > 0])))
+    lower = (8 * n + Hsum) / 8
+    assert lower <= len(s) <= lower * 1.01 + 1024 * (n // be + 1)
+    assert np.array_equal(ref.decompress(s, fmt, n), x)
+
+
+@pytest.mark.parametrize("fmt", ["e4m3fn", "e5m2"])
+def test_fp8_specials_and_random_bits_roundtrip(fmt):
+    rng = np.random.default_rng(5)
+    x = W.normal_fp8_pairs(70_001, fmt, seed=9)
+    specials = np.array([0x0000, 0x8080, 0x7F7F, 0xFFFF, 0x7E00, 0x007C, 0xFC7B, 0x0101], np.uint16)
+    pos = rng.integers(0, x.size, x.size // 10)
+    x[pos] = rng.choice(specials, pos.size)
+    r = W.random_bits(9000, 16, seed=3)
+    for arr in (x, r):
+        for bb in (4096, 65536):
+            st = ref.compress(arr, fmt, bb)
+            assert np.array_equal(ref.decompress(st, fmt, arr.size), arr)
+
+
 # ------------------------------------------------------- losslessness
 def _special_words(dtype, n, seed):
     rng = np.random.default_rng(seed)
@@ -340,11 +414,16 @@ def _special_words(dtype, n, seed):
         specials = [0x0000, 0x8000, 0x7F80, 0xFF80, 0x7FC0, 0x7F81, 0xFFFF, 0x0001, 0x807F, 0x3F80]
     elif dtype == "fp16":
         specials = [0x0000, 0x8000, 0x7C00, 0xFC00, 0x7E00, 0x7C01, 0xFFFF, 0x0001, 0x83FF, 0x3C00]
+    elif dtype in ("e4m3fn", "e5m2"):
+        specials = [0x0000, 0x8080, 0x7F7F, 0xFFFF, 0x7E00, 0x007C, 0xFC7B, 0x0101, 0x3838, 0x3C3C]
     else:
         specials = [0, 0x80000000, 0x7F800000, 0xFF800000, 0x7FC00000, 0x7F800001, 0xFFFFFFFF, 1,
                     0x807FFFFF, 0x3F800000]
-    x = W.normal_bf16(n, seed=seed) if dtype == "bf16" else (
-        W.grad_fp16(n, seed=seed) if dtype == "fp16" else W.grad_fp32(n, seed=seed))
+    if dtype in ("e4m3fn", "e5m2"):
+        x = W.normal_fp8_pairs(n, dtype, seed=seed)
+    else:
+        x = W.normal_bf16(n, seed=seed) if dtype == "bf16" else (
+            W.grad_fp16(n, seed=seed) if dtype == "fp16" else W.grad_fp32(n, seed=seed))
     pos = rng.integers(0, n, n // 10)
     x[pos] = rng.choice(specials, pos.size)
     noise = rng.integers(0, n, n // 50)
@@ -497,8 +576,8 @@ def test_scalar_conversions_against_numpy_and_torch():
 # ------------------------------------ second CPU reading (micro-model)
 def test_c_oracle_matches_python_model():
     rng = np.random.default_rng(17)
-    for trial in range(24):
-        dtype = ["bf16", "fp16", "fp32"][trial % 3]
+    for trial in range(30):
+        dtype = ["bf16", "fp16", "fp32", "e4m3fn", "e5m2"][trial % 5]
         n = int(rng.integers(0, 9000))
         if trial % 4 == 0:
             x = W.random_bits(n, 8 * EB[dtype], seed=trial)

@@ -89,6 +89,20 @@ def uniform_bf16(n: int, lo: float = -1.0, hi: float = 1.0, seed: int = 11) -> n
     return _pieces(n, fn, np.empty(n, np.uint16))
 
 
+FP8_TORCH = {"e4m3fn": torch.float8_e4m3fn, "e5m2": torch.float8_e5m2}
+
+
+def normal_fp8_pairs(n_pairs: int, fmt: str = "e4m3fn", sigma: float = 1.0, seed: int = 13) -> np.ndarray:
+    """FP8 values N(0, sigma^2), converted by torch (round to nearest even,
+    saturating), as 16-bit pairs (value 2i in the low byte): the element the
+    codec takes for FP8 (section 4.1)."""
+    def fn(p, lo, hi):
+        z = _rng(seed, p).standard_normal(2 * (hi - lo), dtype=np.float32) * np.float32(sigma)
+        b = torch.from_numpy(z).to(FP8_TORCH[fmt]).view(torch.uint8).numpy()
+        return b.view(np.uint16)
+    return _pieces(n_pairs, fn, np.empty(n_pairs, np.uint16))
+
+
 def random_bits(n: int, bits: int, seed: int = 12) -> np.ndarray:
     dt = np.uint16 if bits == 16 else np.uint32
 

@@ -204,6 +204,41 @@ def main() -> int:
                             "ratio_out": round(int(rsz.item()) / (2 * rn), 4)}
         log(f"[bench] fused reduce {r_ms:.3f} ms")
 
+        # ------------- FP8 pairs: 1 GiB of e4m3fn / e5m2 values N(0, 1) -------------
+        del cout, cws, rout, rws, streams
+        for fmt, code in (("e4m3fn", uz.E4M3FN), ("e5m2", uz.E5M2)):
+            f8 = torch.from_numpy(W.normal_fp8_pairs(n, fmt).view(np.int16)).to(dev)
+            fout = torch.empty(uz.uzip_max_compressed_size(code, n, bb), dtype=torch.uint8, device=dev)
+            fws = torch.empty(uz.uzip_workspace_size(uz.OP_COMPRESS, code, n, bb), dtype=torch.uint8, device=dev)
+            fy = torch.empty_like(f8)
+            for _ in range(2):
+                _, fsz = uz.compress(f8, bb, dtype=fmt, out=fout, ws=fws)
+                _, fst = uz.decompress(fout, fmt, n, out=fy, ws=dws)
+            torch.cuda.synchronize()
+            if int(fst.item()) != 0 or not torch.equal(f8, fy):
+                log(f"[bench] {fmt} round trip is NOT lossless")
+                return 1
+            fsize = int(fsz.item())
+            ct, dt_ = [], []
+            for _ in range(reps):
+                e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+                e[0].record(stream)
+                uz.compress(f8, bb, dtype=fmt, out=fout, ws=fws)
+                e[1].record(stream)
+                uz.decompress(fout, fmt, n, out=fy, ws=dws)
+                e[2].record(stream)
+                torch.cuda.synchronize()
+                ct.append(e[0].elapsed_time(e[1]))
+                dt_.append(e[1].elapsed_time(e[2]))
+            fc, fd = float(np.mean(ct)), float(np.mean(dt_))
+            moved = nbytes + fsize
+            extras[f"fp8_{fmt}"] = {"workload": f"normal_{fmt}_pairs_1GiB", "pairs": n, "ratio": round(fsize / nbytes, 4),
+                                    "compress_ms": round(fc, 4), "decompress_ms": round(fd, 4),
+                                    "compress_frac": round(moved / (fc * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                                    "decompress_frac": round(moved / (fd * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)}
+            log(f"[bench] {fmt}: ratio {fsize / nbytes:.4f} compress {fc:.3f} ms decompress {fd:.3f} ms")
+            del f8, fout, fws, fy
+
     if args.calibrate_copy:
         # a plain device copy of known size, for scaling the HBM counters
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)

@@ -61,7 +61,20 @@
 extern "C" {
 #endif
 
-typedef enum { UZIP_BF16 = 0, UZIP_FP16 = 1, UZIP_FP32 = 2 } uzip_dtype;
+/* Element types.  The FP8 formats (section 4.1) are coded in pairs: one
+ * element is a 16-bit unit holding two FP8 values, the first in the low
+ * byte, so for them n_elems counts pairs and an odd count of values is
+ * padded by the caller.  Each value gives bits 6..3 (e4m3fn: the exponent;
+ * e5m2: its top four exponent bits) to the unit's coded symbol and bit 7
+ * with bits 2..0 to its raw byte.  The fused reduction takes bf16, fp16
+ * and fp32 only. */
+typedef enum {
+  UZIP_BF16 = 0,
+  UZIP_FP16 = 1,
+  UZIP_FP32 = 2,
+  UZIP_E4M3FN = 3, /* pairs of float8 e4m3fn */
+  UZIP_E5M2 = 4    /* pairs of float8 e5m2 */
+} uzip_dtype;
 
 typedef enum {
   UZIP_OK = 0,

@@ -27,7 +27,7 @@ if not os.path.exists(LIB_PATH):
 
 _lib = ctypes.CDLL(LIB_PATH)
 
-BF16, FP16, FP32 = 0, 1, 2
+BF16, FP16, FP32, E4M3FN, E5M2 = 0, 1, 2, 3, 4
 OP_COMPRESS, OP_DECOMPRESS, OP_REDUCE, OP_CHUNKED = 0, 1, 2, 3
 WS_NO_OUT_RAW = 1 << 16
 OK, EINVAL, ENOSPC, ECORRUPT, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
@@ -97,10 +97,12 @@ def uzip_status_str(status: int) -> str:
 
 
 # ---------------------------------------------------------------- torch helpers
-_TORCH_DTYPE = {torch.bfloat16: BF16, torch.float16: FP16, torch.float32: FP32}
-_NAME_DTYPE = {"bf16": BF16, "fp16": FP16, "fp32": FP32}
-_ELEM = {BF16: 2, FP16: 2, FP32: 4}
-_BITS = {BF16: torch.int16, FP16: torch.int16, FP32: torch.int32}
+# FP8 formats are coded in pairs: one element is a 16-bit unit of two values
+_TORCH_DTYPE = {torch.bfloat16: BF16, torch.float16: FP16, torch.float32: FP32,
+                torch.float8_e4m3fn: E4M3FN, torch.float8_e5m2: E5M2}
+_NAME_DTYPE = {"bf16": BF16, "fp16": FP16, "fp32": FP32, "e4m3fn": E4M3FN, "e5m2": E5M2}
+_ELEM = {BF16: 2, FP16: 2, FP32: 4, E4M3FN: 2, E5M2: 2}
+_BITS = {BF16: torch.int16, FP16: torch.int16, FP32: torch.int32, E4M3FN: torch.int16, E5M2: torch.int16}
 
 
 def dtype_code(dt) -> int:
@@ -121,17 +123,27 @@ def _check(rc: int, what: str) -> None:
         raise UzipError(rc, what)
 
 
+def _n_elems(x: torch.Tensor, dt: int) -> int:
+    """Elements of x in units of the codec's element (FP8: value pairs)."""
+    nbytes = x.numel() * x.element_size()
+    if nbytes % _ELEM[dt]:
+        raise ValueError(f"{nbytes} bytes is not a whole number of {_ELEM[dt]}-byte elements "
+                         "(FP8 tensors are coded in pairs and need an even length)")
+    return nbytes // _ELEM[dt]
+
+
 def _dev_empty(nbytes: int, device) -> torch.Tensor:
     return torch.empty(max(int(nbytes), 16), dtype=torch.uint8, device=device)
 
 
 def compress(x: torch.Tensor, block_bytes: int = 65536, dtype=None, out: torch.Tensor | None = None,
              ws: torch.Tensor | None = None, stream=None):
-    """Compress a contiguous CUDA tensor (bf16/fp16/fp32, or an int16/int32
-    bit view with ``dtype`` given).  Returns (stream buffer, device u64 size)."""
+    """Compress a contiguous CUDA tensor (bf16/fp16/fp32/float8, or an
+    int16/int32 bit view with ``dtype`` given; float8 tensors are coded as
+    pairs of values).  Returns (stream buffer, device u64 size)."""
     assert x.is_cuda and x.is_contiguous()
     dt = dtype_code(dtype if dtype is not None else x.dtype)
-    n = x.numel()
+    n = _n_elems(x, dt)
     cap = uzip_max_compressed_size(dt, n, block_bytes)
     if cap == 0:
         _check(EINVAL, "uzip_compress")
@@ -148,7 +160,8 @@ def compress(x: torch.Tensor, block_bytes: int = 65536, dtype=None, out: torch.T
 
 def decompress(s: torch.Tensor, dtype, n_elems: int, out: torch.Tensor | None = None,
                in_bytes: int | None = None, ws: torch.Tensor | None = None, stream=None):
-    """Decompress a stream.  Returns (bit-pattern tensor, device u32 status)."""
+    """Decompress a stream of n_elems elements (FP8: pairs).  Returns
+    (bit-pattern tensor, int16 per FP8 pair; device u32 status)."""
     dt = dtype_code(dtype)
     if out is None:
         out = torch.empty(max(n_elems, 1), dtype=_BITS[dt], device=s.device)[:n_elems]
@@ -196,7 +209,7 @@ def compress_chunked(x: torch.Tensor, block_bytes: int, chunk_bytes: int, dtype=
     device u64 chunk sizes, flags [2 n_chunks] u32)."""
     assert x.is_cuda and x.is_contiguous()
     dt = dtype_code(dtype if dtype is not None else x.dtype)
-    n = x.numel()
+    n = _n_elems(x, dt)
     e = _ELEM[dt]
     ce = chunk_bytes // e
     chunks = (n + ce - 1) // ce

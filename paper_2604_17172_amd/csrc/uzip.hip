@@ -132,12 +132,19 @@ __device__ inline void load_words(const uint8_t *base, uint64_t first, uint32_t 
   }
 }
 
-template <int E>
-__device__ inline void split_group(const uint32_t w[4 * (E / 2)], Group &g) {
-  if (E == 2)
-    split16(w, g);
-  else
+// element width of a dtype code: fp32 4 bytes, the rest (bf16, fp16, FP8
+// pairs) 2
+template <int DT>
+constexpr int dt_bytes() { return DT == 2 ? 4 : 2; }
+
+template <int DT>
+__device__ inline void split_group(const uint32_t w[4 * (dt_bytes<DT>() / 2)], Group &g) {
+  if constexpr (DT >= 3)
+    split8x2(w, g);
+  else if constexpr (DT == 2)
     split32(w, g);
+  else
+    split16(w, g);
 }
 
 // raw plane bytes of a group: 8 (E = 2) or 24 (E = 4) bytes at plane + (E-1) first
@@ -206,12 +213,15 @@ __device__ inline void load_raw(const uint8_t *plane, uint64_t first, uint32_t v
   }
 }
 
-template <int E>
-__device__ inline void merge_group(const uint32_t sym[2], const uint32_t raw[6], uint32_t w[4 * (E / 2)]) {
-  if (E == 2)
-    merge16(sym, raw, w);
-  else
+template <int DT>
+__device__ inline void merge_group(const uint32_t sym[2], const uint32_t raw[6],
+                                   uint32_t w[4 * (dt_bytes<DT>() / 2)]) {
+  if constexpr (DT >= 3)
+    merge8x2(sym, raw, w);
+  else if constexpr (DT == 2)
     merge32(sym, raw, w);
+  else
+    merge16(sym, raw, w);
 }
 
 // Eight elements of one lane out to a tensor.  NT: full groups with
@@ -646,7 +656,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         if (valid > 0) {
           uint32_t w[NW];
           load_words<E>(src, blk0 + i0, valid, w);
-          split_group<E>(w, gr);
+          split_group<DT>(w, gr);
           store_raw<E, SYS>(raw_plane, blk0 + i0, valid, gr);
           hist_add8(h, gr, valid);
         }
@@ -677,7 +687,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
               const uint32_t rn = (r + D < full) ? r + D : full - 1;
               load_round<E>(src_blk + (uint64_t)rn * kRound * E, buf[rr % D]);
               Group gr;
-              split_group<E>(w, gr);
+              split_group<DT>(w, gr);
               S.v3[2 * rr] = gr.sym[0];
               S.v3[2 * rr + 1] = gr.sym[1];
               if (r < full) {
@@ -701,7 +711,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
               const uint32_t rn = (r + u + D < full) ? r + u + D : full - 1;
               load_round<E>(src_blk + (uint64_t)rn * kRound * E, buf[u]);
               Group gr;
-              split_group<E>(w, gr);
+              split_group<DT>(w, gr);
               store_raw_round<E, SYS>(raw_blk + (uint64_t)(r + u) * kRound * (E - 1), gr);
               hist_add8(h, gr, 8);
             }
@@ -710,7 +720,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
           for (int u = 0; u < D - 1; ++u) {
             if (r + u < full) {
               Group gr;
-              split_group<E>(buf[u], gr);
+              split_group<DT>(buf[u], gr);
               store_raw_round<E, SYS>(raw_blk + (uint64_t)(r + u) * kRound * (E - 1), gr);
               hist_add8(h, gr, 8);
             }
@@ -760,7 +770,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         uint32_t w[NW];
         Group gr;
         load_words<E>(src, blk0 + i0, valid, w);
-        split_group<E>(w, gr);
+        split_group<DT>(w, gr);
         s0 = gr.sym[0];
         s1 = gr.sym[1];
       }
@@ -803,7 +813,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
       for (; r >= 1 && !stored; r -= 2) {
         load_round<E>(src_blk + (uint64_t)(r - 1) * kRound * E, wbuf);
         Group gr;
-        split_group<E>(wa, gr);
+        split_group<DT>(wa, gr);
         uint4 e[8];
 #pragma unroll
         for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
@@ -812,7 +822,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         if (stored) break;
         const uint32_t rn = r >= 2 ? (uint32_t)(r - 2) : 0u;
         load_round<E>(src_blk + (uint64_t)rn * kRound * E, wa);
-        split_group<E>(wbuf, gr);
+        split_group<DT>(wbuf, gr);
 #pragma unroll
         for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
         enc_round<true>(x, e, 8, pos, lds_rel, trash);
@@ -820,7 +830,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
       }
       if (r == 0 && !stored) {  // wa holds round 0
         Group gr;
-        split_group<E>(wa, gr);
+        split_group<DT>(wa, gr);
         uint4 e[8];
 #pragma unroll
         for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
@@ -928,7 +938,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
             uint32_t w[NW];
             Group gr;
             load_words<E>(src, blk0 + i0, valid, w);
-            split_group<E>(w, gr);
+            split_group<DT>(w, gr);
             s0 = gr.sym[0];
             s1 = gr.sym[1];
           }
@@ -1028,9 +1038,10 @@ __device__ __forceinline__ void ring_put(uint8_t *ring, uint32_t pos, uint4 v) {
 
 // Eight decoded elements of one lane from their table entries (symbols in
 // the top bytes) and raw bytes: the inverse of the byte-plane split.
-template <int E>
-__device__ inline void merge_entries(const uint32_t e[8], const uint32_t raw[6], uint32_t w[4 * (E / 2)]) {
-  if (E == 2) {
+template <int DT>
+__device__ inline void merge_entries(const uint32_t e[8], const uint32_t raw[6],
+                                     uint32_t w[4 * (dt_bytes<DT>() / 2)]) {
+  if constexpr (DT <= 1) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       // [raw, sym, raw, sym] of elements 2j, 2j + 1, then rotate each half back
@@ -1045,7 +1056,7 @@ __device__ inline void merge_entries(const uint32_t e[8], const uint32_t raw[6],
       const uint32_t hi = __builtin_amdgcn_perm(e[4 * h + 3], e[4 * h + 2], 0x07030303u);
       sym[h] = __builtin_amdgcn_perm(hi, lo, 0x07060100u);
     }
-    merge32(sym, raw, w);
+    merge_group<DT>(sym, raw, w);
   }
 }
 
@@ -1192,7 +1203,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
         uint32_t raw[6];
         load_raw<E>(raw_plane, blk0 + i0, valid, raw);
         uint32_t w[NW];
-        merge_group<E>(sym, raw, w);
+        merge_group<DT>(sym, raw, w);
         store_words<E>(a.out, blk0 + i0, valid, w);
       }
       continue;
@@ -1249,7 +1260,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
         e[t] = decode_step_ring<true, kDecRingBytes, false>(x, true, lut, ring, rb, p);
       }
       uint32_t w[NW];
-      merge_entries<E>(e, rawA, w);
+      merge_entries<DT>(e, rawA, w);
       store_words<E, true>(outp, r * kRound + kPerLane * lane, 8, w);
 
       ringd_half<0>(rg, ring, sec, wb + 2 * p);
@@ -1260,7 +1271,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
         if (t == kPerLane / 2) ringd_half<1>(rg, ring, sec, wb + 2 * p);
         e[t] = decode_step_ring<true, kDecRingBytes, false>(x, true, lut, ring, rb, p);
       }
-      merge_entries<E>(e, rawB, w);
+      merge_entries<DT>(e, rawB, w);
       store_words<E, true>(outp, (r + 1) * kRound + kPerLane * lane, 8, w);
     }
     if (r < full) {  // odd number of full rounds: rawA holds round r
@@ -1272,7 +1283,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
         e[t] = decode_step_ring<true, kDecRingBytes, false>(x, true, lut, ring, rb, p);
       }
       uint32_t w[NW];
-      merge_entries<E>(e, rawA, w);
+      merge_entries<DT>(e, rawA, w);
       store_words<E, true>(outp, r * kRound + kPerLane * lane, 8, w);
       ++r;
     }
@@ -1290,7 +1301,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
         uint32_t raw[6];
         load_raw<E>(raw_plane, blk0 + i0, valid, raw);
         uint32_t w[NW];
-        merge_entries<E>(e, raw, w);
+        merge_entries<DT>(e, raw, w);
         store_words<E>(a.out, blk0 + i0, valid, w);
       }
     }
@@ -1445,7 +1456,7 @@ __global__ void __launch_bounds__(64 * (kReduceGroup + 1)) reduce_decode_kernel(
         }
         uint32_t raw[6] = {0, 0, 0, 0, 0, 0};
         load_raw<E>(raw_plane, blk0 + i0, valid, raw);
-        merge_entries<E>(e, raw, w);
+        merge_entries<DT>(e, raw, w);
       } else if (mode == kStored && valid > 0) {
         uint32_t sym[2] = {0, 0};
 #pragma unroll
@@ -1453,7 +1464,7 @@ __global__ void __launch_bounds__(64 * (kReduceGroup + 1)) reduce_decode_kernel(
           if (q < valid) sym[q >> 2] |= (uint32_t)sec[i0 + q] << (8 * (q & 3));
         uint32_t raw[6] = {0, 0, 0, 0, 0, 0};
         load_raw<E>(raw_plane, blk0 + i0, valid, raw);
-        merge_group<E>(sym, raw, w);
+        merge_group<DT>(sym, raw, w);
       }
       uint4 *dst = (uint4 *)(slab + wave * kSlab + kPerLane * E * lane);
       dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
@@ -1506,7 +1517,7 @@ __global__ void __launch_bounds__(64 * (kReduceGroup + 1)) reduce_decode_kernel(
         store_words<E>(a.ybuf, blk0 + i0, valid, w);
         if (a.yout != nullptr && a.yout != a.ybuf) store_words<E>(a.yout, blk0 + i0, valid, w);
         Group gr;
-        split_group<E>(w, gr);
+        split_group<DT>(w, gr);
         store_raw<E>(a.out_raw_plane, blk0 + i0, valid, gr);
         hist_add8(h, gr, valid);
       } else {
@@ -1552,7 +1563,7 @@ __global__ void empty_stream_kernel(uint8_t *out, uint32_t dt, uint32_t block_el
 // ---------------------------------------------------------------------------
 // encoder kernels: index = dt * 4 + kind, kind 0/1 = compress large/small
 // blocks, 2/3 = split-send producer large/small blocks; fused reduce apart
-constexpr int kEncodeKernels = 12;
+constexpr int kEncodeKernels = 20;
 const void *encode_kernel_ptr(int k) {
   static const void *const tab[kEncodeKernels] = {
       (const void *)encode_kernel<0, false, false>, (const void *)encode_kernel<0, true, false>,
@@ -1560,7 +1571,11 @@ const void *encode_kernel_ptr(int k) {
       (const void *)encode_kernel<1, false, false>, (const void *)encode_kernel<1, true, false>,
       (const void *)encode_kernel<1, false, true>,  (const void *)encode_kernel<1, true, true>,
       (const void *)encode_kernel<2, false, false>, (const void *)encode_kernel<2, true, false>,
-      (const void *)encode_kernel<2, false, true>,  (const void *)encode_kernel<2, true, true>};
+      (const void *)encode_kernel<2, false, true>,  (const void *)encode_kernel<2, true, true>,
+      (const void *)encode_kernel<3, false, false>, (const void *)encode_kernel<3, true, false>,
+      (const void *)encode_kernel<3, false, true>,  (const void *)encode_kernel<3, true, true>,
+      (const void *)encode_kernel<4, false, false>, (const void *)encode_kernel<4, true, false>,
+      (const void *)encode_kernel<4, false, true>,  (const void *)encode_kernel<4, true, true>};
   return tab[k];
 }
 const void *reduce_kernel_ptr(int dt) {
@@ -1604,7 +1619,9 @@ uzip_status device_info(DeviceInfo &out) {
 }
 
 uint32_t elem_bytes(uzip_dtype dt) { return dt == UZIP_FP32 ? 4u : 2u; }
-bool valid_dtype(uzip_dtype dt) { return dt == UZIP_BF16 || dt == UZIP_FP16 || dt == UZIP_FP32; }
+bool valid_dtype(uzip_dtype dt) { return dt >= UZIP_BF16 && dt <= UZIP_E5M2; }
+// the fused reduction adds values, which FP8 pairs are not given for
+bool valid_reduce_dtype(uzip_dtype dt) { return dt >= UZIP_BF16 && dt <= UZIP_FP32; }
 bool valid_block(uint32_t bb) { return bb >= kMinBlockBytes && bb <= kMaxBlockBytes && (bb & (bb - 1)) == 0; }
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 uint64_t pad256(uint64_t x) { return (x + 255u) & ~uint64_t(255); }
@@ -1725,6 +1742,7 @@ size_t uzip_workspace_size(int op, uzip_dtype dtype, uint64_t n_elems, uint32_t 
       return (size_t)encode_ws(chunks * (ce / be), chunks, be, 0).total;
     }
     case UZIP_OP_REDUCE: {
+      if (!valid_reduce_dtype(dtype)) return 0;
       const uint64_t n_in = aux & 0xFFFFu;
       if (n_in < 1 || n_in > kMaxInputs) return 0;
       return (size_t)reduce_ws(nb, be, n_elems, E, (int)n_in, (aux & UZIP_WS_NO_OUT_RAW) != 0).total;
@@ -1825,9 +1843,10 @@ uzip_status uzip_decompress(const void *d_in, size_t in_bytes, uzip_dtype dtype,
   a.ticket = (uint32_t *)d_ws;
   // resident waves take blocks by ticket until none are left
   const uint64_t most = (n_elems + (kMinBlockBytes / elem_bytes(dtype)) - 1) / (kMinBlockBytes / elem_bytes(dtype));
-  const void *fn = dtype == UZIP_BF16   ? (const void *)decode_kernel<0>
-                   : dtype == UZIP_FP16 ? (const void *)decode_kernel<1>
-                                        : (const void *)decode_kernel<2>;
+  static const void *const dec_tab[5] = {(const void *)decode_kernel<0>, (const void *)decode_kernel<1>,
+                                         (const void *)decode_kernel<2>, (const void *)decode_kernel<3>,
+                                         (const void *)decode_kernel<4>};
+  const void *fn = dec_tab[(int)dtype];
   int occ = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, 64, 0) != hipSuccess || occ < 1) occ = 1;
   uint64_t grid = (uint64_t)info.cus * (uint64_t)occ;
@@ -1844,7 +1863,7 @@ uzip_status uzip_reduce_fused(const void *const *d_in, const size_t *in_bytes, i
                               uzip_dtype dtype, uint64_t n_elems, uint32_t block_bytes, void *d_out, size_t out_cap,
                               uint64_t *d_out_size, void *d_out_raw, uint32_t *d_status, void *d_ws,
                               size_t ws_bytes, hipStream_t stream) {
-  if (!valid_dtype(dtype) || !valid_block(block_bytes)) return UZIP_EINVAL;
+  if (!valid_reduce_dtype(dtype) || !valid_block(block_bytes)) return UZIP_EINVAL;
   if (n_in < 1 || n_in > kMaxInputs || d_in == nullptr || in_bytes == nullptr) return UZIP_EINVAL;
   for (int i = 0; i < n_in; ++i)
     if (d_in[i] == nullptr || !aligned16(d_in[i]) || in_bytes[i] < kHeaderBytes) return UZIP_EINVAL;

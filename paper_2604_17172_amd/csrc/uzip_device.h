@@ -135,6 +135,38 @@ __device__ inline void merge16(const uint32_t sym[2], const uint32_t raw[2], uin
   w[3] = rotr16x2(__builtin_amdgcn_perm(sym[1], raw[1], 0x07030602u));
 }
 
+// FP8 pairs (section 4.1): element = 16-bit unit of two FP8 values, the
+// first in the low byte.  Per value byte, bits 6..3 form its symbol nibble
+// and bit 7 with bits 2..0 its raw nibble; a unit's symbol (raw byte) is
+// the first value's nibble | the second's << 4.
+__device__ inline void split8x2(const uint32_t w[4], Group &g) {
+  uint32_t s[4], r[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t t = (w[q] >> 3) & 0x0F0F0F0Fu;                            // symbol nibble per byte
+    s[q] = t | (t >> 4);                                                      // units' symbols: bytes 0, 2
+    const uint32_t u = ((w[q] >> 4) & 0x08080808u) | (w[q] & 0x07070707u);  // raw nibble per byte
+    r[q] = u | (u >> 4);
+  }
+  g.sym[0] = __builtin_amdgcn_perm(s[1], s[0], 0x06040200u);
+  g.sym[1] = __builtin_amdgcn_perm(s[3], s[2], 0x06040200u);
+  g.raw[0] = __builtin_amdgcn_perm(r[1], r[0], 0x06040200u);
+  g.raw[1] = __builtin_amdgcn_perm(r[3], r[2], 0x06040200u);
+}
+
+__device__ inline void merge8x2(const uint32_t sym[2], const uint32_t raw[2], uint32_t w[4]) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    // units 2q, 2q + 1: each unit byte twice, then one nibble per value byte
+    const uint32_t sel = (q & 1) ? 0x03030202u : 0x01010000u;
+    const uint32_t sp = __builtin_amdgcn_perm(0u, sym[q >> 1], sel);
+    const uint32_t rp = __builtin_amdgcn_perm(0u, raw[q >> 1], sel);
+    const uint32_t sn = (sp & 0x000F000Fu) | ((sp >> 4) & 0x0F000F00u);
+    const uint32_t rn = (rp & 0x000F000Fu) | ((rp >> 4) & 0x0F000F00u);
+    w[q] = ((rn << 4) & 0x80808080u) | (sn << 3) | (rn & 0x07070707u);
+  }
+}
+
 __device__ inline void split32(const uint32_t w[8], Group &g) {
   uint32_t r[8];
 #pragma unroll

@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(uz._lib, name), name
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "fp16", "fp32"])
+@pytest.mark.parametrize("dtype", ["bf16", "fp16", "fp32", "e4m3fn", "e5m2"])
 @pytest.mark.parametrize("bb", [4096, 65536, 262144])
 def test_max_size_matches_oracle(dtype, bb):
     import paper_2604_17172_amd as uz
@@ -61,6 +61,13 @@ def test_invalid_arguments_rejected_on_host():
     assert uz.uzip_workspace_size(uz.OP_CHUNKED, 0, 1000, 65536, 3000) == 0
     assert uz.uzip_workspace_size(uz.OP_REDUCE, 0, 1000, 65536, 0) == 0
     assert uz.uzip_workspace_size(uz.OP_REDUCE, 0, 1000, 65536, 17) == 0
+    # FP8 pairs are coded but not reduced
+    for dt in (uz.E4M3FN, uz.E5M2):
+        assert uz.uzip_max_compressed_size(dt, 100, 65536) == uz.uzip_max_compressed_size(uz.BF16, 100, 65536)
+        assert uz.uzip_workspace_size(uz.OP_REDUCE, dt, 1000, 65536, 2) == 0
+        assert uz.uzip_reduce_fused([16, 32], [64, 64], 2, None, dt, 10, 65536, 48, 1 << 20, None, None,
+                                    None, 64, 1 << 20, None) == uz.EINVAL
+    assert uz.uzip_max_compressed_size(5, 100, 65536) == 0
 
 
 def test_workspace_sizes_are_bounded():

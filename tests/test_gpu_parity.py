@@ -16,8 +16,9 @@ import workloads as W
 
 pytestmark = pytest.mark.gpu
 
-EB = {"bf16": 2, "fp16": 2, "fp32": 4}
-NP_BITS = {"bf16": np.int16, "fp16": np.int16, "fp32": np.int32}
+# FP8 formats are coded as 16-bit pairs of values
+EB = {"bf16": 2, "fp16": 2, "fp32": 4, "e4m3fn": 2, "e5m2": 2}
+NP_BITS = {"bf16": np.int16, "fp16": np.int16, "fp32": np.int32, "e4m3fn": np.int16, "e5m2": np.int16}
 
 
 def say(msg):
@@ -57,8 +58,13 @@ def special_words(dtype, n, seed):
     specials = {"bf16": [0x0000, 0x8000, 0x7F80, 0xFF80, 0x7FC0, 0x7F81, 0xFFFF, 0x0001, 0x807F],
                 "fp16": [0x0000, 0x8000, 0x7C00, 0xFC00, 0x7E00, 0x7C01, 0xFFFF, 0x0001, 0x83FF],
                 "fp32": [0, 0x80000000, 0x7F800000, 0xFF800000, 0x7FC00000, 0x7F800001, 0xFFFFFFFF, 1,
-                         0x807FFFFF]}[dtype]
-    if dtype == "bf16":
+                         0x807FFFFF],
+                # pairs: NaN/NaN, -0/+0, max/min subnormal, +-inf (e5m2), NaN beside a normal
+                "e4m3fn": [0x7F7F, 0x0080, 0xFE7E, 0x0180, 0xFF38, 0x7F01, 0xFFFF, 0x0000, 0x8808],
+                "e5m2": [0x7F7F, 0x0080, 0xFC7C, 0x7B03, 0x7CFC, 0x7E3C, 0xFFFF, 0x0000, 0x8484]}[dtype]
+    if dtype in ("e4m3fn", "e5m2"):
+        x = W.normal_fp8_pairs(n, dtype, seed=seed)
+    elif dtype == "bf16":
         x = W.normal_bf16(n, seed=seed)
     elif dtype == "fp16":
         x = W.grad_fp16(n, seed=seed)
@@ -150,6 +156,68 @@ def test_empty_tensor(uz):
     y, status = uz.decompress(out, "bf16", 0)
     torch.cuda.synchronize()
     assert int(status.item()) == 0 and y.numel() == 0
+
+
+# ---------------------------------------------------------- FP8 pairs (section 4.1)
+@pytest.mark.parametrize("dtype", ["e4m3fn", "e5m2"])
+@pytest.mark.parametrize("n", [1, 511, 513, 8191, 70_001])
+def test_fp8_edge_sizes(uz, dtype, n):
+    x = special_words(dtype, n, seed=n + 7)
+    for bb in (4096, 65536):
+        check_roundtrip(uz, x, dtype, bb, f"fp8 edge n={n}")
+
+
+@pytest.mark.parametrize("dtype", ["e4m3fn", "e5m2"])
+@pytest.mark.parametrize("sigma,bb", [(1.0, 65536), (0.02, 65536), (1.0, 262144), (0.3, 4096)])
+def test_fp8_normal_pairs(uz, dtype, sigma, bb):
+    """4 MiB of FP8 N(0, sigma^2) values (2 Mi pairs), several block sizes."""
+    x = W.normal_fp8_pairs(1 << 21, dtype, sigma=sigma, seed=21)
+    check_roundtrip(uz, x, dtype, bb, f"fp8 normal sigma={sigma}")
+
+
+@pytest.mark.parametrize("dtype", ["e4m3fn", "e5m2"])
+def test_fp8_random_bits_stored(uz, dtype):
+    x = W.random_bits(200_003, 16, seed=19)
+    check_roundtrip(uz, x, dtype, 65536, "fp8 random bits")
+
+
+@pytest.mark.parametrize("dtype", ["e4m3fn", "e5m2"])
+def test_fp8_tensor_input_counts_pairs(uz, dtype):
+    """A float8 tensor is taken as pairs: the same stream as its int16 view."""
+    say(f"[parity] fp8 tensor input {dtype}")
+    x = W.normal_fp8_pairs(100_001, dtype, seed=4)
+    f8 = dev(x.view(np.uint8)).view(W.FP8_TORCH[dtype])
+    out, size = uz.compress(f8, 65536)
+    torch.cuda.synchronize()
+    got = out[:int(size.item())].cpu().numpy()
+    assert np.array_equal(got, ref.compress(x, dtype, 65536))
+    with pytest.raises(ValueError):
+        uz.compress(f8[:-1].clone(), 65536)
+
+
+@pytest.mark.parametrize("dtype", ["e4m3fn", "e5m2"])
+def test_fp8_chunked_producer(uz, dtype):
+    n, bb, cb = 3 * (1 << 19) + 999, 65536, 1 << 20
+    say(f"[parity] fp8 chunked dtype={dtype} n={n}")
+    x = special_words(dtype, n, seed=41)
+    out, slot, sizes, flags = uz.compress_chunked(to_dev_bits(x, dtype), bb, cb, dtype=dtype, epoch=5)
+    torch.cuda.synchronize()
+    assert np.all(flags.cpu().numpy() == 5)
+    sz = sizes.cpu().numpy()
+    buf = out.cpu().numpy()
+    for c, w in enumerate(ref.compress_chunked(x, dtype, bb, cb)):
+        assert sz[c] == w.size and np.array_equal(buf[c * slot:c * slot + w.size], w), f"chunk {c}"
+
+
+def test_fp8_stream_dtype_must_match(uz):
+    """An e4m3fn stream decoded as e5m2 (or bf16) is reported corrupt."""
+    say("[parity] fp8 dtype mismatch")
+    x = W.normal_fp8_pairs(10_000, "e4m3fn", seed=2)
+    out, _ = gpu_compress(uz, x, "e4m3fn", 65536)
+    for other in ("e5m2", "bf16"):
+        _, st = uz.decompress(out, other, x.size)
+        torch.cuda.synchronize()
+        assert int(st.item()) == uz.ECORRUPT
 
 
 # ---------------------------------------------------------- split-send producer

@@ -528,13 +528,54 @@ __device__ __forceinline__ void enc_round(uint32_t &x, const uint4 (&e)[8], uint
   for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step_lds<FULL>(x, e[tt], (uint32_t)tt < valid, pos, lds_rel, trash);
 }
 
-// The LDS staging window holds virtual indices [lo, lo + cap).  Before a
-// round that could write below it, move the words written so far,
-// [pos, lo + cap), to the same indices of the workgroup's overflow slot in
-// global memory and slide the window down to end at pos.
-__device__ __forceinline__ void spill_window(const __attribute__((address_space(3))) uint16_t *lds_rel, uint16_t *ovf,
-                                          uint32_t pos, uint32_t top) {
-  for (uint32_t v = pos + lane_id(); v < top; v += 64) __builtin_nontemporal_store(lds_rel[v], ovf + v);
+// The LDS staging window holds virtual indices [lo, lo + cap) at win[v - lo]
+// (lo, cap and the slide x are multiples of 8 words, win and the overflow
+// slot are 16-byte aligned).  Before a round that could write below it, the
+// window's x oldest words (the highest indices) go to the same indices of
+// the workgroup's overflow slot and the rest, from the 16-byte unit holding
+// pos up, moves up by x: the window then covers [lo - x, lo - x + cap).
+constexpr uint32_t kSlideWords = 2048;
+__device__ __forceinline__ void slide_window(__attribute__((address_space(3))) uint16_t *win, uint16_t *ovf_lo,
+                                             uint32_t cap, uint32_t x, uint32_t pos_rel) {
+  typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) v4u lds_u4;
+  const uint32_t lane = lane_id();
+  for (uint32_t i = 8 * lane; i < x; i += 8 * kLanes)
+    *(v4u *)(ovf_lo + cap - x + i) = *(const lds_u4 *)(win + cap - x + i);
+  // top chunk first: every word is read before its old place is written
+  const int32_t start = (int32_t)(pos_rel & ~7u);
+  for (int32_t c = (int32_t)(cap - x) - (int32_t)(8 * kLanes); c + (int32_t)(8 * kLanes) > start;
+       c -= (int32_t)(8 * kLanes)) {
+    const int32_t i = c + 8 * (int32_t)lane;
+    if (i >= start) *(lds_u4 *)(win + i + x) = *(const lds_u4 *)(win + i);
+  }
+}
+
+// 16 bytes starting `sh` bytes into p0 (sh even, < 16), continuing into p1
+__device__ __forceinline__ uint4 funnel16(const uint4 p0, const uint4 p1, uint32_t sh) {
+  uint32_t q0, q1, q2, q3, q4;
+  switch (sh >> 2) {
+    case 0: q0 = p0.x; q1 = p0.y; q2 = p0.z; q3 = p0.w; q4 = p1.x; break;
+    case 1: q0 = p0.y; q1 = p0.z; q2 = p0.w; q3 = p1.x; q4 = p1.y; break;
+    case 2: q0 = p0.z; q1 = p0.w; q2 = p1.x; q3 = p1.y; q4 = p1.z; break;
+    default: q0 = p0.w; q1 = p1.x; q2 = p1.y; q3 = p1.z; q4 = p1.w; break;
+  }
+  const uint32_t b = sh & 3u;
+  return make_uint4(__builtin_amdgcn_alignbyte(q1, q0, b), __builtin_amdgcn_alignbyte(q2, q1, b),
+                    __builtin_amdgcn_alignbyte(q3, q2, b), __builtin_amdgcn_alignbyte(q4, q3, b));
+}
+
+// zero the bytes of a 16-byte unit at or past byte `keep` (even, < 16)
+__device__ __forceinline__ uint4 keep_bytes(uint4 o, uint32_t keep) {
+  uint32_t w[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+  for (uint32_t j = 0; j < 4; ++j) {
+    if (4 * j >= keep)
+      w[j] = 0;
+    else if (4 * j + 2 == keep)
+      w[j] &= 0xFFFFu;
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
 template <int E>
@@ -787,10 +828,11 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         for (int rr = 15; rr >= 0; --rr) {
           const int r = 16 * gi + rr;
           if (r < (int)full && !stored) {
-            if (pos < lo + kRound) {  // rare: slide the LDS window down
-              spill_window(lds_rel, ovf, pos, spilled);
-              spilled = pos;
-              lo = pos > a.lds_words ? pos - a.lds_words : 0;
+            if (pos < lo + kRound && lo > 0) {  // the LDS window is full: slide it down
+              const uint32_t x = lo < kSlideWords ? lo : kSlideWords;
+              slide_window((lds16_t *)stage16, ovf + lo, a.lds_words, x, pos - lo);
+              lo -= x;
+              spilled = lo + a.lds_words;
               lds_rel = (lds16_t *)stage16 - lo;
             }
             const uint32_t s0 = S.v3[2 * rr], s1 = S.v3[2 * rr + 1];
@@ -885,33 +927,49 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
           out128<SYS>(sec + 16 * u, o);
         }
       } else {
-        // rare: words [spilled, wcap) went to the overflow slot; gather the
-        // header (LDS), the LDS words [pos, spilled) and the spilled words
-        // (global, read back with device-coherent loads)
-        put_header((uint16_t *)stage);
+        // words [spilled, wcap) went to the overflow slot: section bytes
+        // [0, lb) are in LDS (header right before the words), bytes
+        // [lb, img) are the slot's bytes [2 spilled, 2 wcap).  The slot was
+        // written by this wave; the fence orders those stores before the
+        // reads (one wave per workgroup, one CU: no cache in between).
+        const uint32_t A = kStageHead + 2 * (pos - lo) - hdr;
+        put_header((uint16_t *)(stage + A));
         __threadfence_block();
         __syncthreads();
+        const uint32_t lb = hdr + 2 * (spilled - pos);
+        const uint32_t imgb = (uint32_t)img;
+        const uint32_t *s32 = (const uint32_t *)(stage + (A & ~3u));
+        const uint32_t sh = A & 3u;
+        const uint32_t d = 2 * spilled - lb;  // slot byte = section byte + d (mod 2^32)
+        const uint8_t *ovb = (const uint8_t *)ovf;
         for (uint32_t u = lane; u < sec_len / 16; u += 64) {
-          uint32_t o[4] = {0, 0, 0, 0};
+          uint4 o;
+          if (16 * u + 16 <= lb) {
+            const uint32_t *q = s32 + 4 * u;
+            o.x = __builtin_amdgcn_alignbyte(q[1], q[0], sh);
+            o.y = __builtin_amdgcn_alignbyte(q[2], q[1], sh);
+            o.z = __builtin_amdgcn_alignbyte(q[3], q[2], sh);
+            o.w = __builtin_amdgcn_alignbyte(q[4], q[3], sh);
+          } else if (16 * u >= lb) {
+            const uint32_t off = 16 * u + d;
+            const uint4 *p = (const uint4 *)(ovb + (off & ~15u));
+            o = funnel16(p[0], p[1], off & 15u);
+            if (16 * u + 16 > imgb) o = keep_bytes(o, imgb - 16 * u);
+          } else {  // the unit where LDS and slot bytes meet
+            uint32_t w[4] = {0, 0, 0, 0};
 #pragma unroll
-          for (uint32_t hw = 0; hw < 8; ++hw) {
-            const uint32_t ob = 16 * u + 2 * hw;
-            uint32_t v16 = 0;
-            if (ob < hdr) {
-              v16 = ((const uint16_t *)stage)[ob / 2];
-            } else if ((ob - hdr) / 2 < n_words) {
-              const uint32_t v = pos + (ob - hdr) / 2;
-              if (v < spilled) {
-                v16 = stage16[v - lo];
-              } else {
-                const uint32_t dw = __hip_atomic_load((const uint32_t *)ovf + (v >> 1), __ATOMIC_RELAXED,
-                                                      __HIP_MEMORY_SCOPE_AGENT);
-                v16 = (dw >> (16 * (v & 1))) & 0xFFFFu;
-              }
+            for (uint32_t hw = 0; hw < 8; ++hw) {
+              const uint32_t ob = 16 * u + 2 * hw;
+              uint32_t v16 = 0;
+              if (ob < lb)
+                v16 = *(const uint16_t *)(stage + A + ob);
+              else if (ob < imgb)
+                v16 = *(const uint16_t *)(ovb + ob + d);
+              w[hw >> 1] |= v16 << (16 * (hw & 1));
             }
-            o[hw >> 1] |= v16 << (16 * (hw & 1));
+            o = make_uint4(w[0], w[1], w[2], w[3]);
           }
-          out128<SYS>(sec + 16 * u, make_uint4(o[0], o[1], o[2], o[3]));
+          out128<SYS>(sec + 16 * u, o);
         }
       }
     } else {

@@ -18,8 +18,9 @@ import workloads as W
 
 pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
 
-EB = {"bf16": 2, "fp16": 2, "fp32": 4}
-NP_BITS = {"bf16": np.int16, "fp16": np.int16, "fp32": np.int32}
+# FP8 formats are coded as 16-bit pairs of values
+EB = {"bf16": 2, "fp16": 2, "fp32": 4, "e4m3fn": 2, "e5m2": 2}
+NP_BITS = {"bf16": np.int16, "fp16": np.int16, "fp32": np.int32, "e4m3fn": np.int16, "e5m2": np.int16}
 
 
 def say(msg):
@@ -108,6 +109,13 @@ def test_grad_fp16_512MiB(uz):
 
 def test_kv_cache_2GiB_chunked(uz):
     check_chunked(uz, W.kv_cache(), "bf16", 65536, 1 << 20, "kv_cache_bf16_2GiB")
+
+
+@pytest.mark.parametrize("fmt", ["e4m3fn", "e5m2"])
+def test_fp8_pairs_1GiB_whole_stream(uz, fmt):
+    """1 GiB of FP8 N(0, 1) values (2^29 pairs), 64 KiB blocks: the
+    benchmark's FP8 workload."""
+    check_whole(uz, W.normal_fp8_pairs(1 << 29, fmt), fmt, 65536, f"normal_{fmt}_pairs_1GiB")
 
 
 def test_reduce_8x16MiB(uz):

@@ -215,3 +215,86 @@ def decompress(stream: bytes, dtype: str, n: int) -> list[int]:
         start = end
     assert coded + start == total
     return out
+
+
+# --------------------------------------------------------------------------
+# Stream-wide tables (section 3.3.1's table from a sample of the range,
+# section 3.4's table sent once and reused): one table codes every block.
+# Mode 1 keeps it in the stream after the directory, mode 2 leaves it to
+# the caller.  Every symbol keeps a nonzero frequency, so symbols that the
+# sample (the first 256 KiB) missed can still be coded.
+# --------------------------------------------------------------------------
+SAMPLE_BYTES = 256 * 1024
+
+
+def table_all(sample: list[int]) -> list[int]:
+    n = len(sample)
+    if n == 0:
+        return [M // 256] * 256
+    c = [sample.count(s) for s in range(256)]
+    f = [1 + (c[s] * (M - 256)) // n for s in range(256)]
+    top = max(range(256), key=lambda s: (c[s], -s))
+    f[top] += M - sum(f)
+    return f
+
+
+def shared_section(symbols: list[int], f: list[int]) -> tuple[bytes, bool]:
+    n = len(symbols)
+    states, words = encode(symbols, f)
+    if 256 + 2 * len(words) < n:
+        body = struct.pack("<64I", *states) + struct.pack(f"<{len(words)}H", *words)
+        return body + bytes(pad16(len(body)) - len(body)), False
+    return bytes(symbols) + bytes(pad16(n) - n), True
+
+
+def compress_shared(words_in: list[int], dtype: str, block_bytes: int, mode: int, ext=None) -> bytes:
+    e = EB[dtype]
+    n = len(words_in)
+    be = block_bytes // e
+    nb = -(-n // be)
+    planes = [to_planes(dtype, w) for w in words_in]
+    f = table_all([s for s, _ in planes[:SAMPLE_BYTES // e]]) if mode == 1 else list(ext)
+    secs = [shared_section([s for s, _ in planes[b * be:(b + 1) * be]], f) for b in range(nb)]
+    ends, end = [], 0
+    for sec, stored in secs:
+        end += len(sec)
+        ends.append((0x80000000 if stored else 0) | (end // 16))
+    dir_bytes = struct.pack(f"<{nb}I", *ends)
+    table_bytes = struct.pack("<256H", *f) if (mode == 1 and nb) else b""
+    raw = b"".join(r.to_bytes(e - 1, "little") for _, r in planes)
+    body = (dir_bytes + bytes(pad16(len(dir_bytes)) - len(dir_bytes)) + table_bytes
+            + raw + bytes(pad16(len(raw)) - len(raw)) + b"".join(sec for sec, _ in secs))
+    return struct.pack("<IBBBBIIQQ", 0x31505A55, 1, CODE[dtype], 11, mode, be, nb, n, 32 + len(body)) + body
+
+
+def decompress_shared(stream: bytes, dtype: str, n: int, ext=None) -> list[int]:
+    e = EB[dtype]
+    magic, ver, code, pb, mode, be, nb, n2, total = struct.unpack_from("<IBBBBIIQQ", stream, 0)
+    assert (magic, ver, code, pb, n2) == (0x31505A55, 1, CODE[dtype], 11, n) and mode in (1, 2)
+    tab_off = 32 + pad16(4 * nb)
+    if mode == 1:
+        f = list(struct.unpack_from("<256H", stream, tab_off)) if nb else [M // 256] * 256
+        raw_off = tab_off + (512 if nb else 0)
+    else:
+        f, raw_off = list(ext), tab_off
+    assert min(f) >= 1 and sum(f) == M
+    coded = raw_off + pad16((e - 1) * n)
+    out, start = [], 0
+    for b in range(nb):
+        d = struct.unpack_from("<I", stream, 32 + 4 * b)[0]
+        end = 16 * (d & 0x7FFFFFFF)
+        sec = stream[coded + start:coded + end]
+        nbk = min(be, n - b * be)
+        if d >> 31:
+            syms = list(sec[:nbk])
+        else:
+            states = list(struct.unpack_from("<64I", sec, 0))
+            words = list(struct.unpack_from(f"<{(len(sec) - 256) // 2}H", sec, 256))
+            syms = decode(states, words, f, nbk)
+        for q, s in enumerate(syms):
+            i = b * be + q
+            raw = int.from_bytes(stream[raw_off + (e - 1) * i: raw_off + (e - 1) * (i + 1)], "little")
+            out.append(from_planes(dtype, s, raw))
+        start = end
+    assert coded + start == total
+    return out

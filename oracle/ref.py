@@ -25,6 +25,8 @@ ELEM_BYTES = {"bf16": 2, "fp16": 2, "fp32": 4, "e4m3fn": 2, "e5m2": 2}
 BITS_DTYPE = {"bf16": np.uint16, "fp16": np.uint16, "fp32": np.uint32, "e4m3fn": np.uint16, "e5m2": np.uint16}
 
 REF_EINVAL, REF_ENOSPC, REF_ECORRUPT = -1, -2, -3
+# stream-wide table modes (sections 3.3.1 and 3.4)
+TABLE_MODES = {"per_block": 0, "sampled": 1, "external": 2}
 
 
 def build() -> str:
@@ -45,7 +47,7 @@ _lib = None
 def lib() -> ctypes.CDLL:
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
+        if not os.path.exists(LIB_PATH) or os.path.getmtime(LIB_PATH) < os.path.getmtime(SRC):
             build()
         L = ctypes.CDLL(LIB_PATH)
         vp, u8p = ctypes.c_void_p, ctypes.c_void_p
@@ -67,6 +69,14 @@ def lib() -> ctypes.CDLL:
         L.ref_compress.restype = i64
         L.ref_decompress.argtypes = [u8p, u64, ctypes.c_int, u64, vp]
         L.ref_decompress.restype = ctypes.c_int
+        L.ref_build_table_all.argtypes = [vp, u64, vp]
+        L.ref_sampled_table.argtypes = [vp, u64, ctypes.c_int, vp]
+        L.ref_max_compressed_size_mode.argtypes = [ctypes.c_int, u64, u32, ctypes.c_int]
+        L.ref_max_compressed_size_mode.restype = u64
+        L.ref_compress_table.argtypes = [vp, u64, ctypes.c_int, u32, ctypes.c_int, vp, u8p, u64]
+        L.ref_compress_table.restype = i64
+        L.ref_decompress_table.argtypes = [u8p, u64, ctypes.c_int, u64, vp, vp]
+        L.ref_decompress_table.restype = ctypes.c_int
         L.ref_reduce.argtypes = [vp, vp, ctypes.c_int, vp, ctypes.c_int, u64, u32, vp, u8p, u64]
         L.ref_reduce.restype = i64
         L.ref_half_to_float.argtypes = [u32]
@@ -163,6 +173,53 @@ def decompress(stream: np.ndarray, dtype: str, n: int):
     s = np.ascontiguousarray(stream, dtype=np.uint8)
     out = np.zeros(max(n, 1), BITS_DTYPE[dtype])
     rc = lib().ref_decompress(_ptr(s), s.size, DTYPES[dtype], n, _ptr(out))
+    if rc != 0:
+        return None
+    return out[:n]
+
+
+def build_table_all(count, n_s: int) -> np.ndarray:
+    """All-symbol table freq[256] of a histogram over n_s symbols."""
+    c = np.ascontiguousarray(count, dtype=np.uint32)
+    assert c.shape == (256,)
+    f = np.zeros(256, np.uint32)
+    lib().ref_build_table_all(_ptr(c), n_s, _ptr(f))
+    return f
+
+
+def sampled_table(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Stream-wide table from the first 256 KiB of ``x`` (uint32[256])."""
+    xb = _bits(x, dtype).ravel()
+    f = np.zeros(256, np.uint32)
+    lib().ref_sampled_table(_ptr(xb) if xb.size else None, xb.size, DTYPES[dtype], _ptr(f))
+    return f
+
+
+def max_compressed_size_mode(dtype: str, n: int, block_bytes: int, mode: str) -> int:
+    return lib().ref_max_compressed_size_mode(DTYPES[dtype], n, block_bytes, TABLE_MODES[mode])
+
+
+def compress_table(x: np.ndarray, dtype: str, block_bytes: int, mode: str, table=None) -> np.ndarray:
+    """Compress with a table mode; ``table`` (256 frequencies) for "external"."""
+    xb = _bits(x, dtype).ravel()
+    n = xb.size
+    cap = max_compressed_size_mode(dtype, n, block_bytes, mode)
+    out = np.zeros(cap, np.uint8)
+    t = None if table is None else np.ascontiguousarray(table, dtype=np.uint16)
+    total = lib().ref_compress_table(_ptr(xb) if n else None, n, DTYPES[dtype], block_bytes,
+                                     TABLE_MODES[mode], _ptr(t) if t is not None else None, _ptr(out), cap)
+    if total < 0:
+        raise ValueError(f"ref_compress_table failed: {total}")
+    return out[:total]
+
+
+def decompress_table(stream: np.ndarray, dtype: str, n: int, table=None):
+    """Decodes any table mode; None if the stream (or table) is rejected."""
+    s = np.ascontiguousarray(stream, dtype=np.uint8)
+    out = np.zeros(max(n, 1), BITS_DTYPE[dtype])
+    t = None if table is None else np.ascontiguousarray(table, dtype=np.uint16)
+    rc = lib().ref_decompress_table(_ptr(s), s.size, DTYPES[dtype], n, _ptr(t) if t is not None else None,
+                                    _ptr(out))
     if rc != 0:
         return None
     return out[:n]

@@ -59,6 +59,21 @@
  *   zero pad to 16.  A block is CODED iff 288 + 2k + 2W < n_b; otherwise it
  *   is STORED: its n_b symbol bytes, zero-padded to 16.
  *
+ *   Stream-wide tables (the sampled localized table of section 3.3.1 and
+ *   the table sent once per collective of section 3.4; our reading).  The
+ *   header's flags byte names the table mode: 0 = a table per block (as
+ *   above), 1 = SAMPLED, 2 = EXTERNAL.  SAMPLED: one table for the whole
+ *   stream from the histogram c[256] of its first n_s = min(n, 262144 / E)
+ *   elements (the first 256 KiB); every symbol is covered, f[s] = 1 +
+ *   floor(c[s](M-256)/n_s) for all 256 symbols, the remainder to the most
+ *   frequent (ties: smallest), so a symbol the sample missed stays codable;
+ *   the table (u16 f[256], 512 bytes) follows the directory (when there is
+ *   at least one block) and the raw plane moves behind it.  EXTERNAL: the
+ *   caller's table (any f[256] >= 1 summing to M, e.g. a SAMPLED table of
+ *   an earlier call) codes every block and is not in the stream.  With a
+ *   stream-wide table a CODED section is u32 state[64] | u16 word[W] | zero
+ *   pad to 16, and a block is CODED iff 256 + 2W < n_b.
+ *
  *   Fused reduce (section 3.4: decompress, reduce, recompress).  Element by
  *   element, acc = x_0, then acc = acc + x_i for i = 1.. in input order in
  *   IEEE binary32 (round to nearest even, subnormals kept), the optional raw
@@ -449,6 +464,224 @@ int ref_decompress(const uint8_t *in, uint64_t in_bytes, int dtype, uint64_t n,
       uint64_t n_words = (len - o) / 2;
       uint16_t *words = (uint16_t *)malloc((size_t)(n_words + 1) * sizeof(uint16_t));
       for (uint64_t q = 0; q < n_words; ++q) words[q] = (uint16_t)get16(sec + o + 2 * q);
+      int64_t used = ref_rans_decode(state, words, n_words, freq, cum, n_b, sym);
+      free(words);
+      if (used < 0) {
+        rc = REF_ECORRUPT;
+        break;
+      }
+    }
+    for (uint32_t i = 0; i < n_b; ++i) {
+      uint32_t raw = 0;
+      for (uint32_t q = 0; q + 1 < E; ++q)
+        raw |= (uint32_t)in[raw_off + (uint64_t)(E - 1) * (lo + i) + q] << (8 * q);
+      store_elem(out, dtype, lo + i, ref_merge_word(dtype, sym[i], raw));
+    }
+    start = end;
+  }
+  if (rc == 0 && coded_off + start != total) rc = REF_ECORRUPT;
+  free(sym);
+  return rc;
+}
+
+/* ------------------------------------------------------------------ */
+/* Stream-wide tables (sections 3.3.1 and 3.4)                         */
+/* ------------------------------------------------------------------ */
+#define SAMPLE_BYTES 262144u
+#define SHARED_SECTION_FIXED 256u /* 64 states */
+
+void ref_build_table_all(const uint32_t *count, uint64_t n_s, uint32_t *freq) {
+  if (n_s == 0) {
+    for (int s = 0; s < 256; ++s) freq[s] = M_TOTAL / 256u;
+    return;
+  }
+  uint32_t total = 0;
+  for (int s = 0; s < 256; ++s) {
+    freq[s] = 1u + (uint32_t)(((uint64_t)count[s] * (M_TOTAL - 256u)) / n_s);
+    total += freq[s];
+  }
+  int best = 0;
+  for (int s = 1; s < 256; ++s)
+    if (count[s] > count[best]) best = s;
+  freq[best] += M_TOTAL - total;
+}
+
+void ref_sampled_table(const void *in, uint64_t n, int dtype, uint32_t *freq) {
+  uint64_t n_s = SAMPLE_BYTES / elem_bytes(dtype);
+  if (n_s > n) n_s = n;
+  uint32_t count[256] = {0};
+  for (uint64_t i = 0; i < n_s; ++i) {
+    uint32_t s, raw;
+    ref_split_word(dtype, load_elem(in, dtype, i), &s, &raw);
+    count[s] += 1;
+  }
+  ref_build_table_all(count, n_s, freq);
+}
+
+static int table_ok(const uint32_t *freq) {
+  uint32_t sum = 0;
+  for (int s = 0; s < 256; ++s) {
+    if (freq[s] == 0 || freq[s] > M_TOTAL) return 0;
+    sum += freq[s];
+  }
+  return sum == M_TOTAL;
+}
+
+static uint64_t table_bytes(int mode, uint64_t nb) {
+  return (mode == REF_TABLE_SAMPLED && nb > 0) ? REF_TABLE_BYTES : 0;
+}
+
+uint64_t ref_max_compressed_size_mode(int dtype, uint64_t n, uint32_t block_bytes, int mode) {
+  uint64_t be = block_bytes / elem_bytes(dtype);
+  return ref_max_compressed_size(dtype, n, block_bytes) + table_bytes(mode, (n + be - 1) / be);
+}
+
+/* one block's section under a stream-wide table */
+static int64_t shared_block_section(const void *in, uint64_t n, int dtype, uint64_t be, uint64_t b,
+                                    const uint32_t *freq, const uint32_t *cum, uint8_t *sec,
+                                    int *stored) {
+  uint64_t lo = b * be;
+  uint32_t n_b = (uint32_t)((lo + be < n ? lo + be : n) - lo);
+  uint8_t *sym = (uint8_t *)malloc(n_b);
+  uint16_t *words = (uint16_t *)malloc((size_t)n_b * sizeof(uint16_t) + 16);
+  uint32_t state[LANES];
+  for (uint32_t i = 0; i < n_b; ++i) {
+    uint32_t s, raw;
+    ref_split_word(dtype, load_elem(in, dtype, lo + i), &s, &raw);
+    sym[i] = (uint8_t)s;
+  }
+  int64_t w = ref_rans_encode(sym, n_b, freq, cum, state, words, n_b);
+  uint64_t coded_len = SHARED_SECTION_FIXED + (w < 0 ? 2u * (uint64_t)n_b : 2u * (uint64_t)w);
+  int64_t len;
+  if (w >= 0 && coded_len < n_b) {
+    len = (int64_t)pad16(coded_len);
+    memset(sec, 0, (size_t)len);
+    for (uint32_t j = 0; j < LANES; ++j) put32(sec + 4 * j, state[j]);
+    for (int64_t q = 0; q < w; ++q) put16(sec + SHARED_SECTION_FIXED + 2 * q, words[q]);
+    *stored = 0;
+  } else {
+    len = (int64_t)pad16(n_b);
+    memset(sec, 0, (size_t)len);
+    memcpy(sec, sym, n_b);
+    *stored = 1;
+  }
+  free(sym);
+  free(words);
+  return len;
+}
+
+int64_t ref_compress_table(const void *in, uint64_t n, int dtype, uint32_t block_bytes,
+                           int mode, const uint16_t *table, uint8_t *out, uint64_t out_cap) {
+  if (mode == REF_TABLE_PER_BLOCK) return ref_compress(in, n, dtype, block_bytes, out, out_cap);
+  if (dtype < 0 || dtype > 4 || !valid_block_bytes(block_bytes)) return REF_EINVAL;
+  if (mode != REF_TABLE_SAMPLED && mode != REF_TABLE_EXTERNAL) return REF_EINVAL;
+  uint32_t E = elem_bytes(dtype);
+  uint64_t be = block_bytes / E;
+  uint64_t nb = (n + be - 1) / be;
+  if (nb >= 0x80000000ull) return REF_EINVAL;
+  if (out_cap < ref_max_compressed_size_mode(dtype, n, block_bytes, mode)) return REF_ENOSPC;
+  uint32_t freq[256], cum[256];
+  if (mode == REF_TABLE_SAMPLED) {
+    ref_sampled_table(in, n, dtype, freq);
+  } else {
+    if (table == NULL) return REF_EINVAL;
+    for (int s = 0; s < 256; ++s) freq[s] = table[s];
+    if (!table_ok(freq)) return REF_EINVAL;
+  }
+  uint32_t run = 0;
+  for (int s = 0; s < 256; ++s) {
+    cum[s] = run;
+    run += freq[s];
+  }
+  uint64_t table_off = raw_offset(nb);
+  uint64_t raw_off = table_off + table_bytes(mode, nb);
+  uint64_t coded_off = raw_off + pad16((uint64_t)(E - 1) * n);
+  memset(out, 0, (size_t)coded_off);
+  if (table_bytes(mode, nb))
+    for (int s = 0; s < 256; ++s) put16(out + table_off + 2 * s, freq[s]);
+  for (uint64_t i = 0; i < n; ++i) {
+    uint32_t s, raw;
+    ref_split_word(dtype, load_elem(in, dtype, i), &s, &raw);
+    for (uint32_t q = 0; q + 1 < E; ++q)
+      out[raw_off + (uint64_t)(E - 1) * i + q] = (uint8_t)(raw >> (8 * q));
+  }
+  uint64_t off = 0;
+  for (uint64_t b = 0; b < nb; ++b) {
+    int stored = 0;
+    int64_t len = shared_block_section(in, n, dtype, be, b, freq, cum, out + coded_off + off, &stored);
+    off += (uint64_t)len;
+    put32(out + HEADER_BYTES + 4 * b, (stored ? 0x80000000u : 0u) | (uint32_t)(off / 16));
+  }
+  uint64_t total = coded_off + off;
+  put32(out + 0, MAGIC);
+  out[4] = 1;
+  out[5] = (uint8_t)dtype;
+  out[6] = (uint8_t)PROB_BITS;
+  out[7] = (uint8_t)mode;
+  put32(out + 8, (uint32_t)be);
+  put32(out + 12, (uint32_t)nb);
+  put64(out + 16, n);
+  put64(out + 24, total);
+  return (int64_t)total;
+}
+
+int ref_decompress_table(const uint8_t *in, uint64_t in_bytes, int dtype, uint64_t n,
+                         const uint16_t *table, void *out) {
+  if (in_bytes < HEADER_BYTES) return REF_ECORRUPT;
+  int mode = in[7];
+  if (mode == REF_TABLE_PER_BLOCK) return ref_decompress(in, in_bytes, dtype, n, out);
+  if (mode != REF_TABLE_SAMPLED && mode != REF_TABLE_EXTERNAL) return REF_ECORRUPT;
+  if (mode == REF_TABLE_EXTERNAL && table == NULL) return REF_EINVAL;
+  if (get32(in) != MAGIC || in[4] != 1 || in[5] != dtype || in[6] != PROB_BITS) return REF_ECORRUPT;
+  uint32_t E = elem_bytes(dtype);
+  uint64_t be = get32(in + 8), nb = get32(in + 12);
+  if (get64(in + 16) != n || be == 0 || !valid_block_bytes((uint32_t)(be * E))) return REF_ECORRUPT;
+  if (nb != (n + be - 1) / be) return REF_ECORRUPT;
+  uint64_t total = get64(in + 24);
+  uint64_t table_off = raw_offset(nb);
+  uint64_t raw_off = table_off + table_bytes(mode, nb);
+  uint64_t coded_off = raw_off + pad16((uint64_t)(E - 1) * n);
+  if (total > in_bytes || total < coded_off) return REF_ECORRUPT;
+  uint32_t freq[256], cum[256];
+  for (int s = 0; s < 256; ++s)
+    freq[s] = mode == REF_TABLE_SAMPLED ? (nb > 0 ? get16(in + table_off + 2 * s) : M_TOTAL / 256u)
+                                        : table[s];
+  if (!table_ok(freq)) return mode == REF_TABLE_SAMPLED ? REF_ECORRUPT : REF_EINVAL;
+  uint32_t run = 0;
+  for (int s = 0; s < 256; ++s) {
+    cum[s] = run;
+    run += freq[s];
+  }
+  uint8_t *sym = (uint8_t *)malloc(be ? be : 1);
+  uint64_t start = 0;
+  int rc = 0;
+  for (uint64_t b = 0; b < nb && rc == 0; ++b) {
+    uint32_t d = get32(in + HEADER_BYTES + 4 * b);
+    uint64_t end = 16ull * (d & 0x7FFFFFFFu);
+    if (end < start || coded_off + end > total) {
+      rc = REF_ECORRUPT;
+      break;
+    }
+    const uint8_t *sec = in + coded_off + start;
+    uint64_t len = end - start;
+    uint64_t lo = b * be;
+    uint32_t n_b = (uint32_t)((lo + be < n ? lo + be : n) - lo);
+    if (d & 0x80000000u) {
+      if (len < n_b) {
+        rc = REF_ECORRUPT;
+        break;
+      }
+      memcpy(sym, sec, n_b);
+    } else {
+      if (len < SHARED_SECTION_FIXED) {
+        rc = REF_ECORRUPT;
+        break;
+      }
+      uint32_t state[LANES];
+      for (uint32_t j = 0; j < LANES; ++j) state[j] = get32(sec + 4 * j);
+      uint64_t n_words = (len - SHARED_SECTION_FIXED) / 2;
+      uint16_t *words = (uint16_t *)malloc((size_t)(n_words + 1) * sizeof(uint16_t));
+      for (uint64_t q = 0; q < n_words; ++q) words[q] = (uint16_t)get16(sec + SHARED_SECTION_FIXED + 2 * q);
       int64_t used = ref_rans_decode(state, words, n_words, freq, cum, n_b, sym);
       free(words);
       if (used < 0) {

@@ -85,6 +85,33 @@ int64_t ref_compress(const void *in, uint64_t n, int dtype,
 int ref_decompress(const uint8_t *in, uint64_t in_bytes, int dtype, uint64_t n,
                    void *out);
 
+/* ---- stream-wide tables (sections 3.3.1 and 3.4) ----
+ * Table modes: REF_TABLE_PER_BLOCK is the stream above.  REF_TABLE_SAMPLED
+ * builds one table for the whole stream from its first
+ * min(n, 262144 / E) elements (the first 256 KiB) and stores it once, after
+ * the directory.  REF_TABLE_EXTERNAL codes with a table the caller holds
+ * (built once, reused across calls) and leaves it out of the stream.
+ * A stream-wide table gives every one of the 256 symbols a frequency of
+ * at least 1, so symbols outside the sample stay codable. */
+#define REF_TABLE_PER_BLOCK 0
+#define REF_TABLE_SAMPLED 1
+#define REF_TABLE_EXTERNAL 2
+#define REF_TABLE_BYTES 512u
+/* freq[256] of the sampled table of the first min(n, 262144 / E) elements
+ * (sums to 2048, every entry >= 1) */
+void ref_sampled_table(const void *in, uint64_t n, int dtype, uint32_t *freq);
+/* counts[256] over n_s symbols -> all-symbol table freq[256] */
+void ref_build_table_all(const uint32_t *count, uint64_t n_s, uint32_t *freq);
+/* largest stream of a mode (SAMPLED adds the table) */
+uint64_t ref_max_compressed_size_mode(int dtype, uint64_t n, uint32_t block_bytes, int mode);
+/* table: freq[256] as u16, required for EXTERNAL (ignored otherwise).
+ * Returns total stream bytes or a negative error. */
+int64_t ref_compress_table(const void *in, uint64_t n, int dtype, uint32_t block_bytes,
+                           int mode, const uint16_t *table, uint8_t *out, uint64_t out_cap);
+/* Decodes any mode; table is required for EXTERNAL streams. */
+int ref_decompress_table(const uint8_t *in, uint64_t in_bytes, int dtype, uint64_t n,
+                         const uint16_t *table, void *out);
+
 /* ---- fused reduce (section 3.4) ----
  * ins[i] are n_in streams of the same dtype, n and block size.  local_raw
  * (may be NULL) is an uncompressed addend taken last.  y (n elements of

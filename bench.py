@@ -204,6 +204,42 @@ def main() -> int:
                             "ratio_out": round(int(rsz.item()) / (2 * rn), 4)}
         log(f"[bench] fused reduce {r_ms:.3f} ms")
 
+        # ------------- stream-wide tables: the same buffer, one table per stream -------------
+        tws = torch.empty(uz.uzip_workspace_size(uz.OP_COMPRESS_TABLE, uz.BF16, n, bb), dtype=torch.uint8, device=dev)
+        tout = torch.empty(cap + uz.TABLE_BYTES, dtype=torch.uint8, device=dev)
+        ty = torch.empty_like(x)
+        tab = uz.build_table(x, dtype="bf16")
+        for mode in ("sampled", "external"):
+            tabarg = tab if mode == "external" else None
+            for _ in range(2):
+                _, tsz = uz.compress_table(x, bb, mode, tabarg, dtype="bf16", out=tout, ws=tws)
+                _, tst = uz.decompress_table(tout, "bf16", n, tabarg, out=ty, ws=dws)
+            torch.cuda.synchronize()
+            if int(tst.item()) != 0 or not torch.equal(x, ty):
+                log(f"[bench] table mode {mode}: round trip is NOT lossless")
+                return 1
+            tsize = int(tsz.item())
+            ct, dt_ = [], []
+            for _ in range(reps):
+                e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+                e[0].record(stream)
+                uz.compress_table(x, bb, mode, tabarg, dtype="bf16", out=tout, ws=tws)
+                e[1].record(stream)
+                uz.decompress_table(tout, "bf16", n, tabarg, out=ty, ws=dws)
+                e[2].record(stream)
+                torch.cuda.synchronize()
+                ct.append(e[0].elapsed_time(e[1]))
+                dt_.append(e[1].elapsed_time(e[2]))
+            fc, fd = float(np.mean(ct)), float(np.mean(dt_))
+            moved = nbytes + tsize
+            extras[f"table_{mode}"] = {"ratio": round(tsize / nbytes, 5),
+                                       "ratio_cost_vs_per_block": round(tsize / total - 1, 4),
+                                       "compress_ms": round(fc, 4), "decompress_ms": round(fd, 4),
+                                       "compress_frac": round(moved / (fc * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                                       "decompress_frac": round(moved / (fd * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)}
+            log(f"[bench] table {mode}: ratio {tsize / nbytes:.4f} compress {fc:.3f} ms decompress {fd:.3f} ms")
+        del tws, tout, ty
+
         # ------------- FP8 pairs: 1 GiB of e4m3fn / e5m2 values N(0, 1) -------------
         del cout, cws, rout, rws, streams
         for fmt, code in (("e4m3fn", uz.E4M3FN), ("e5m2", uz.E5M2)):

@@ -86,7 +86,27 @@ typedef enum {
 } uzip_status;
 
 /* operation codes for uzip_workspace_size */
-enum { UZIP_OP_COMPRESS = 0, UZIP_OP_DECOMPRESS = 1, UZIP_OP_REDUCE = 2, UZIP_OP_CHUNKED = 3 };
+enum {
+  UZIP_OP_COMPRESS = 0,
+  UZIP_OP_DECOMPRESS = 1, /* also uzip_decompress_table */
+  UZIP_OP_REDUCE = 2,
+  UZIP_OP_CHUNKED = 3,
+  UZIP_OP_COMPRESS_TABLE = 4
+};
+
+/* Table modes (sections 3.3.1 and 3.4).  PER_BLOCK: every block carries
+ * its own table (the plain stream).  SAMPLED: one table for the whole
+ * stream, built from the symbols of its first 256 KiB (min(n, 262144 / E)
+ * elements) and stored once after the directory.  EXTERNAL: the caller's
+ * table (for example one uzip_build_table made in an earlier call) codes
+ * every block and is not stored: section 3.4's table sent once and reused.
+ * A stream-wide table is u16 f[256] (UZIP_TABLE_BYTES bytes) with every
+ * f >= 1 and sum 2048: f[s] = 1 + floor(c[s] * 1792 / n_s) over the
+ * sample's symbol counts c, the remainder to the most frequent symbol
+ * (ties: the smallest), so a symbol the sample missed stays codable.  Its
+ * sections hold the 64 states and the words only. */
+typedef enum { UZIP_TABLE_PER_BLOCK = 0, UZIP_TABLE_SAMPLED = 1, UZIP_TABLE_EXTERNAL = 2 } uzip_table_mode;
+#define UZIP_TABLE_BYTES 512
 
 /* Largest possible stream for n_elems values (every block STORED), in
  * bytes.  Section 4.1's "size after compression" never exceeds it.
@@ -128,6 +148,36 @@ uzip_status uzip_decompress(const void *d_in, size_t in_bytes, uzip_dtype dtype,
                             uint64_t n_elems, void *d_out, size_t out_cap,
                             uint32_t *d_status, void *d_ws, size_t ws_bytes,
                             hipStream_t stream);
+
+/* The stream-wide table of a tensor (section 3.3.1): from the symbols of
+ * its first min(n_elems, 262144 / E) elements, as UZIP_TABLE_SAMPLED builds
+ * it.  d_table: UZIP_TABLE_BYTES of device memory, 16-byte aligned.
+ * Errors: EINVAL, EHIP, EUNSUPPORTED. */
+uzip_status uzip_build_table(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint16_t *d_table,
+                             hipStream_t stream);
+
+/* Compress with a table mode (sections 3.3.1 and 3.4).  As uzip_compress,
+ * and:
+ *   mode:           PER_BLOCK is uzip_compress itself.
+ *   d_table:        EXTERNAL only: the table (u16 f[256], 16-byte aligned).
+ *                   One that is not an all-symbol table (an f of 0, or a
+ *                   sum other than 2048) codes nothing and *d_out_size
+ *                   reads 0.
+ *   out_cap:        >= uzip_max_compressed_size + UZIP_TABLE_BYTES.
+ *   d_ws, ws_bytes: uzip_workspace_size(UZIP_OP_COMPRESS_TABLE, ...).
+ * Errors: EINVAL, ENOSPC, EHIP, EUNSUPPORTED. */
+uzip_status uzip_compress_table(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint32_t block_bytes,
+                                uzip_table_mode mode, const uint16_t *d_table, void *d_out, size_t out_cap,
+                                uint64_t *d_out_size, void *d_ws, size_t ws_bytes, hipStream_t stream);
+
+/* Decompress a stream of mode SAMPLED or EXTERNAL (a PER_BLOCK stream, or
+ * an EXTERNAL one without d_table, sets *d_status to UZIP_ECORRUPT; so
+ * does a table that is not an all-symbol table).  d_table: the table the
+ * stream was coded with (EXTERNAL; ignored for SAMPLED; may be NULL),
+ * 16-byte aligned.  Otherwise as uzip_decompress. */
+uzip_status uzip_decompress_table(const void *d_in, size_t in_bytes, uzip_dtype dtype, uint64_t n_elems,
+                                  const uint16_t *d_table, void *d_out, size_t out_cap, uint32_t *d_status,
+                                  void *d_ws, size_t ws_bytes, hipStream_t stream);
 
 /* Fused decompress -> reduce -> recompress of one rank's share (section
  * 3.4, the CopyReducePacks step with compression fused in).

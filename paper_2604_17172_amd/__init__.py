@@ -28,7 +28,9 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 BF16, FP16, FP32, E4M3FN, E5M2 = 0, 1, 2, 3, 4
-OP_COMPRESS, OP_DECOMPRESS, OP_REDUCE, OP_CHUNKED = 0, 1, 2, 3
+OP_COMPRESS, OP_DECOMPRESS, OP_REDUCE, OP_CHUNKED, OP_COMPRESS_TABLE = 0, 1, 2, 3, 4
+TABLE_PER_BLOCK, TABLE_SAMPLED, TABLE_EXTERNAL = 0, 1, 2
+TABLE_BYTES = 512
 WS_NO_OUT_RAW = 1 << 16
 OK, EINVAL, ENOSPC, ECORRUPT, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 
@@ -48,11 +50,18 @@ _lib.uzip_reduce_fused.argtypes = [_c.POINTER(_vp), _c.POINTER(_sz), _int, _vp, 
 _lib.uzip_reduce_fused.restype = _int
 _lib.uzip_compress_chunked.argtypes = [_vp, _u64, _int, _u32, _u64, _vp, _sz, _vp, _vp, _u32, _vp, _sz, _vp]
 _lib.uzip_compress_chunked.restype = _int
+_lib.uzip_build_table.argtypes = [_vp, _u64, _int, _vp, _vp]
+_lib.uzip_build_table.restype = _int
+_lib.uzip_compress_table.argtypes = [_vp, _u64, _int, _u32, _int, _vp, _vp, _sz, _vp, _vp, _sz, _vp]
+_lib.uzip_compress_table.restype = _int
+_lib.uzip_decompress_table.argtypes = [_vp, _sz, _int, _u64, _vp, _vp, _sz, _vp, _vp, _sz, _vp]
+_lib.uzip_decompress_table.restype = _int
 _lib.uzip_status_str.argtypes = [_int]
 _lib.uzip_status_str.restype = _c.c_char_p
 
 EXPORTED = ["uzip_max_compressed_size", "uzip_workspace_size", "uzip_compress", "uzip_decompress",
-            "uzip_reduce_fused", "uzip_compress_chunked", "uzip_status_str"]
+            "uzip_reduce_fused", "uzip_compress_chunked", "uzip_status_str", "uzip_build_table",
+            "uzip_compress_table", "uzip_decompress_table"]
 
 
 class UzipError(RuntimeError):
@@ -90,6 +99,22 @@ def uzip_compress_chunked(d_in, n_elems, dtype, block_bytes, chunk_bytes, d_out,
                           flags, epoch, d_ws, ws_bytes, stream) -> int:
     return _lib.uzip_compress_chunked(d_in, n_elems, dtype, block_bytes, chunk_bytes, d_out, slot_bytes,
                                       chunk_sizes, flags, epoch, d_ws, ws_bytes, stream)
+
+
+def uzip_build_table(d_in, n_elems, dtype, d_table, stream) -> int:
+    return _lib.uzip_build_table(d_in, n_elems, dtype, d_table, stream)
+
+
+def uzip_compress_table(d_in, n_elems, dtype, block_bytes, mode, d_table, d_out, out_cap, d_out_size, d_ws,
+                        ws_bytes, stream) -> int:
+    return _lib.uzip_compress_table(d_in, n_elems, dtype, block_bytes, mode, d_table, d_out, out_cap, d_out_size,
+                                    d_ws, ws_bytes, stream)
+
+
+def uzip_decompress_table(d_in, in_bytes, dtype, n_elems, d_table, d_out, out_cap, d_status, d_ws, ws_bytes,
+                          stream) -> int:
+    return _lib.uzip_decompress_table(d_in, in_bytes, dtype, n_elems, d_table, d_out, out_cap, d_status, d_ws,
+                                      ws_bytes, stream)
 
 
 def uzip_status_str(status: int) -> str:
@@ -227,3 +252,60 @@ def compress_chunked(x: torch.Tensor, block_bytes: int, chunk_bytes: int, dtype=
                                  slot, sizes.data_ptr(), flags.data_ptr(), epoch, ws.data_ptr(), ws.numel(),
                                  _stream(stream)), "uzip_compress_chunked")
     return out, slot, sizes, flags
+
+
+_MODE = {"per_block": TABLE_PER_BLOCK, "sampled": TABLE_SAMPLED, "external": TABLE_EXTERNAL}
+
+
+def build_table(x: torch.Tensor, dtype=None, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """The stream-wide table of ``x`` (from its first 256 KiB): int16[256]
+    holding the u16 frequencies."""
+    assert x.is_cuda and x.is_contiguous()
+    dt = dtype_code(dtype if dtype is not None else x.dtype)
+    n = _n_elems(x, dt)
+    if out is None:
+        out = torch.empty(256, dtype=torch.int16, device=x.device)
+    _check(uzip_build_table(x.data_ptr() if n else None, n, dt, out.data_ptr(), _stream(stream)), "uzip_build_table")
+    return out
+
+
+def compress_table(x: torch.Tensor, block_bytes: int, mode="sampled", table: torch.Tensor | None = None, dtype=None,
+                   out: torch.Tensor | None = None, ws: torch.Tensor | None = None, stream=None):
+    """Compress with a table mode ("per_block", "sampled", "external" with
+    ``table``).  Returns (stream buffer, device u64 size)."""
+    assert x.is_cuda and x.is_contiguous()
+    dt = dtype_code(dtype if dtype is not None else x.dtype)
+    md = _MODE[mode] if isinstance(mode, str) else mode
+    n = _n_elems(x, dt)
+    cap = uzip_max_compressed_size(dt, n, block_bytes)
+    if cap == 0:
+        _check(EINVAL, "uzip_compress_table")
+    cap += TABLE_BYTES
+    if out is None:
+        out = _dev_empty(cap, x.device)
+    wsb = uzip_workspace_size(OP_COMPRESS_TABLE, dt, n, block_bytes)
+    if ws is None:
+        ws = _dev_empty(wsb, x.device)
+    size = torch.zeros(1, dtype=torch.int64, device=x.device)
+    _check(uzip_compress_table(x.data_ptr() if n else None, n, dt, block_bytes, md,
+                               table.data_ptr() if table is not None else None, out.data_ptr(), out.numel(),
+                               size.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream)), "uzip_compress_table")
+    return out, size
+
+
+def decompress_table(s: torch.Tensor, dtype, n_elems: int, table: torch.Tensor | None = None,
+                     out: torch.Tensor | None = None, in_bytes: int | None = None, ws: torch.Tensor | None = None,
+                     stream=None):
+    """Decompress a stream with a stream-wide table.  Returns (bit-pattern
+    tensor, device u32 status)."""
+    dt = dtype_code(dtype)
+    if out is None:
+        out = torch.empty(max(n_elems, 1), dtype=_BITS[dt], device=s.device)[:n_elems]
+    status = torch.zeros(1, dtype=torch.int32, device=s.device)
+    nbytes = s.numel() * s.element_size() if in_bytes is None else in_bytes
+    if ws is None:
+        ws = _dev_empty(uzip_workspace_size(OP_DECOMPRESS, dt, n_elems, 65536, 0), s.device)
+    _check(uzip_decompress_table(s.data_ptr(), nbytes, dt, n_elems, table.data_ptr() if table is not None else None,
+                                 out.data_ptr() if n_elems else None, n_elems * _ELEM[dt], status.data_ptr(),
+                                 ws.data_ptr(), ws.numel(), _stream(stream)), "uzip_decompress_table")
+    return out, status

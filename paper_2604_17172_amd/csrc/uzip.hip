@@ -73,6 +73,11 @@ struct EncodeArgs {
   uint16_t *slots;
   uint32_t slot_words;
   uint32_t lds_words;       // staging words held in LDS
+  // stream-wide table (table modes 1, 2): frequencies f[256], the mode
+  // written to the header's flags byte, and the table bytes in the stream
+  const uint16_t *table;
+  uint32_t table_mode;
+  uint32_t table_bytes;
 };
 
 constexpr size_t kDecodeWsBytes = 256;   // the block ticket
@@ -85,6 +90,7 @@ struct DecodeArgs {
   uint8_t *out;
   uint32_t *dstatus;
   uint32_t *ticket;  // workspace: next block to decode
+  const uint16_t *table;  // the caller's table (streams of table mode 2)
 };
 
 // first error wins
@@ -264,6 +270,7 @@ __device__ __forceinline__ void wave_lds_fence() {
 // Entry for slot: f | (slot - cum) << 12 | sym << 24.
 // Returns false (uniformly) if the stored table is not a valid ANS table.
 // ---------------------------------------------------------------------------
+__device__ void fill_lut(const uint32_t f[4], uint32_t *lut, uint16_t *cum_s, uint16_t *f_s);
 __device__ bool build_lut(const uint8_t *sec, uint64_t sec_len, uint32_t *lut, uint16_t *cum_s,
                           uint16_t *f_s, uint32_t &k_out) {
   const uint32_t lane = lane_id();
@@ -292,7 +299,16 @@ __device__ bool build_lut(const uint8_t *sec, uint64_t sec_len, uint32_t *lut, u
                  (nib & 8 && f[3] == 0);
   ok = ok && !__any(bad) && wave_sum(total) == kM;
   if (!ok) return false;
-  uint32_t c = wave_excl_scan(total);
+  fill_lut(f, lut, cum_s, f_s);
+  k_out = k;
+  return true;
+}
+
+// The lookup table from this lane's frequencies f[4] of symbols 4 lane ..
+// 4 lane + 3 (summing to M over the wave).
+__device__ void fill_lut(const uint32_t f[4], uint32_t *lut, uint16_t *cum_s, uint16_t *f_s) {
+  const uint32_t lane = lane_id();
+  uint32_t c = wave_excl_scan(f[0] + f[1] + f[2] + f[3]);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     cum_s[4 * lane + q] = (uint16_t)c;
@@ -321,7 +337,17 @@ __device__ bool build_lut(const uint8_t *sec, uint64_t sec_len, uint32_t *lut, u
     lut[slot] = fs | ((slot - c0) << 12) | (s << 24);
   }
   wave_lds_fence();
-  k_out = k;
+}
+
+// Lookup table of a stream-wide table (u16 f[256] in memory): every symbol
+// has f >= 1 and the sum is M, else false (uniformly).
+__device__ bool build_lut_shared(const uint16_t *table, uint32_t *lut, uint16_t *cum_s, uint16_t *f_s) {
+  const uint32_t lane = lane_id();
+  const uint2 v = *(const uint2 *)(table + 4 * lane);
+  const uint32_t f[4] = {v.x & 0xFFFFu, v.x >> 16, v.y & 0xFFFFu, v.y >> 16};
+  const bool bad = f[0] == 0 || f[1] == 0 || f[2] == 0 || f[3] == 0;
+  if (__any(bad) || wave_sum(f[0] + f[1] + f[2] + f[3]) != kM) return false;
+  fill_lut(f, lut, cum_s, f_s);
   return true;
 }
 
@@ -339,6 +365,7 @@ struct Table {
 // for present symbols, the remainder to the most frequent symbol (ties to
 // the smallest), cum in ascending symbol order.  Writes the encoder table
 // {reciprocal, f << 20, (M - f) | shift << 24, cum (+2047 if f == 1)}.
+__device__ void enc_entries(const Table &t, uint4 *enc);
 __device__ void build_enc_table(const uint32_t *hist, uint32_t n_b, uint4 *enc, Table &t) {
   const uint32_t lane = lane_id();
   uint32_t c[4];
@@ -369,8 +396,17 @@ __device__ void build_enc_table(const uint32_t *hist, uint32_t n_b, uint4 *enc, 
 #pragma unroll
   for (uint32_t q = 0; q < 4; ++q)
     if (best == 4 * lane + q) t.f[q] += d;
-  lt = t.f[0] + t.f[1] + t.f[2] + t.f[3];
-  uint32_t cum = wave_excl_scan(lt);
+  t.k = k;
+  t.rank0 = wave_excl_scan(pres);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) t.present[q] = __ballot(c[q] > 0);
+  enc_entries(t, enc);
+}
+
+// Encoder table entries of this lane's frequencies t.f[4].
+__device__ void enc_entries(const Table &t, uint4 *enc) {
+  const uint32_t lane = lane_id();
+  uint32_t cum = wave_excl_scan(t.f[0] + t.f[1] + t.f[2] + t.f[3]);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     uint32_t f = t.f[q];
@@ -394,10 +430,6 @@ __device__ void build_enc_table(const uint32_t *hist, uint32_t n_b, uint4 *enc, 
     }
     cum += f;
   }
-  t.k = k;
-  t.rank0 = wave_excl_scan(pres);
-#pragma unroll
-  for (int q = 0; q < 4; ++q) t.present[q] = __ballot(c[q] > 0);
 }
 
 // Decoupled look-back over the blocks of one stream: returns the exclusive
@@ -637,7 +669,7 @@ __device__ __forceinline__ void hist_add8(uint32_t *h, const Group &g, uint32_t 
 //   workgroup's overflow slot.  Otherwise the coding pass re-reads the block
 //   and LDS holds the whole staging area.
 // ---------------------------------------------------------------------------
-template <int DT, bool REDUCE, bool SMALL, bool SYS>
+template <int DT, bool REDUCE, bool SMALL, bool SYS, bool SHARED = false>
 __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   constexpr int E = (DT == 2) ? 4 : 2;
   constexpr int NW = 4 * (E / 2);
@@ -653,6 +685,25 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   typedef __attribute__((address_space(3))) uint16_t lds16_t;
   // one private 4-byte slot per lane for words that are not emitted
   lds16_t *trash = (lds16_t *)smem_base + 2 * lane;
+  // a stream-wide table codes every block: its encoder entries once
+  if constexpr (SHARED) {
+    Table ts;
+    const uint2 v = *(const uint2 *)(a.table + 4 * lane);
+    ts.f[0] = v.x & 0xFFFFu;
+    ts.f[1] = v.x >> 16;
+    ts.f[2] = v.y & 0xFFFFu;
+    ts.f[3] = v.y >> 16;
+    ts.k = 256;
+    // a table that is not an all-symbol table (some f = 0, or a sum other
+    // than M) codes nothing: the stream size reads 0
+    const bool bad = ts.f[0] == 0 || ts.f[1] == 0 || ts.f[2] == 0 || ts.f[3] == 0;
+    if (__any(bad) || wave_sum(ts.f[0] + ts.f[1] + ts.f[2] + ts.f[3]) != kM) {
+      if (blockIdx.x == 0 && lane == 0 && a.sizes != nullptr) a.sizes[0] = 0;
+      return;
+    }
+    enc_entries(ts, enc);
+    __syncthreads();
+  }
 
   while (true) {
     uint32_t b = 0;
@@ -665,7 +716,10 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     const uint32_t first_block = b - lb;
     const uint64_t chunk_first = (uint64_t)chunk * a.chunk_elems;
     const uint64_t chunk_n = (a.n - chunk_first) < a.chunk_elems ? (a.n - chunk_first) : a.chunk_elems;
-    const Geom g = make_geom(chunk_n, a.block_elems, E);
+    Geom g = make_geom(chunk_n, a.block_elems, E);
+    const uint64_t dir_end = g.raw_off;  // a stored stream-wide table sits between the directory and the raw plane
+    g.raw_off += a.table_bytes;
+    g.coded_off += a.table_bytes;
     uint8_t *sout = a.out + (uint64_t)chunk * a.slot_bytes;
     const uint64_t blk0 = (uint64_t)lb * a.block_elems;  // chunk-relative
     const uint32_t n_b = (uint32_t)((chunk_n - blk0) < a.block_elems ? (chunk_n - blk0) : a.block_elems);
@@ -699,7 +753,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
           load_words<E>(src, blk0 + i0, valid, w);
           split_group<DT>(w, gr);
           store_raw<E, SYS>(raw_plane, blk0 + i0, valid, gr);
-          hist_add8(h, gr, valid);
+          if constexpr (!SHARED) hist_add8(h, gr, valid);
         }
         psym0 = gr.sym[0];
         psym1 = gr.sym[1];
@@ -733,7 +787,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
               S.v3[2 * rr + 1] = gr.sym[1];
               if (r < full) {
                 store_raw_round<E, SYS>(raw_blk + (uint64_t)r * kRound * (E - 1), gr);
-                hist_add8(h, gr, 8);
+                if constexpr (!SHARED) hist_add8(h, gr, 8);
               }
             }
             if (gi < 3) shift_down(S);
@@ -754,7 +808,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
               Group gr;
               split_group<DT>(w, gr);
               store_raw_round<E, SYS>(raw_blk + (uint64_t)(r + u) * kRound * (E - 1), gr);
-              hist_add8(h, gr, 8);
+              if constexpr (!SHARED) hist_add8(h, gr, 8);
             }
           }
 #pragma unroll
@@ -763,7 +817,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
               Group gr;
               split_group<DT>(buf[u], gr);
               store_raw_round<E, SYS>(raw_blk + (uint64_t)(r + u) * kRound * (E - 1), gr);
-              hist_add8(h, gr, 8);
+              if constexpr (!SHARED) hist_add8(h, gr, 8);
             }
           }
         }
@@ -788,14 +842,21 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     __builtin_amdgcn_s_setprio(0);
     // ---- table ----
     Table t;
-    build_enc_table(hist, n_b, enc, t);
-    t.k = uniform(t.k);
-    __syncthreads();
+    if constexpr (SHARED) {
+      t.k = 256;  // only the section head differs: no bitmap, no frequencies
+    } else {
+      build_enc_table(hist, n_b, enc, t);
+      t.k = uniform(t.k);
+      __syncthreads();
+    }
+    // section bytes before the words: states, and for a table of its own
+    // the presence bitmap and the frequencies
+    const uint32_t hdr = SHARED ? kSharedSectionFixed : kSectionFixed + 2 * t.k;
 
     // ---- pass 2: rANS over the block, backwards; words staged ----
     for (uint32_t i = lane; i < kStageTail / 4; i += 64)
       ((uint32_t *)(stage + kStageHead + 2 * a.lds_words))[i] = 0;
-    const uint32_t limit_words = (n_b > kSectionFixed + 2 * t.k) ? (n_b - kSectionFixed - 2 * t.k + 1) / 2 : 0;
+    const uint32_t limit_words = (n_b > hdr) ? (n_b - hdr + 1) / 2 : 0;
     uint32_t pos = a.wcap;  // virtual staging indices [pos, wcap) hold the words written so far
     // LDS window over virtual indices [lo, lo + lds_words); lds_rel[v] is index v
     uint32_t lo = a.wcap - a.lds_words;
@@ -882,7 +943,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     }
     pos = uniform(pos);
     const uint32_t n_words = a.wcap - pos;
-    const uint64_t img = kSectionFixed + 2ull * t.k + 2ull * n_words;
+    const uint64_t img = hdr + 2ull * n_words;
     const uint64_t sec_len = stored ? pad16(n_b) : pad16(img);
 
     // ---- output offset: single-pass scan over the stream's blocks ----
@@ -892,11 +953,11 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
       out32<SYS>((uint32_t *)(sout + kHeaderBytes + 4 * lb), (stored ? kStoredBit : 0u) | (uint32_t)(excl + sec_len / 16));
 
     if (!stored) {
-      const uint32_t hdr = kSectionFixed + 2 * t.k;
-      // header bytes: states | bitmap | f[k]
+      // header bytes: states | bitmap | f[k] (states only with a stream-wide table)
       auto put_header = [&](uint16_t *h16) {
         h16[2 * lane] = (uint16_t)x;
         h16[2 * lane + 1] = (uint16_t)(x >> 16);
+        if (SHARED) return;
         if (lane < 16) {
           uint32_t word = 0;
           for (uint32_t bit = 0; bit < 16; ++bit) {
@@ -1010,7 +1071,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
       if (lane == 0) {
         uint32_t hh[8];
         hh[0] = kMagic;
-        hh[1] = kVersion | ((uint32_t)DT << 8) | (kProbBits << 16);
+        hh[1] = kVersion | ((uint32_t)DT << 8) | (kProbBits << 16) | (a.table_mode << 24);
         hh[2] = a.block_elems;
         hh[3] = g.n_blocks;
         hh[4] = (uint32_t)chunk_n;
@@ -1027,7 +1088,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
       }
       // zero padding after the directory
       uint64_t db = kHeaderBytes + 4ull * g.n_blocks + lane;
-      if (lane < 16 && db < g.raw_off) out8<SYS>(sout + db, 0);
+      if (lane < 16 && db < dir_end) out8<SYS>(sout + db, 0);
     }
     if (a.flags != nullptr) {
       publish_chunk(&a.chunk_cnt[2 * chunk + 1], g.n_blocks, &a.flags[2 * chunk + 1], a.epoch);
@@ -1038,9 +1099,9 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
 
 // Compress kernels keep two waves per SIMD (the LDS budget allows eight
 // workgroups per CU); the fused reduce holds many more per-input states.
-template <int DT, bool SMALL, bool SYS>
+template <int DT, bool SMALL, bool SYS, bool SHARED = false>
 __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) encode_kernel(EncodeArgs a) {
-  encode_body<DT, false, SMALL, SYS>(a);
+  encode_body<DT, false, SMALL, SYS, SHARED>(a);
 }
 template <int DT>
 __global__ void __launch_bounds__(64) reduce_kernel(EncodeArgs a) {
@@ -1191,7 +1252,7 @@ __device__ inline void load_raw_full(const uint8_t *plane, uint64_t first, uint3
   }
 }
 
-template <int DT>
+template <int DT, bool SHARED = false>
 __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
   constexpr int E = (DT == 2) ? 4 : 2;
   constexpr int NW = 4 * (E / 2);
@@ -1208,11 +1269,25 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
   const uint32_t be = ld32(s + 8);
   const uint32_t nb = ld32(s + 12);
   const uint64_t total = ld64(s + 24);
-  bool ok = ld32(s) == kMagic && s[4] == kVersion && s[5] == DT && s[6] == kProbBits && s[7] == 0 &&
+  // flags byte: the table mode (0: a table per block; 1: a stream-wide
+  // table after the directory; 2: the caller's stream-wide table)
+  const uint32_t mode = s[7];
+  bool ok = ld32(s) == kMagic && s[4] == kVersion && s[5] == DT && s[6] == kProbBits &&
+            (SHARED ? ((mode == 1) || (mode == 2 && a.table != nullptr)) : mode == 0) &&
             ld64(s + 16) == a.n && be > 0 && (be & (be - 1)) == 0 && (uint64_t)be * E >= kMinBlockBytes &&
             (uint64_t)be * E <= kMaxBlockBytes && (uint64_t)nb == (a.n + be - 1) / be && total <= a.in_bytes;
   Geom g = make_geom(a.n, ok ? be : 1, E);
+  const uint64_t table_off = g.raw_off;
+  if (SHARED && mode == 1 && nb > 0) {
+    g.raw_off += kTableBytes;
+    g.coded_off += kTableBytes;
+  }
   ok = ok && total >= g.coded_off;
+  if (SHARED && ok && nb > 0) {
+    // one lookup table for every block of the stream
+    ok = build_lut_shared(mode == 1 ? (const uint16_t *)(s + table_off) : a.table, lut, cum_s, f_s);
+    __syncthreads();
+  }
   if (!ok) {
     if (blockIdx.x == 0 && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
     return;
@@ -1267,14 +1342,21 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
       continue;
     }
     uint32_t k = 0;
-    if (!build_lut(sec, len, lut, cum_s, f_s, k)) {
-      if (lane == 0) report(a.dstatus, UZIP_ECORRUPT);
-      continue;
+    if constexpr (SHARED) {
+      if (len < kSharedSectionFixed) {
+        if (lane == 0) report(a.dstatus, UZIP_ECORRUPT);
+        continue;
+      }
+    } else {
+      if (!build_lut(sec, len, lut, cum_s, f_s, k)) {
+        if (lane == 0) report(a.dstatus, UZIP_ECORRUPT);
+        continue;
+      }
+      k = uniform(k);
     }
-    k = uniform(k);
     uint32_t x = ((const uint32_t *)sec)[lane];
     const uint32_t x0 = x;  // checked at the end of the block: no wait for it here
-    const uint32_t wb = kSectionFixed + 2 * k;  // section offset of word 0
+    const uint32_t wb = SHARED ? kSharedSectionFixed : kSectionFixed + 2 * k;  // section offset of word 0
     const uint32_t w_avail = (len - wb) / 2;
     RingD rg;
     rg.len = len;
@@ -1607,13 +1689,67 @@ __global__ void clear_kernel(uint32_t *p, uint64_t words) {
 }
 
 // n == 0: the stream is the 32-byte header alone
-__global__ void empty_stream_kernel(uint8_t *out, uint32_t dt, uint32_t block_elems, uint64_t *size_out) {
+__global__ void empty_stream_kernel(uint8_t *out, uint32_t dt, uint32_t block_elems, uint64_t *size_out,
+                                    uint32_t mode = 0) {
   if (threadIdx.x == 0) {
     uint4 *hp = (uint4 *)out;
-    hp[0] = make_uint4(kMagic, kVersion | (dt << 8) | (kProbBits << 16), block_elems, 0);
+    hp[0] = make_uint4(kMagic, kVersion | (dt << 8) | (kProbBits << 16) | (mode << 24), block_elems, 0);
     hp[1] = make_uint4(0, 0, kHeaderBytes, 0);
     if (size_out != nullptr) *size_out = kHeaderBytes;
   }
+}
+
+// ---------------------------------------------------------------------------
+// table_kernel: the stream-wide table of a tensor (section 3.3.1's table from
+// a sample of the range): histogram of the symbols of its first
+// min(n, 256 KiB / E) elements, then f[s] = 1 + floor(c[s](M - 256)/n_s) for
+// all 256 symbols, the remainder to the most frequent (ties: the smallest).
+// One workgroup of 16 waves, a sub-histogram per wave; written to dst0 and,
+// if given, dst1 (the table's place in the stream).
+// ---------------------------------------------------------------------------
+constexpr uint32_t kTableThreads = 1024;
+template <int DT>
+__global__ void __launch_bounds__(kTableThreads) table_kernel(const uint8_t *in, uint64_t n, uint16_t *dst0,
+                                                             uint16_t *dst1) {
+  constexpr int E = dt_bytes<DT>();
+  constexpr int NW = 4 * (E / 2);
+  constexpr uint32_t kWaves = kTableThreads / 64;
+  __shared__ uint32_t h[kWaves * kHistStride];
+  for (uint32_t i = threadIdx.x; i < kWaves * kHistStride; i += kTableThreads) h[i] = 0;
+  __syncthreads();
+  const uint64_t n_s = n < kSampleBytes / E ? n : kSampleBytes / E;
+  uint32_t *hw = h + (threadIdx.x / 64) * kHistStride;
+  for (uint64_t i0 = (uint64_t)kPerLane * threadIdx.x; i0 < n_s; i0 += (uint64_t)kPerLane * kTableThreads) {
+    const uint32_t valid = (uint32_t)(n_s - i0 < kPerLane ? n_s - i0 : kPerLane);
+    uint32_t w[NW];
+    load_words<E>(in, i0, valid, w);
+    Group gr;
+    split_group<DT>(w, gr);
+    hist_add8(hw, gr, valid);
+  }
+  __syncthreads();
+  if (threadIdx.x >= 64) return;
+  const uint32_t lane = threadIdx.x;
+  uint32_t c[4], f[4], lt = 0, key = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    uint32_t acc = 0;
+    for (uint32_t wv = 0; wv < kWaves; ++wv) acc += h[wv * kHistStride + 4 * lane + q];
+    c[q] = acc;
+    // c (M - 256) < 2^17 * 2^11: the quotient is exact in 32 bits
+    f[q] = n_s ? 1u + (c[q] * (kM - 256u)) / (uint32_t)n_s : kM / 256u;
+    lt += f[q];
+    const uint32_t kq = (c[q] << 8) | (255u - (4 * lane + q));
+    key = kq > key ? kq : key;
+  }
+  const uint32_t d = kM - wave_sum(lt);
+  const uint32_t best = 255u - (wave_max(key) & 0xFFu);
+#pragma unroll
+  for (uint32_t q = 0; q < 4; ++q)
+    if (best == 4 * lane + q) f[q] += d;
+  const uint2 v = make_uint2(f[0] | (f[1] << 16), f[2] | (f[3] << 16));
+  *(uint2 *)(dst0 + 4 * lane) = v;
+  if (dst1 != nullptr) *(uint2 *)(dst1 + 4 * lane) = v;
 }
 
 // ---------------------------------------------------------------------------
@@ -1634,6 +1770,17 @@ const void *encode_kernel_ptr(int k) {
       (const void *)encode_kernel<3, false, true>,  (const void *)encode_kernel<3, true, true>,
       (const void *)encode_kernel<4, false, false>, (const void *)encode_kernel<4, true, false>,
       (const void *)encode_kernel<4, false, true>,  (const void *)encode_kernel<4, true, true>};
+  return tab[k];
+}
+// encoders with a stream-wide table: index = dt * 2 + small blocks
+constexpr int kSharedKernels = 10;
+const void *shared_kernel_ptr(int k) {
+  static const void *const tab[kSharedKernels] = {
+      (const void *)encode_kernel<0, false, false, true>, (const void *)encode_kernel<0, true, false, true>,
+      (const void *)encode_kernel<1, false, false, true>, (const void *)encode_kernel<1, true, false, true>,
+      (const void *)encode_kernel<2, false, false, true>, (const void *)encode_kernel<2, true, false, true>,
+      (const void *)encode_kernel<3, false, false, true>, (const void *)encode_kernel<3, true, false, true>,
+      (const void *)encode_kernel<4, false, false, true>, (const void *)encode_kernel<4, true, false, true>};
   return tab[k];
 }
 const void *reduce_kernel_ptr(int dt) {
@@ -1664,6 +1811,8 @@ uzip_status device_info(DeviceInfo &out) {
     const int lds_max = 160 * 1024;
     for (int k = 0; k < kEncodeKernels; ++k)
       (void)hipFuncSetAttribute(encode_kernel_ptr(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
+    for (int k = 0; k < kSharedKernels; ++k)
+      (void)hipFuncSetAttribute(shared_kernel_ptr(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
     for (int k = 0; k < 3; ++k)
       (void)hipFuncSetAttribute(reduce_kernel_ptr(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
     (void)hipFuncSetAttribute((const void *)reduce_decode_kernel<0>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
@@ -1745,8 +1894,19 @@ ReduceWs reduce_ws(uint64_t n_blocks, uint32_t block_elems, uint64_t n, uint32_t
   return w;
 }
 
+uzip_status launch_table(const void *d_in, uint64_t n, uzip_dtype dt, uint16_t *dst0, uint16_t *dst1,
+                         hipStream_t stream) {
+  static const void *const tab[5] = {(const void *)table_kernel<0>, (const void *)table_kernel<1>,
+                                     (const void *)table_kernel<2>, (const void *)table_kernel<3>,
+                                     (const void *)table_kernel<4>};
+  const uint8_t *in = (const uint8_t *)d_in;
+  void *args[] = {&in, &n, &dst0, &dst1};
+  if (hipLaunchKernel(tab[(int)dt], dim3(1), dim3(kTableThreads), args, 0, stream) != hipSuccess) return UZIP_EHIP;
+  return UZIP_OK;
+}
+
 uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws, const EncodeWs &w,
-                          const DeviceInfo &info, hipStream_t stream) {
+                          const DeviceInfo &info, hipStream_t stream, bool shared = false) {
   const bool small = !reduce && small_path(a.block_elems);
   a.ticket = (uint32_t *)ws;
   a.status = (uint64_t *)(ws + w.status_off);
@@ -1759,7 +1919,8 @@ uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws
   const uint32_t lds = encode_lds(a.block_elems, small);
   if (lds > 160 * 1024) return UZIP_EINVAL;
   const void *fn = reduce ? reduce_kernel_ptr((int)dt)
-                          : encode_kernel_ptr((int)dt * 4 + (a.flags != nullptr ? 2 : 0) + (small ? 1 : 0));
+                   : shared ? shared_kernel_ptr((int)dt * 2 + (small ? 1 : 0))
+                            : encode_kernel_ptr((int)dt * 4 + (a.flags != nullptr ? 2 : 0) + (small ? 1 : 0));
   int occ = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, 64, lds) != hipSuccess || occ < 1) occ = 1;
   uint64_t grid = (uint64_t)info.cus * (uint64_t)occ;
@@ -1793,6 +1954,8 @@ size_t uzip_workspace_size(int op, uzip_dtype dtype, uint64_t n_elems, uint32_t 
       return (size_t)encode_ws(nb, 1, be, 0).total;
     case UZIP_OP_DECOMPRESS:
       return kDecodeWsBytes;
+    case UZIP_OP_COMPRESS_TABLE:
+      return (size_t)encode_ws(nb, 1, be, 0).total + kTableBytes;
     case UZIP_OP_CHUNKED: {
       if (aux == 0 || aux % block_bytes) return 0;
       const uint64_t ce = aux / E;
@@ -1882,9 +2045,14 @@ uzip_status uzip_compress_chunked(const void *d_in, uint64_t n_elems, uzip_dtype
   return launch_encode(a, dtype, false, (uint8_t *)d_ws, w, info, stream);
 }
 
-uzip_status uzip_decompress(const void *d_in, size_t in_bytes, uzip_dtype dtype, uint64_t n_elems, void *d_out,
-                            size_t out_cap, uint32_t *d_status, void *d_ws, size_t ws_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+uzip_status launch_decode(const void *d_in, size_t in_bytes, uzip_dtype dtype, uint64_t n_elems, void *d_out,
+                          size_t out_cap, uint32_t *d_status, void *d_ws, size_t ws_bytes, hipStream_t stream,
+                          bool shared, const uint16_t *d_table) {
   if (!valid_dtype(dtype) || d_in == nullptr || !aligned16(d_in)) return UZIP_EINVAL;
+  if (d_table != nullptr && !aligned16(d_table)) return UZIP_EINVAL;
   if (n_elems > 0 && (d_out == nullptr || !aligned16(d_out))) return UZIP_EINVAL;
   if (out_cap < n_elems * elem_bytes(dtype)) return UZIP_ENOSPC;
   if (d_ws == nullptr || !aligned16(d_ws) || ws_bytes < kDecodeWsBytes) return UZIP_EINVAL;
@@ -1892,6 +2060,7 @@ uzip_status uzip_decompress(const void *d_in, size_t in_bytes, uzip_dtype dtype,
   uzip_status st = device_info(info);
   if (st != UZIP_OK) return st;
   DecodeArgs a;
+  memset(&a, 0, sizeof(a));
   a.in = (const uint8_t *)d_in;
   a.in_bytes = in_bytes;
   a.n = n_elems;
@@ -1899,12 +2068,15 @@ uzip_status uzip_decompress(const void *d_in, size_t in_bytes, uzip_dtype dtype,
   a.out = (uint8_t *)d_out;
   a.dstatus = d_status;
   a.ticket = (uint32_t *)d_ws;
+  a.table = d_table;
   // resident waves take blocks by ticket until none are left
   const uint64_t most = (n_elems + (kMinBlockBytes / elem_bytes(dtype)) - 1) / (kMinBlockBytes / elem_bytes(dtype));
-  static const void *const dec_tab[5] = {(const void *)decode_kernel<0>, (const void *)decode_kernel<1>,
-                                         (const void *)decode_kernel<2>, (const void *)decode_kernel<3>,
-                                         (const void *)decode_kernel<4>};
-  const void *fn = dec_tab[(int)dtype];
+  static const void *const dec_tab[10] = {
+      (const void *)decode_kernel<0>,       (const void *)decode_kernel<1>,       (const void *)decode_kernel<2>,
+      (const void *)decode_kernel<3>,       (const void *)decode_kernel<4>,       (const void *)decode_kernel<0, true>,
+      (const void *)decode_kernel<1, true>, (const void *)decode_kernel<2, true>, (const void *)decode_kernel<3, true>,
+      (const void *)decode_kernel<4, true>};
+  const void *fn = dec_tab[(int)dtype + (shared ? 5 : 0)];
   int occ = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, 64, 0) != hipSuccess || occ < 1) occ = 1;
   uint64_t grid = (uint64_t)info.cus * (uint64_t)occ;
@@ -1915,6 +2087,83 @@ uzip_status uzip_decompress(const void *d_in, size_t in_bytes, uzip_dtype dtype,
   void *args[] = {&a};
   if (hipLaunchKernel(fn, dim3((unsigned)grid), dim3(64), args, 0, stream) != hipSuccess) return UZIP_EHIP;
   return UZIP_OK;
+}
+}  // namespace
+
+extern "C" {
+
+uzip_status uzip_decompress(const void *d_in, size_t in_bytes, uzip_dtype dtype, uint64_t n_elems, void *d_out,
+                            size_t out_cap, uint32_t *d_status, void *d_ws, size_t ws_bytes, hipStream_t stream) {
+  return launch_decode(d_in, in_bytes, dtype, n_elems, d_out, out_cap, d_status, d_ws, ws_bytes, stream, false,
+                       nullptr);
+}
+
+uzip_status uzip_decompress_table(const void *d_in, size_t in_bytes, uzip_dtype dtype, uint64_t n_elems,
+                                  const uint16_t *d_table, void *d_out, size_t out_cap, uint32_t *d_status,
+                                  void *d_ws, size_t ws_bytes, hipStream_t stream) {
+  return launch_decode(d_in, in_bytes, dtype, n_elems, d_out, out_cap, d_status, d_ws, ws_bytes, stream, true,
+                       d_table);
+}
+
+uzip_status uzip_build_table(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint16_t *d_table,
+                             hipStream_t stream) {
+  if (!valid_dtype(dtype) || d_table == nullptr || !aligned16(d_table)) return UZIP_EINVAL;
+  if (n_elems > 0 && (d_in == nullptr || !aligned16(d_in))) return UZIP_EINVAL;
+  DeviceInfo info;
+  uzip_status st = device_info(info);
+  if (st != UZIP_OK) return st;
+  return launch_table(d_in, n_elems, dtype, d_table, nullptr, stream);
+}
+
+uzip_status uzip_compress_table(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint32_t block_bytes,
+                                uzip_table_mode mode, const uint16_t *d_table, void *d_out, size_t out_cap,
+                                uint64_t *d_out_size, void *d_ws, size_t ws_bytes, hipStream_t stream) {
+  if (mode == UZIP_TABLE_PER_BLOCK)
+    return uzip_compress(d_in, n_elems, dtype, block_bytes, d_out, out_cap, d_out_size, d_ws, ws_bytes, stream);
+  if (mode != UZIP_TABLE_SAMPLED && mode != UZIP_TABLE_EXTERNAL) return UZIP_EINVAL;
+  if (!valid_dtype(dtype) || !valid_block(block_bytes)) return UZIP_EINVAL;
+  if (d_out == nullptr || !aligned16(d_out) || (n_elems > 0 && (d_in == nullptr || !aligned16(d_in))))
+    return UZIP_EINVAL;
+  if (mode == UZIP_TABLE_EXTERNAL && (d_table == nullptr || !aligned16(d_table))) return UZIP_EINVAL;
+  const uint32_t E = elem_bytes(dtype), be = block_bytes / E;
+  const uint64_t nb = (n_elems + be - 1) / be;
+  if (nb >= 0x7FFFFFFFull) return UZIP_EINVAL;
+  const uint32_t tb = (mode == UZIP_TABLE_SAMPLED && nb > 0) ? kTableBytes : 0;
+  if (out_cap < max_size(E, n_elems, be) + tb) return UZIP_ENOSPC;
+  DeviceInfo info;
+  uzip_status st = device_info(info);
+  if (st != UZIP_OK) return st;
+  if (n_elems == 0) {
+    hipLaunchKernelGGL(empty_stream_kernel, dim3(1), dim3(64), 0, stream, (uint8_t *)d_out, (uint32_t)dtype, be,
+                       d_out_size, (uint32_t)mode);
+    return hipGetLastError() == hipSuccess ? UZIP_OK : UZIP_EHIP;
+  }
+  EncodeWs w = encode_ws(nb, 1, be, 0);
+  if (d_ws == nullptr || !aligned16(d_ws) || ws_bytes < w.total + kTableBytes) return UZIP_ENOSPC;
+  uint8_t *ws = (uint8_t *)d_ws;
+  const uint16_t *table = d_table;
+  if (mode == UZIP_TABLE_SAMPLED) {
+    // the table, into the workspace and its place in the stream
+    uint16_t *t = (uint16_t *)(ws + w.total);
+    st = launch_table(d_in, n_elems, dtype, t, (uint16_t *)((uint8_t *)d_out + kHeaderBytes + pad16(4 * nb)), stream);
+    if (st != UZIP_OK) return st;
+    table = t;
+  }
+  EncodeArgs a;
+  memset(&a, 0, sizeof(a));
+  a.in = (const uint8_t *)d_in;
+  a.n = n_elems;
+  a.chunk_elems = (nb * be);
+  a.block_elems = be;
+  a.blocks_per_chunk = (uint32_t)nb;
+  a.n_blocks = (uint32_t)nb;
+  a.out = (uint8_t *)d_out;
+  a.slot_bytes = 0;
+  a.sizes = d_out_size;
+  a.table = table;
+  a.table_mode = (uint32_t)mode;
+  a.table_bytes = tb;
+  return launch_encode(a, dtype, false, ws, w, info, stream, true);
 }
 
 uzip_status uzip_reduce_fused(const void *const *d_in, const size_t *in_bytes, int n_in, const void *d_local_raw,

@@ -20,6 +20,9 @@ constexpr uint32_t kPerLane = 8;            // consecutive elements per lane and
 constexpr uint32_t kRound = kLanes * kPerLane;
 constexpr uint32_t kHeaderBytes = 32;
 constexpr uint32_t kSectionFixed = 288;     // 64 states + 32-byte presence bitmap
+constexpr uint32_t kSharedSectionFixed = 256;  // 64 states (stream-wide table)
+constexpr uint32_t kTableBytes = 512;          // a stream-wide table: u16 f[256]
+constexpr uint32_t kSampleBytes = 262144;      // the sample a stream-wide table is built from
 constexpr uint32_t kMagic = 0x31505A55u;
 constexpr uint32_t kVersion = 1;
 constexpr uint32_t kStoredBit = 0x80000000u;

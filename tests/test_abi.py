@@ -101,3 +101,25 @@ def test_status_strings():
     assert uz.uzip_status_str(0) == "ok"
     assert "corrupt" in uz.uzip_status_str(uz.ECORRUPT)
     assert uz.uzip_status_str(123) == "unknown status"
+
+
+def test_table_api_host_checks():
+    import paper_2604_17172_amd as uz
+    n, bb = 1 << 20, 65536
+    base = uz.uzip_workspace_size(uz.OP_COMPRESS, uz.BF16, n, bb)
+    assert uz.uzip_workspace_size(uz.OP_COMPRESS_TABLE, uz.BF16, n, bb) == base + uz.TABLE_BYTES
+    # bad mode, missing or misaligned table, too small an output
+    assert uz.uzip_compress_table(16, 100, 0, bb, 3, None, 32, 1 << 20, None, 48, 1 << 20, None) == uz.EINVAL
+    assert uz.uzip_compress_table(16, 100, 0, bb, uz.TABLE_EXTERNAL, None, 32, 1 << 20, None, 48, 1 << 20,
+                                  None) == uz.EINVAL
+    assert uz.uzip_compress_table(16, 100, 0, bb, uz.TABLE_EXTERNAL, 24, 32, 1 << 20, None, 48, 1 << 20,
+                                  None) == uz.EINVAL
+    cap = uz.uzip_max_compressed_size(uz.BF16, 1000, bb)
+    assert uz.uzip_compress_table(16, 1000, 0, bb, uz.TABLE_SAMPLED, None, 32, cap, None, 48, 1 << 20,
+                                  None) == uz.ENOSPC
+    assert uz.uzip_compress_table(16, 1000, 7, bb, uz.TABLE_SAMPLED, None, 32, cap + 512, None, 48, 1 << 20,
+                                  None) == uz.EINVAL
+    assert uz.uzip_build_table(16, 100, 0, 24, None) == uz.EINVAL
+    assert uz.uzip_build_table(16, 100, 9, 32, None) == uz.EINVAL
+    assert uz.uzip_decompress_table(16, 100, 0, 10, 24, 32, 100, None, 48, 256, None) == uz.EINVAL
+    assert uz.uzip_decompress_table(16, 100, 0, 10, None, 32, 100, None, None, 0, None) == uz.EINVAL

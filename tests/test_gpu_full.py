@@ -118,6 +118,23 @@ def test_fp8_pairs_1GiB_whole_stream(uz, fmt):
     check_whole(uz, W.normal_fp8_pairs(1 << 29, fmt), fmt, 65536, f"normal_{fmt}_pairs_1GiB")
 
 
+def test_weight_sync_1GiB_sampled_table(uz):
+    """The whole 1 GiB buffer with one table sampled from its first 256 KiB."""
+    x = W.weight_sync()
+    say(f"[full] weight_sync sampled table: n={x.size}")
+    t0 = time.time()
+    want = ref.compress_table(x, "bf16", 65536, "sampled")
+    say(f"[full] oracle {time.time() - t0:.1f}s, ratio {want.size / (2 * x.size):.4f}")
+    xt = to_dev(x, "bf16")
+    out, size = uz.compress_table(xt, 65536, "sampled", dtype="bf16")
+    torch.cuda.synchronize()
+    got = out[:int(size.item())].cpu().numpy()
+    assert got.size == want.size and np.array_equal(got, want), f"first diff at {first_diff(got, want)}"
+    y, st = uz.decompress_table(out, "bf16", x.size)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0 and torch.equal(y, xt)
+
+
 def test_reduce_8x16MiB(uz):
     xs = W.reduce_slices()
     n = xs[0].size

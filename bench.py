@@ -239,6 +239,28 @@ def main() -> int:
                                        "decompress_frac": round(moved / (fd * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)}
             log(f"[bench] table {mode}: ratio {tsize / nbytes:.4f} compress {fc:.3f} ms decompress {fd:.3f} ms")
         del tws, tout, ty
+        # split-send producer with a table per 4 MiB chunk (sampled from the chunk's first 256 KiB)
+        cws2 = torch.empty(uz.uzip_workspace_size(uz.OP_CHUNKED_TABLE, uz.BF16, n, bb, cb), dtype=torch.uint8,
+                           device=dev)
+        slot2 = (uz.uzip_max_compressed_size(uz.BF16, cb // 2, bb) + uz.TABLE_BYTES + 255) // 256 * 256
+        cout2 = torch.empty(slot2 * chunks, dtype=torch.uint8, device=dev)
+        times = []
+        for r in range(reps + 1):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            _, _, sizes2, _ = uz.compress_chunked_table(x, bb, cb, "sampled", dtype="bf16", epoch=r + 1, flags=flags,
+                                                        out=cout2, ws=cws2)
+            b.record(stream)
+            torch.cuda.synchronize()
+            if r > 0:
+                times.append(a.elapsed_time(b))
+        assert bool((flags == reps + 1).all())
+        c2 = int(sizes2.sum().item())
+        extras["chunked_sampled_tables"] = {"chunk_bytes": cb, "ms": round(float(np.mean(times)), 4),
+                                            "ratio": round(c2 / nbytes, 5),
+                                            "ratio_cost_vs_per_block": round(c2 / total - 1, 4)}
+        log(f"[bench] chunked, sampled table per chunk: ratio {c2 / nbytes:.4f} {np.mean(times):.3f} ms")
+        del cws2, cout2
 
         # ------------- FP8 pairs: 1 GiB of e4m3fn / e5m2 values N(0, 1) -------------
         del cout, cws, rout, rws, streams

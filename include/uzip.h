@@ -91,7 +91,8 @@ enum {
   UZIP_OP_DECOMPRESS = 1, /* also uzip_decompress_table */
   UZIP_OP_REDUCE = 2,
   UZIP_OP_CHUNKED = 3,
-  UZIP_OP_COMPRESS_TABLE = 4
+  UZIP_OP_COMPRESS_TABLE = 4,
+  UZIP_OP_CHUNKED_TABLE = 5 /* aux = chunk_bytes */
 };
 
 /* Table modes (sections 3.3.1 and 3.4).  PER_BLOCK: every block carries
@@ -169,6 +170,21 @@ uzip_status uzip_build_table(const void *d_in, uint64_t n_elems, uzip_dtype dtyp
 uzip_status uzip_compress_table(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint32_t block_bytes,
                                 uzip_table_mode mode, const uint16_t *d_table, void *d_out, size_t out_cap,
                                 uint64_t *d_out_size, void *d_ws, size_t ws_bytes, hipStream_t stream);
+
+/* The split-send producer (uzip_compress_chunked) with a table mode: with
+ * SAMPLED every chunk's stream takes its own table from the chunk's first
+ * 256 KiB (the analogue of section 3.3.1's table per CTA range) and stores
+ * it; with EXTERNAL every chunk is coded with d_table.  slot_bytes >=
+ * uzip_max_compressed_size(one chunk) + UZIP_TABLE_BYTES; workspace:
+ * uzip_workspace_size(UZIP_OP_CHUNKED_TABLE, ..., chunk_bytes).  An
+ * EXTERNAL table that is not an all-symbol table codes nothing: the chunk
+ * sizes read 0 and no flag is raised.  Otherwise as uzip_compress_chunked
+ * (PER_BLOCK is that call).  Each chunk decodes with
+ * uzip_decompress_table. */
+uzip_status uzip_compress_chunked_table(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint32_t block_bytes,
+                                        uint64_t chunk_bytes, uzip_table_mode mode, const uint16_t *d_table,
+                                        void *d_out, size_t slot_bytes, uint64_t *chunk_sizes, uint32_t *flags,
+                                        uint32_t epoch, void *d_ws, size_t ws_bytes, hipStream_t stream);
 
 /* Decompress a stream of mode SAMPLED or EXTERNAL (a PER_BLOCK stream, or
  * an EXTERNAL one without d_table, sets *d_status to UZIP_ECORRUPT; so

@@ -257,11 +257,15 @@ def reduce(streams, dtype: str, n: int, block_bytes: int, local=None):
     return out[:total], y[:n]
 
 
-def compress_chunked(x: np.ndarray, dtype: str, block_bytes: int, chunk_bytes: int):
-    """Each chunk of ``chunk_bytes`` of input is an independent stream."""
+def compress_chunked(x: np.ndarray, dtype: str, block_bytes: int, chunk_bytes: int, mode: str = "per_block",
+                     table=None):
+    """Each chunk of ``chunk_bytes`` of input is an independent stream (with
+    a table mode: a sampled table per chunk, or the given table for all)."""
     xb = _bits(x, dtype).ravel()
     ce = chunk_bytes // ELEM_BYTES[dtype]
-    return [compress(xb[c:c + ce], dtype, block_bytes) for c in range(0, xb.size, ce)]
+    if mode == "per_block":
+        return [compress(xb[c:c + ce], dtype, block_bytes) for c in range(0, xb.size, ce)]
+    return [compress_table(xb[c:c + ce], dtype, block_bytes, mode, table) for c in range(0, xb.size, ce)]
 
 
 def half_to_float(h: int) -> float:

@@ -28,7 +28,7 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 BF16, FP16, FP32, E4M3FN, E5M2 = 0, 1, 2, 3, 4
-OP_COMPRESS, OP_DECOMPRESS, OP_REDUCE, OP_CHUNKED, OP_COMPRESS_TABLE = 0, 1, 2, 3, 4
+OP_COMPRESS, OP_DECOMPRESS, OP_REDUCE, OP_CHUNKED, OP_COMPRESS_TABLE, OP_CHUNKED_TABLE = 0, 1, 2, 3, 4, 5
 TABLE_PER_BLOCK, TABLE_SAMPLED, TABLE_EXTERNAL = 0, 1, 2
 TABLE_BYTES = 512
 WS_NO_OUT_RAW = 1 << 16
@@ -54,6 +54,9 @@ _lib.uzip_build_table.argtypes = [_vp, _u64, _int, _vp, _vp]
 _lib.uzip_build_table.restype = _int
 _lib.uzip_compress_table.argtypes = [_vp, _u64, _int, _u32, _int, _vp, _vp, _sz, _vp, _vp, _sz, _vp]
 _lib.uzip_compress_table.restype = _int
+_lib.uzip_compress_chunked_table.argtypes = [_vp, _u64, _int, _u32, _u64, _int, _vp, _vp, _sz, _vp, _vp, _u32, _vp,
+                                             _sz, _vp]
+_lib.uzip_compress_chunked_table.restype = _int
 _lib.uzip_decompress_table.argtypes = [_vp, _sz, _int, _u64, _vp, _vp, _sz, _vp, _vp, _sz, _vp]
 _lib.uzip_decompress_table.restype = _int
 _lib.uzip_status_str.argtypes = [_int]
@@ -61,7 +64,7 @@ _lib.uzip_status_str.restype = _c.c_char_p
 
 EXPORTED = ["uzip_max_compressed_size", "uzip_workspace_size", "uzip_compress", "uzip_decompress",
             "uzip_reduce_fused", "uzip_compress_chunked", "uzip_status_str", "uzip_build_table",
-            "uzip_compress_table", "uzip_decompress_table"]
+            "uzip_compress_table", "uzip_decompress_table", "uzip_compress_chunked_table"]
 
 
 class UzipError(RuntimeError):
@@ -109,6 +112,12 @@ def uzip_compress_table(d_in, n_elems, dtype, block_bytes, mode, d_table, d_out,
                         ws_bytes, stream) -> int:
     return _lib.uzip_compress_table(d_in, n_elems, dtype, block_bytes, mode, d_table, d_out, out_cap, d_out_size,
                                     d_ws, ws_bytes, stream)
+
+
+def uzip_compress_chunked_table(d_in, n_elems, dtype, block_bytes, chunk_bytes, mode, d_table, d_out, slot_bytes,
+                                chunk_sizes, flags, epoch, d_ws, ws_bytes, stream) -> int:
+    return _lib.uzip_compress_chunked_table(d_in, n_elems, dtype, block_bytes, chunk_bytes, mode, d_table, d_out,
+                                            slot_bytes, chunk_sizes, flags, epoch, d_ws, ws_bytes, stream)
 
 
 def uzip_decompress_table(d_in, in_bytes, dtype, n_elems, d_table, d_out, out_cap, d_status, d_ws, ws_bytes,
@@ -309,3 +318,31 @@ def decompress_table(s: torch.Tensor, dtype, n_elems: int, table: torch.Tensor |
                                  out.data_ptr() if n_elems else None, n_elems * _ELEM[dt], status.data_ptr(),
                                  ws.data_ptr(), ws.numel(), _stream(stream)), "uzip_decompress_table")
     return out, status
+
+
+def compress_chunked_table(x: torch.Tensor, block_bytes: int, chunk_bytes: int, mode="sampled",
+                           table: torch.Tensor | None = None, dtype=None, epoch: int = 1,
+                           flags: torch.Tensor | None = None, out: torch.Tensor | None = None,
+                           ws: torch.Tensor | None = None, stream=None):
+    """Split-send producer with a table mode.  Returns (buffer of n_chunks
+    slots, slot_bytes, device u64 chunk sizes, flags)."""
+    assert x.is_cuda and x.is_contiguous()
+    dt = dtype_code(dtype if dtype is not None else x.dtype)
+    md = _MODE[mode] if isinstance(mode, str) else mode
+    n = _n_elems(x, dt)
+    ce = chunk_bytes // _ELEM[dt]
+    chunks = (n + ce - 1) // ce
+    slot = uzip_max_compressed_size(dt, min(n, ce), block_bytes) + TABLE_BYTES
+    slot = (slot + 255) // 256 * 256
+    if out is None:
+        out = _dev_empty(slot * max(chunks, 1), x.device)
+    if ws is None:
+        ws = _dev_empty(uzip_workspace_size(OP_CHUNKED_TABLE, dt, n, block_bytes, chunk_bytes), x.device)
+    sizes = torch.zeros(max(chunks, 1), dtype=torch.int64, device=x.device)
+    if flags is None:
+        flags = torch.zeros(2 * max(chunks, 1), dtype=torch.int32, device=x.device)
+    _check(uzip_compress_chunked_table(x.data_ptr() if n else None, n, dt, block_bytes, chunk_bytes, md,
+                                       table.data_ptr() if table is not None else None, out.data_ptr(), slot,
+                                       sizes.data_ptr(), flags.data_ptr(), epoch, ws.data_ptr(), ws.numel(),
+                                       _stream(stream)), "uzip_compress_chunked_table")
+    return out, slot, sizes, flags

@@ -76,6 +76,7 @@ struct EncodeArgs {
   // stream-wide table (table modes 1, 2): frequencies f[256], the mode
   // written to the header's flags byte, and the table bytes in the stream
   const uint16_t *table;
+  uint32_t table_stride;  // u16 entries between the tables of consecutive streams (0: one table for all)
   uint32_t table_mode;
   uint32_t table_bytes;
 };
@@ -685,25 +686,9 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   typedef __attribute__((address_space(3))) uint16_t lds16_t;
   // one private 4-byte slot per lane for words that are not emitted
   lds16_t *trash = (lds16_t *)smem_base + 2 * lane;
-  // a stream-wide table codes every block: its encoder entries once
-  if constexpr (SHARED) {
-    Table ts;
-    const uint2 v = *(const uint2 *)(a.table + 4 * lane);
-    ts.f[0] = v.x & 0xFFFFu;
-    ts.f[1] = v.x >> 16;
-    ts.f[2] = v.y & 0xFFFFu;
-    ts.f[3] = v.y >> 16;
-    ts.k = 256;
-    // a table that is not an all-symbol table (some f = 0, or a sum other
-    // than M) codes nothing: the stream size reads 0
-    const bool bad = ts.f[0] == 0 || ts.f[1] == 0 || ts.f[2] == 0 || ts.f[3] == 0;
-    if (__any(bad) || wave_sum(ts.f[0] + ts.f[1] + ts.f[2] + ts.f[3]) != kM) {
-      if (blockIdx.x == 0 && lane == 0 && a.sizes != nullptr) a.sizes[0] = 0;
-      return;
-    }
-    enc_entries(ts, enc);
-    __syncthreads();
-  }
+  // a stream-wide table codes every block of its stream: the wave derives
+  // its encoder entries when it moves to a block of another stream
+  uint32_t table_chunk = ~0u;
 
   while (true) {
     uint32_t b = 0;
@@ -714,6 +699,27 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     const uint32_t chunk = b / a.blocks_per_chunk;
     const uint32_t lb = b - chunk * a.blocks_per_chunk;
     const uint32_t first_block = b - lb;
+    if constexpr (SHARED) {
+      if (chunk != table_chunk && (a.table_stride != 0 || table_chunk == ~0u)) {
+        Table ts;
+        const uint2 v = *(const uint2 *)(a.table + (uint64_t)chunk * a.table_stride + 4 * lane);
+        ts.f[0] = v.x & 0xFFFFu;
+        ts.f[1] = v.x >> 16;
+        ts.f[2] = v.y & 0xFFFFu;
+        ts.f[3] = v.y >> 16;
+        // a table that is not an all-symbol table (some f = 0, or a sum
+        // other than M) codes nothing: the stream sizes read 0
+        const bool bad = ts.f[0] == 0 || ts.f[1] == 0 || ts.f[2] == 0 || ts.f[3] == 0;
+        if (__any(bad) || wave_sum(ts.f[0] + ts.f[1] + ts.f[2] + ts.f[3]) != kM) {
+          if (lane == 0 && a.sizes != nullptr) a.sizes[chunk] = 0;
+          return;
+        }
+        __syncthreads();  // the previous block's coding pass is done with the entries
+        enc_entries(ts, enc);
+        __syncthreads();
+      }
+      table_chunk = chunk;
+    }
     const uint64_t chunk_first = (uint64_t)chunk * a.chunk_elems;
     const uint64_t chunk_n = (a.n - chunk_first) < a.chunk_elems ? (a.n - chunk_first) : a.chunk_elems;
     Geom g = make_geom(chunk_n, a.block_elems, E);
@@ -783,6 +789,12 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
               load_round<E>(src_blk + (uint64_t)rn * kRound * E, buf[rr % D]);
               Group gr;
               split_group<DT>(w, gr);
+              // the compiler would otherwise carry the split words (four;
+              // eight for fp32) to the coding pass instead of the two symbol
+              // words and spill, when no histogram update takes the symbols
+              // here or fp32's wider words crowd the registers: make the
+              // symbols now
+              if constexpr (SHARED || DT == 2) asm volatile("" : "+v"(gr.sym[0]), "+v"(gr.sym[1]));
               S.v3[2 * rr] = gr.sym[0];
               S.v3[2 * rr + 1] = gr.sym[1];
               if (r < full) {
@@ -1704,17 +1716,27 @@ __global__ void empty_stream_kernel(uint8_t *out, uint32_t dt, uint32_t block_el
 // a sample of the range): histogram of the symbols of its first
 // min(n, 256 KiB / E) elements, then f[s] = 1 + floor(c[s](M - 256)/n_s) for
 // all 256 symbols, the remainder to the most frequent (ties: the smallest).
-// One workgroup of 16 waves, a sub-histogram per wave; written to dst0 and,
-// if given, dst1 (the table's place in the stream).
+// One workgroup of 16 waves per stream (workgroup c: the stream of
+// elements [c chunk_elems, ...)), a sub-histogram per wave; written to
+// dst0 + 256 c and, if `out` is given, to the table's place in stream c
+// (out + c slot_bytes, after its directory).
 // ---------------------------------------------------------------------------
 constexpr uint32_t kTableThreads = 1024;
 template <int DT>
-__global__ void __launch_bounds__(kTableThreads) table_kernel(const uint8_t *in, uint64_t n, uint16_t *dst0,
-                                                             uint16_t *dst1) {
+__global__ void __launch_bounds__(kTableThreads) table_kernel(const uint8_t *in_all, uint64_t n_all,
+                                                             uint64_t chunk_elems, uint32_t block_elems,
+                                                             uint16_t *dst0_all, uint8_t *out, uint64_t slot_bytes) {
   constexpr int E = dt_bytes<DT>();
   constexpr int NW = 4 * (E / 2);
   constexpr uint32_t kWaves = kTableThreads / 64;
   __shared__ uint32_t h[kWaves * kHistStride];
+  const uint64_t first = (uint64_t)blockIdx.x * chunk_elems;
+  const uint8_t *in = in_all + first * E;
+  const uint64_t n = n_all - first < chunk_elems ? n_all - first : chunk_elems;
+  uint16_t *dst0 = dst0_all + 256ull * blockIdx.x;
+  uint16_t *dst1 = out == nullptr ? nullptr
+                                  : (uint16_t *)(out + blockIdx.x * slot_bytes + kHeaderBytes +
+                                                 pad16(4 * ((n + block_elems - 1) / block_elems)));
   for (uint32_t i = threadIdx.x; i < kWaves * kHistStride; i += kTableThreads) h[i] = 0;
   __syncthreads();
   const uint64_t n_s = n < kSampleBytes / E ? n : kSampleBytes / E;
@@ -1772,15 +1794,20 @@ const void *encode_kernel_ptr(int k) {
       (const void *)encode_kernel<4, false, true>,  (const void *)encode_kernel<4, true, true>};
   return tab[k];
 }
-// encoders with a stream-wide table: index = dt * 2 + small blocks
-constexpr int kSharedKernels = 10;
+// encoders with stream-wide tables: index = dt * 4 + kind (as above)
+constexpr int kSharedKernels = 20;
 const void *shared_kernel_ptr(int k) {
   static const void *const tab[kSharedKernels] = {
       (const void *)encode_kernel<0, false, false, true>, (const void *)encode_kernel<0, true, false, true>,
+      (const void *)encode_kernel<0, false, true, true>,  (const void *)encode_kernel<0, true, true, true>,
       (const void *)encode_kernel<1, false, false, true>, (const void *)encode_kernel<1, true, false, true>,
+      (const void *)encode_kernel<1, false, true, true>,  (const void *)encode_kernel<1, true, true, true>,
       (const void *)encode_kernel<2, false, false, true>, (const void *)encode_kernel<2, true, false, true>,
+      (const void *)encode_kernel<2, false, true, true>,  (const void *)encode_kernel<2, true, true, true>,
       (const void *)encode_kernel<3, false, false, true>, (const void *)encode_kernel<3, true, false, true>,
-      (const void *)encode_kernel<4, false, false, true>, (const void *)encode_kernel<4, true, false, true>};
+      (const void *)encode_kernel<3, false, true, true>,  (const void *)encode_kernel<3, true, true, true>,
+      (const void *)encode_kernel<4, false, false, true>, (const void *)encode_kernel<4, true, false, true>,
+      (const void *)encode_kernel<4, false, true, true>,  (const void *)encode_kernel<4, true, true, true>};
   return tab[k];
 }
 const void *reduce_kernel_ptr(int dt) {
@@ -1894,14 +1921,15 @@ ReduceWs reduce_ws(uint64_t n_blocks, uint32_t block_elems, uint64_t n, uint32_t
   return w;
 }
 
-uzip_status launch_table(const void *d_in, uint64_t n, uzip_dtype dt, uint16_t *dst0, uint16_t *dst1,
-                         hipStream_t stream) {
+uzip_status launch_table(const void *d_in, uint64_t n, uzip_dtype dt, uint64_t chunk_elems, uint32_t block_elems,
+                         uint64_t chunks, uint16_t *dst0, uint8_t *out, uint64_t slot_bytes, hipStream_t stream) {
   static const void *const tab[5] = {(const void *)table_kernel<0>, (const void *)table_kernel<1>,
                                      (const void *)table_kernel<2>, (const void *)table_kernel<3>,
                                      (const void *)table_kernel<4>};
   const uint8_t *in = (const uint8_t *)d_in;
-  void *args[] = {&in, &n, &dst0, &dst1};
-  if (hipLaunchKernel(tab[(int)dt], dim3(1), dim3(kTableThreads), args, 0, stream) != hipSuccess) return UZIP_EHIP;
+  void *args[] = {&in, &n, &chunk_elems, &block_elems, &dst0, &out, &slot_bytes};
+  if (hipLaunchKernel(tab[(int)dt], dim3((unsigned)chunks), dim3(kTableThreads), args, 0, stream) != hipSuccess)
+    return UZIP_EHIP;
   return UZIP_OK;
 }
 
@@ -1919,7 +1947,7 @@ uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws
   const uint32_t lds = encode_lds(a.block_elems, small);
   if (lds > 160 * 1024) return UZIP_EINVAL;
   const void *fn = reduce ? reduce_kernel_ptr((int)dt)
-                   : shared ? shared_kernel_ptr((int)dt * 2 + (small ? 1 : 0))
+                   : shared ? shared_kernel_ptr((int)dt * 4 + (a.flags != nullptr ? 2 : 0) + (small ? 1 : 0))
                             : encode_kernel_ptr((int)dt * 4 + (a.flags != nullptr ? 2 : 0) + (small ? 1 : 0));
   int occ = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, 64, lds) != hipSuccess || occ < 1) occ = 1;
@@ -1956,6 +1984,12 @@ size_t uzip_workspace_size(int op, uzip_dtype dtype, uint64_t n_elems, uint32_t 
       return kDecodeWsBytes;
     case UZIP_OP_COMPRESS_TABLE:
       return (size_t)encode_ws(nb, 1, be, 0).total + kTableBytes;
+    case UZIP_OP_CHUNKED_TABLE: {
+      if (aux == 0 || aux % block_bytes) return 0;
+      const uint64_t ce = aux / E;
+      const uint64_t chunks = (n_elems + ce - 1) / ce;
+      return (size_t)(encode_ws(chunks * (ce / be), chunks, be, 0).total + chunks * kTableBytes);
+    }
     case UZIP_OP_CHUNKED: {
       if (aux == 0 || aux % block_bytes) return 0;
       const uint64_t ce = aux / E;
@@ -2011,7 +2045,17 @@ uzip_status uzip_compress_chunked(const void *d_in, uint64_t n_elems, uzip_dtype
                                   uint64_t chunk_bytes, void *d_out, size_t slot_bytes, uint64_t *chunk_sizes,
                                   uint32_t *flags, uint32_t epoch, void *d_ws, size_t ws_bytes,
                                   hipStream_t stream) {
+  return uzip_compress_chunked_table(d_in, n_elems, dtype, block_bytes, chunk_bytes, UZIP_TABLE_PER_BLOCK, nullptr,
+                                     d_out, slot_bytes, chunk_sizes, flags, epoch, d_ws, ws_bytes, stream);
+}
+
+uzip_status uzip_compress_chunked_table(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint32_t block_bytes,
+                                        uint64_t chunk_bytes, uzip_table_mode mode, const uint16_t *d_table,
+                                        void *d_out, size_t slot_bytes, uint64_t *chunk_sizes, uint32_t *flags,
+                                        uint32_t epoch, void *d_ws, size_t ws_bytes, hipStream_t stream) {
   if (!valid_dtype(dtype) || !valid_block(block_bytes)) return UZIP_EINVAL;
+  if (mode != UZIP_TABLE_PER_BLOCK && mode != UZIP_TABLE_SAMPLED && mode != UZIP_TABLE_EXTERNAL) return UZIP_EINVAL;
+  if (mode == UZIP_TABLE_EXTERNAL && (d_table == nullptr || !aligned16(d_table))) return UZIP_EINVAL;
   if (chunk_bytes == 0 || chunk_bytes % block_bytes) return UZIP_EINVAL;
   if (d_out == nullptr || !aligned16(d_out) || (slot_bytes & 15u) || (n_elems > 0 && (d_in == nullptr || !aligned16(d_in))))
     return UZIP_EINVAL;
@@ -2021,16 +2065,31 @@ uzip_status uzip_compress_chunked(const void *d_in, uint64_t n_elems, uzip_dtype
   if (ce / be >= 0x7FFFFFFFull) return UZIP_EINVAL;
   const uint64_t chunks = (n_elems + ce - 1) / ce;
   if (n_elems == 0) return UZIP_OK;
-  if (slot_bytes < max_size(E, n_elems < ce ? n_elems : ce, be)) return UZIP_ENOSPC;
+  const uint32_t tb = mode == UZIP_TABLE_SAMPLED ? kTableBytes : 0;  // every chunk has a block
+  if (slot_bytes < max_size(E, n_elems < ce ? n_elems : ce, be) + tb) return UZIP_ENOSPC;
   const uint64_t nb = (chunks - 1) * (ce / be) + ((n_elems - (chunks - 1) * ce) + be - 1) / be;
   if (nb >= 0x7FFFFFFFull) return UZIP_EINVAL;
   DeviceInfo info;
   uzip_status st = device_info(info);
   if (st != UZIP_OK) return st;
   EncodeWs w = encode_ws(chunks * (ce / be), chunks, be, 0);
-  if (d_ws == nullptr || !aligned16(d_ws) || ws_bytes < w.total) return UZIP_ENOSPC;
+  const uint64_t ws_need = w.total + (mode == UZIP_TABLE_SAMPLED ? chunks * kTableBytes : 0);
+  if (d_ws == nullptr || !aligned16(d_ws) || ws_bytes < ws_need) return UZIP_ENOSPC;
+  const uint16_t *table = d_table;
+  if (mode == UZIP_TABLE_SAMPLED) {
+    // each chunk's table from its own first 256 KiB, into the workspace
+    // and its place in the chunk's stream
+    uint16_t *t = (uint16_t *)((uint8_t *)d_ws + w.total);
+    st = launch_table(d_in, n_elems, dtype, ce, be, chunks, t, (uint8_t *)d_out, slot_bytes, stream);
+    if (st != UZIP_OK) return st;
+    table = t;
+  }
   EncodeArgs a;
   memset(&a, 0, sizeof(a));
+  a.table = table;
+  a.table_stride = mode == UZIP_TABLE_SAMPLED ? 256 : 0;
+  a.table_mode = (uint32_t)mode;
+  a.table_bytes = tb;
   a.in = (const uint8_t *)d_in;
   a.n = n_elems;
   a.chunk_elems = ce;
@@ -2042,7 +2101,7 @@ uzip_status uzip_compress_chunked(const void *d_in, uint64_t n_elems, uzip_dtype
   a.sizes = chunk_sizes;
   a.flags = flags;
   a.epoch = epoch;
-  return launch_encode(a, dtype, false, (uint8_t *)d_ws, w, info, stream);
+  return launch_encode(a, dtype, false, (uint8_t *)d_ws, w, info, stream, mode != UZIP_TABLE_PER_BLOCK);
 }
 
 }  // extern "C"
@@ -2112,7 +2171,8 @@ uzip_status uzip_build_table(const void *d_in, uint64_t n_elems, uzip_dtype dtyp
   DeviceInfo info;
   uzip_status st = device_info(info);
   if (st != UZIP_OK) return st;
-  return launch_table(d_in, n_elems, dtype, d_table, nullptr, stream);
+  const uint32_t be = kMinBlockBytes / elem_bytes(dtype);  // no stream: only the sample matters
+  return launch_table(d_in, n_elems, dtype, n_elems ? n_elems : 1, be, 1, d_table, nullptr, 0, stream);
 }
 
 uzip_status uzip_compress_table(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint32_t block_bytes,
@@ -2145,7 +2205,7 @@ uzip_status uzip_compress_table(const void *d_in, uint64_t n_elems, uzip_dtype d
   if (mode == UZIP_TABLE_SAMPLED) {
     // the table, into the workspace and its place in the stream
     uint16_t *t = (uint16_t *)(ws + w.total);
-    st = launch_table(d_in, n_elems, dtype, t, (uint16_t *)((uint8_t *)d_out + kHeaderBytes + pad16(4 * nb)), stream);
+    st = launch_table(d_in, n_elems, dtype, n_elems, be, 1, t, (uint8_t *)d_out, 0, stream);
     if (st != UZIP_OK) return st;
     table = t;
   }

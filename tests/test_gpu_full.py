@@ -135,6 +135,33 @@ def test_weight_sync_1GiB_sampled_table(uz):
     assert int(st.item()) == 0 and torch.equal(y, xt)
 
 
+def test_weight_sync_1GiB_chunked_sampled_tables(uz):
+    """Split-send producer, 4 MiB chunks, each with the table sampled from
+    its own first 256 KiB."""
+    x = W.weight_sync()
+    cb, bb = 4 << 20, 65536
+    say(f"[full] weight_sync chunked sampled tables: n={x.size}")
+    xt = to_dev(x, "bf16")
+    flags = torch.zeros(2 * ((x.size * 2 + cb - 1) // cb), dtype=torch.int32).pin_memory()
+    out, slot, sizes, _ = uz.compress_chunked_table(xt, bb, cb, "sampled", dtype="bf16", epoch=5, flags=flags)
+    torch.cuda.synchronize()
+    assert bool((flags == 5).all())
+    buf = out.cpu().numpy()
+    sz = sizes.cpu().numpy()
+    ce = cb // 2
+    t0 = time.time()
+    for c in range(sz.size):
+        w = ref.compress_table(x[c * ce:(c + 1) * ce], "bf16", bb, "sampled")
+        assert sz[c] == w.size and np.array_equal(buf[c * slot:c * slot + w.size], w), f"chunk {c}"
+    say(f"[full] {sz.size} chunks equal to the oracle ({time.time() - t0:.1f}s), ratio {sz.sum() / (2 * x.size):.4f}")
+    y = torch.empty_like(xt)
+    for c in range(sz.size):
+        yc, st = uz.decompress_table(out[c * slot:(c + 1) * slot], "bf16", ce, out=y[c * ce:(c + 1) * ce])
+        assert int(st.item()) == 0
+    torch.cuda.synchronize()
+    assert torch.equal(y, xt)
+
+
 def test_reduce_8x16MiB(uz):
     xs = W.reduce_slices()
     n = xs[0].size

@@ -156,3 +156,46 @@ def test_empty_tensor(uz):
         y, st = uz.decompress_table(out, "bf16", 0, t)
         torch.cuda.synchronize()
         assert int(st.item()) == 0 and y.numel() == 0
+
+
+def check_chunked(uz, x, dtype, bb, cb, mode, label, table=None):
+    say(f"[tables] {label}: chunked dtype={dtype} n={x.size} block={bb} chunk={cb} mode={mode}")
+    t_dev = dev(table.astype(np.uint16).view(np.int16)) if table is not None else None
+    xt = dev(x.view(NP_BITS[dtype]))
+    out, slot, sizes, flags = uz.compress_chunked_table(xt, bb, cb, mode, t_dev, dtype=dtype, epoch=9)
+    torch.cuda.synchronize()
+    assert bool((flags == 9).all())
+    buf = out.cpu().numpy()
+    sz = sizes.cpu().numpy()
+    ce = cb // EB[dtype]
+    for c, w in enumerate(ref.compress_chunked(x, dtype, bb, cb, mode, table)):
+        assert sz[c] == w.size, f"{label}: chunk {c} size {sz[c]} != {w.size}"
+        assert np.array_equal(buf[c * slot:c * slot + w.size], w), f"{label}: chunk {c} differs"
+        y, st = uz.decompress_table(out[c * slot:(c + 1) * slot], dtype, min(ce, x.size - c * ce), t_dev)
+        torch.cuda.synchronize()
+        assert int(st.item()) == 0 and np.array_equal(host_bits(y, dtype), x[c * ce:(c + 1) * ce]), label
+
+
+def test_chunked_sampled_table_per_chunk(uz):
+    """Each chunk samples its own first 256 KiB: across the boundary between
+    the N(0, 1) embedding and the N(0, 0.02) layers of the weight buffer."""
+    x = np.ascontiguousarray(W.weight_sync(136_134_656 + 3_000_000)[-6_000_000:])
+    check_chunked(uz, x, "bf16", 65536, 1 << 20, "sampled", "boundary")
+    check_chunked(uz, W.grad_fp32(3 * (1 << 18) + 5, seed=2), "fp32", 262144, 1 << 20, "sampled", "fp32")
+    check_chunked(uz, W.normal_fp8_pairs(700_001, "e4m3fn", seed=3), "e4m3fn", 4096, 16384, "sampled", "fp8 small")
+
+
+def test_chunked_external_table(uz):
+    x = W.normal_bf16(5 * (1 << 19) + 17, seed=4)
+    check_chunked(uz, x, "bf16", 65536, 1 << 20, "external", "external", ref.sampled_table(x, "bf16"))
+
+
+def test_chunked_invalid_external_table(uz):
+    say("[tables] chunked invalid table")
+    x = W.normal_bf16(3 * (1 << 19), seed=5)
+    bad = ref.sampled_table(x, "bf16").astype(np.uint16)
+    bad[0] += 1
+    out, slot, sizes, flags = uz.compress_chunked_table(dev(x.view(np.int16)), 65536, 1 << 20, "external",
+                                                        dev(bad.view(np.int16)), dtype="bf16", epoch=4)
+    torch.cuda.synchronize()
+    assert int(sizes.sum().item()) == 0 and not bool((flags == 4).any())

@@ -382,7 +382,8 @@ __device__ void build_enc_table(const uint32_t *hist, uint32_t n_b, uint4 *enc, 
   uint32_t lt = 0;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    t.f[q] = c[q] ? 1u + (uint32_t)(((uint64_t)c[q] * (kM - k)) / n_b) : 0u;
+    // c (M - k) < 2^17 * 2^11: the quotient is exact in 32 bits
+    t.f[q] = c[q] ? 1u + (c[q] * (kM - k)) / n_b : 0u;
     lt += t.f[q];
   }
   uint32_t d = kM - wave_sum(lt);
@@ -1396,12 +1397,37 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
     // header, so that the loop below is always entered with the same loads
     // in flight and waits only for what it uses
     load_raw_full<E>(full > 0 ? rawp : s, full > 0 ? kPerLane * lane : 0, rawA);
+    // round 1's (clamped to a full round) likewise
+    load_raw_full<E>(full > 0 ? rawp : s, full > 1 ? (kRound + kPerLane * lane) : (full > 0 ? kPerLane * lane : 0),
+                     rawB);
     // one more memory operation in flight, standing in for the store that
-    // ends every round, so that both ways into the loop match
+    // ends every round, so that both ways into the loops match
     const uint32_t pad_load = *(const uint32_t *)(s + 4 * lane);
     uint32_t r = 0;
+    // full rounds, four per iteration with four raw buffers: each round's
+    // raw bytes are loaded two rounds before their use
+    uint32_t rawC[6] = {0, 0, 0, 0, 0, 0}, rawD[6] = {0, 0, 0, 0, 0, 0};
+    auto clampr = [&](uint32_t q) { return q < full ? q : full - 1; };
+    for (; r + 4 <= full; r += 4) {
+      uint32_t e[kPerLane], w[NW];
+#define UZIP_DEC_ROUND(RAWUSE, RAWLOAD, DR, AHEAD)                                              \
+  ringd_half<0>(rg, ring, sec, wb + 2 * p);                                                     \
+  load_raw_full<E>(rawp, clampr(r + (AHEAD)) * kRound + kPerLane * lane, RAWLOAD);              \
+  _Pragma("unroll") for (uint32_t t = 0; t < kPerLane; ++t) {                                   \
+    if (t == kPerLane / 2) ringd_half<1>(rg, ring, sec, wb + 2 * p);                            \
+    e[t] = decode_step_ring<true, kDecRingBytes, false>(x, true, lut, ring, rb, p);             \
+  }                                                                                             \
+  merge_entries<DT>(e, RAWUSE, w);                                                              \
+  store_words<E, true>(outp, (r + (DR)) * kRound + kPerLane * lane, 8, w);
+      UZIP_DEC_ROUND(rawA, rawC, 0, 2)
+      UZIP_DEC_ROUND(rawB, rawD, 1, 3)
+      UZIP_DEC_ROUND(rawC, rawA, 2, 4)
+      UZIP_DEC_ROUND(rawD, rawB, 3, 5)
+#undef UZIP_DEC_ROUND
+    }
     // full rounds, two per iteration with ping-pong raw registers: every
     // load is issued a round before its use and no register is copied
+    // the rest in twos (rawA, rawB hold rounds r, r + 1 here)
     for (; r + 2 <= full; r += 2) {
       ringd_half<0>(rg, ring, sec, wb + 2 * p);
       load_raw_full<E>(rawp, (r + 1) * kRound + kPerLane * lane, rawB);

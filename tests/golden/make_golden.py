@@ -17,19 +17,23 @@ sys.path.insert(0, os.path.dirname(os.path.dirname(HERE)))
 from oracle import ref  # noqa: E402
 import workloads as W  # noqa: E402
 
+# (name, input, dtype, block bytes, table mode)
 CASES = [
-    ("normal_bf16_5000_b4096", lambda: W.normal_bf16(5000, seed=7), "bf16", 4096),
-    ("grad_fp32_3000_b4096", lambda: W.grad_fp32(3000, seed=7), "fp32", 4096),
-    ("grad_fp16_6000_b4096", lambda: W.grad_fp16(6000, seed=7), "fp16", 4096),
+    ("normal_bf16_5000_b4096", lambda: W.normal_bf16(5000, seed=7), "bf16", 4096, "per_block"),
+    ("grad_fp32_3000_b4096", lambda: W.grad_fp32(3000, seed=7), "fp32", 4096, "per_block"),
+    ("grad_fp16_6000_b4096", lambda: W.grad_fp16(6000, seed=7), "fp16", 4096, "per_block"),
+    ("normal_e4m3fn_6000_b4096", lambda: W.normal_fp8_pairs(6000, "e4m3fn", seed=7), "e4m3fn", 4096, "per_block"),
+    ("normal_e5m2_6000_b4096", lambda: W.normal_fp8_pairs(6000, "e5m2", seed=7), "e5m2", 4096, "per_block"),
+    ("normal_bf16_5000_b4096_sampled", lambda: W.normal_bf16(5000, seed=7), "bf16", 4096, "sampled"),
 ]
 
 
 def main():
     out = {}
-    for name, gen, dtype, bb in CASES:
+    for name, gen, dtype, bb, mode in CASES:
         x = gen()
-        s = ref.compress(x, dtype, bb)
-        out[name] = dict(dtype=dtype, block_bytes=bb, n=int(x.size),
+        s = ref.compress_table(x, dtype, bb, mode)
+        out[name] = dict(dtype=dtype, block_bytes=bb, n=int(x.size), table_mode=mode,
                          input_sha256=hashlib.sha256(x.tobytes()).hexdigest(),
                          stream_bytes=int(s.size),
                          stream_sha256=hashlib.sha256(s.tobytes()).hexdigest())

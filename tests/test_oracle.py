@@ -599,12 +599,17 @@ def test_golden_streams_stable():
     meta = json.load(open(os.path.join(here, "streams.json")))
     gens = {"normal_bf16_5000_b4096": lambda: W.normal_bf16(5000, seed=7),
             "grad_fp32_3000_b4096": lambda: W.grad_fp32(3000, seed=7),
-            "grad_fp16_6000_b4096": lambda: W.grad_fp16(6000, seed=7)}
+            "grad_fp16_6000_b4096": lambda: W.grad_fp16(6000, seed=7),
+            "normal_e4m3fn_6000_b4096": lambda: W.normal_fp8_pairs(6000, "e4m3fn", seed=7),
+            "normal_e5m2_6000_b4096": lambda: W.normal_fp8_pairs(6000, "e5m2", seed=7),
+            "normal_bf16_5000_b4096_sampled": lambda: W.normal_bf16(5000, seed=7)}
+    assert set(meta) == set(gens)
     for name, m in meta.items():
         x = gens[name]()
         assert hashlib.sha256(x.tobytes()).hexdigest() == m["input_sha256"]
         hexs = "".join(open(os.path.join(here, name + ".hex")).read().split())
         stored = np.frombuffer(bytes.fromhex(hexs), np.uint8)
         assert stored.size == m["stream_bytes"]
-        assert np.array_equal(ref.compress(x, m["dtype"], m["block_bytes"]), stored)
-        assert np.array_equal(ref.decompress(stored, m["dtype"], m["n"]), x)
+        mode = m.get("table_mode", "per_block")
+        assert np.array_equal(ref.compress_table(x, m["dtype"], m["block_bytes"], mode), stored)
+        assert np.array_equal(ref.decompress_table(stored, m["dtype"], m["n"]), x)

@@ -1742,20 +1742,21 @@ __global__ void empty_stream_kernel(uint8_t *out, uint32_t dt, uint32_t block_el
 // a sample of the range): histogram of the symbols of its first
 // min(n, 256 KiB / E) elements, then f[s] = 1 + floor(c[s](M - 256)/n_s) for
 // all 256 symbols, the remainder to the most frequent (ties: the smallest).
-// One workgroup of 16 waves per stream (workgroup c: the stream of
-// elements [c chunk_elems, ...)), a sub-histogram per wave; written to
+// One workgroup of 4 waves per stream (workgroup c: the stream of elements
+// [c chunk_elems, ...)), 8 sub-histograms per wave (lane & 7: skewed
+// exponents would otherwise serialise the LDS atomics); written to
 // dst0 + 256 c and, if `out` is given, to the table's place in stream c
 // (out + c slot_bytes, after its directory).
 // ---------------------------------------------------------------------------
-constexpr uint32_t kTableThreads = 1024;
+constexpr uint32_t kTableThreads = 256;
+constexpr uint32_t kTableReplicas = (kTableThreads / 64) * kHistReplicas;
 template <int DT>
 __global__ void __launch_bounds__(kTableThreads) table_kernel(const uint8_t *in_all, uint64_t n_all,
                                                              uint64_t chunk_elems, uint32_t block_elems,
                                                              uint16_t *dst0_all, uint8_t *out, uint64_t slot_bytes) {
   constexpr int E = dt_bytes<DT>();
   constexpr int NW = 4 * (E / 2);
-  constexpr uint32_t kWaves = kTableThreads / 64;
-  __shared__ uint32_t h[kWaves * kHistStride];
+  __shared__ uint32_t h[kTableReplicas * kHistStride];
   const uint64_t first = (uint64_t)blockIdx.x * chunk_elems;
   const uint8_t *in = in_all + first * E;
   const uint64_t n = n_all - first < chunk_elems ? n_all - first : chunk_elems;
@@ -1763,17 +1764,29 @@ __global__ void __launch_bounds__(kTableThreads) table_kernel(const uint8_t *in_
   uint16_t *dst1 = out == nullptr ? nullptr
                                   : (uint16_t *)(out + blockIdx.x * slot_bytes + kHeaderBytes +
                                                  pad16(4 * ((n + block_elems - 1) / block_elems)));
-  for (uint32_t i = threadIdx.x; i < kWaves * kHistStride; i += kTableThreads) h[i] = 0;
+  for (uint32_t i = threadIdx.x; i < kTableReplicas * kHistStride; i += kTableThreads) h[i] = 0;
   __syncthreads();
   const uint64_t n_s = n < kSampleBytes / E ? n : kSampleBytes / E;
-  uint32_t *hw = h + (threadIdx.x / 64) * kHistStride;
-  for (uint64_t i0 = (uint64_t)kPerLane * threadIdx.x; i0 < n_s; i0 += (uint64_t)kPerLane * kTableThreads) {
-    const uint32_t valid = (uint32_t)(n_s - i0 < kPerLane ? n_s - i0 : kPerLane);
-    uint32_t w[NW];
-    load_words<E>(in, i0, valid, w);
-    Group gr;
-    split_group<DT>(w, gr);
-    hist_add8(hw, gr, valid);
+  uint32_t *hw = h + ((threadIdx.x / 64) * kHistReplicas + (threadIdx.x & (kHistReplicas - 1))) * kHistStride;
+  // the sample in batches of 16 groups of 8 elements per thread, every
+  // load of a batch issued before its first use
+  constexpr uint32_t kBatch = 16;
+  constexpr uint32_t kBatches = kSampleBytes / E / (kPerLane * kTableThreads * kBatch);
+  for (uint32_t bt = 0; bt < kBatches; ++bt) {
+    uint32_t w[kBatch][NW];
+    uint32_t valid[kBatch];
+#pragma unroll
+    for (uint32_t it = 0; it < kBatch; ++it) {
+      const uint64_t i0 = (uint64_t)kPerLane * (threadIdx.x + (bt * kBatch + it) * kTableThreads);
+      valid[it] = i0 < n_s ? (uint32_t)(n_s - i0 < kPerLane ? n_s - i0 : kPerLane) : 0u;
+      load_words<E>(in, i0, valid[it], w[it]);
+    }
+#pragma unroll
+    for (uint32_t it = 0; it < kBatch; ++it) {
+      Group gr;
+      split_group<DT>(w[it], gr);
+      hist_add8(hw, gr, valid[it]);
+    }
   }
   __syncthreads();
   if (threadIdx.x >= 64) return;
@@ -1782,7 +1795,7 @@ __global__ void __launch_bounds__(kTableThreads) table_kernel(const uint8_t *in_
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     uint32_t acc = 0;
-    for (uint32_t wv = 0; wv < kWaves; ++wv) acc += h[wv * kHistStride + 4 * lane + q];
+    for (uint32_t rp = 0; rp < kTableReplicas; ++rp) acc += h[rp * kHistStride + 4 * lane + q];
     c[q] = acc;
     // c (M - 256) < 2^17 * 2^11: the quotient is exact in 32 bits
     f[q] = n_s ? 1u + (c[q] * (kM - 256u)) / (uint32_t)n_s : kM / 256u;

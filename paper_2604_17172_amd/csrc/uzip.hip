@@ -367,6 +367,7 @@ struct Table {
 // the smallest), cum in ascending symbol order.  Writes the encoder table
 // {reciprocal, f << 20, (M - f) | shift << 24, cum (+2047 if f == 1)}.
 __device__ void enc_entries(const Table &t, uint4 *enc);
+template <bool PACKED = false>
 __device__ void build_enc_table(const uint32_t *hist, uint32_t n_b, uint4 *enc, Table &t) {
   const uint32_t lane = lane_id();
   uint32_t c[4];
@@ -374,9 +375,15 @@ __device__ void build_enc_table(const uint32_t *hist, uint32_t n_b, uint4 *enc, 
   for (int q = 0; q < 4; ++q) {
     uint32_t s = 4 * lane + q, acc = 0;
 #pragma unroll
-    for (uint32_t rep = 0; rep < kHistReplicas; ++rep) acc += hist[rep * kHistStride + s];
+    for (uint32_t rep = 0; rep < kHistReplicas; ++rep) {
+      if constexpr (PACKED)
+        acc += (hist[rep * kPackedHistStride + (s & 127u)] >> (16 * (s >> 7))) & 0xFFFFu;
+      else
+        acc += hist[rep * kHistStride + s];
+    }
     c[q] = acc;
   }
+  // the counts are read: a packed histogram may share its LDS with `enc`
   uint32_t pres = (c[0] > 0) + (c[1] > 0) + (c[2] > 0) + (c[3] > 0);
   uint32_t k = wave_sum(pres);
   uint32_t lt = 0;
@@ -434,45 +441,78 @@ __device__ void enc_entries(const Table &t, uint4 *enc) {
   }
 }
 
-// Decoupled look-back over the blocks of one stream: returns the exclusive
-// prefix (16-byte units) of block b, whose stream's first block is `first`.
-// Every block publishes its status, and blocks are taken in ticket order, so
+// Decoupled look-back over the blocks of one stream, in two steps: a block
+// publishes its section length (its aggregate; for the stream's first block
+// already its inclusive prefix), and later resolves its exclusive prefix
+// (16-byte units) from its predecessors' states.  Between the two a wave may
+// do other work: a wait is only ever for an aggregate, which every taken
+// block publishes without waiting, and blocks are taken in ticket order, so
 // the wait always ends; the spin is bounded anyway, and a wait that runs out
 // raises the workspace error word instead of hanging.
 constexpr uint32_t kSpinLimit = 1u << 22;
-__device__ uint64_t lookback(uint64_t *status, uint32_t b, uint32_t first, uint64_t len16, uint32_t *err) {
+__device__ __forceinline__ void publish_aggregate(uint64_t *status, uint32_t b, uint32_t first, uint64_t len16) {
+  if (lane_id() == 0)
+    __hip_atomic_store(&status[b], (b == first ? kFlagInclusive : kFlagAggregate) | len16, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ inline uint64_t wave_excl_scan64(uint64_t v) {
   const uint32_t lane = lane_id();
-  if (b == first) {
-    if (lane == 0) __hip_atomic_store(&status[b], kFlagInclusive | len16, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return 0;
+  uint64_t inc = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t w = __shfl_up(inc, o);
+    if (lane >= (uint32_t)o) inc += w;
   }
-  if (lane == 0) __hip_atomic_store(&status[b], kFlagAggregate | len16, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  uint64_t excl = 0;
+  return inc - v;
+}
+
+// Resolves block b's exclusive prefix and publishes its inclusive one.  The
+// nearest predecessors (up to 64) that had only published their length get
+// their inclusive prefix too, the same value their own look-back publishes:
+// later blocks then find an inclusive prefix close by.
+__device__ uint64_t resolve_prefix(uint64_t *status, uint32_t b, uint32_t first, uint64_t len16, uint32_t *err) {
+  const uint32_t lane = lane_id();
+  if (b == first) return 0;
+  uint64_t excl = 0, near_v = 0;
+  bool near_agg = false, near = true;
   int64_t look = (int64_t)b - 1;
   uint32_t spins = 0;
   while (true) {
-    int64_t idx = look - (int64_t)lane;
+    const int64_t idx = look - (int64_t)lane;
     uint64_t st = kFlagInclusive;  // before the stream's first block: inclusive 0
     if (idx >= (int64_t)first) st = __hip_atomic_load(&status[idx], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    uint32_t flag = (uint32_t)(st >> 62);
-    uint64_t inc = __ballot(flag == 2);
-    uint64_t upto = inc ? ((inc & (~inc + 1)) << 1) - 1 : ~0ull;  // lanes up to the first inclusive
-    uint64_t notready = __ballot(flag == 0) & upto;
+    const uint32_t flag = (uint32_t)(st >> 62);
+    const uint64_t inc = __ballot(flag == 2);
+    const uint64_t upto = inc ? ((inc & (~inc + 1)) << 1) - 1 : ~0ull;  // lanes up to the first inclusive
+    const uint64_t notready = __ballot(flag == 0) & upto;
     if (notready) {
       if (++spins < kSpinLimit) {
         __builtin_amdgcn_s_sleep(2);
         continue;
       }
       if (lane == 0) __hip_atomic_store(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      break;
+      return excl;
     }
-    uint64_t v = ((upto >> lane) & 1) ? (st & kValueMask) : 0;
+    const bool mine = (upto >> lane) & 1;
+    const uint64_t v = mine ? (st & kValueMask) : 0;
+    if (near) {
+      near_v = v;
+      near_agg = mine && flag == 1;
+      near = false;
+    }
     excl += wave_sum64(v);
     if (inc) break;
     look -= 64;
   }
   if (lane == 0)
     __hip_atomic_store(&status[b], kFlagInclusive | (excl + len16), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // lane l of the nearest window is block b-1-l: its inclusive prefix is
+  // excl less the lengths of blocks b-l .. b-1
+  const uint64_t later = wave_excl_scan64(near_v);
+  if (near_agg)
+    __hip_atomic_store(&status[b - 1 - lane], kFlagInclusive | (excl - later), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
   return excl;
 }
 
@@ -663,6 +703,152 @@ __device__ __forceinline__ void hist_add8(uint32_t *h, const Group &g, uint32_t 
     if (q < valid) atomicAdd(&h[sym_at(g.sym, q)], 1u);
 }
 
+// Packed 16-bit counts (a block holds at most 32768 symbols): symbols s and
+// s + 128 share word s & 127, low and high half.
+__device__ __forceinline__ void hist_add8_packed(uint32_t *h, const Group &g, uint32_t valid) {
+#pragma unroll
+  for (uint32_t q = 0; q < 8; ++q) {
+    const uint32_t sy = sym_at(g.sym, q);
+    if (q < valid) atomicAdd(&h[sy & 127u], 1u << ((sy >> 3) & 16u));
+  }
+}
+
+// 16 image bytes from LDS: unit u of the image at byte offset sh of s32
+__device__ __forceinline__ uint4 lds_unit(const uint32_t *s32, uint32_t u, uint32_t sh) {
+  const uint32_t *q = s32 + 4 * u;
+  uint4 o;
+  o.x = __builtin_amdgcn_alignbyte(q[1], q[0], sh);
+  o.y = __builtin_amdgcn_alignbyte(q[2], q[1], sh);
+  o.z = __builtin_amdgcn_alignbyte(q[3], q[2], sh);
+  o.w = __builtin_amdgcn_alignbyte(q[4], q[3], sh);
+  return o;
+}
+
+// bytes [0, m) of a and [m, 16) of b (m even, 0 < m < 16)
+__device__ __forceinline__ uint4 splice_bytes(uint4 a, uint4 b, uint32_t m) {
+  const uint32_t x[4] = {a.x, a.y, a.z, a.w}, y[4] = {b.x, b.y, b.z, b.w};
+  uint32_t w[4];
+#pragma unroll
+  for (uint32_t j = 0; j < 4; ++j)
+    w[j] = (4 * j + 4 <= m) ? x[j] : (4 * j >= m) ? y[j] : ((x[j] & 0xFFFFu) | (y[j] & 0xFFFF0000u));
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// What the copy-out of a coded block needs once its offset is known, all
+// wave-uniform.  Small blocks keep it across the next block's first pass:
+// the offset is resolved only then, when the predecessors have long
+// published their lengths.
+struct Fin {
+  uint8_t *sout;       // the block's stream
+  const uint8_t *src;  // the stream's input (a STORED block re-reads its symbols)
+  uint64_t coded_off;  // stream offset of the coded sections
+  uint64_t dir_end;    // end of the directory (a stored table follows)
+  uint64_t chunk_n;    // elements of the stream
+  uint64_t blk0;       // first element of the block, stream-relative
+  uint64_t sec_len;    // section bytes, a multiple of 16
+  uint32_t img;        // section image bytes (header + words) of a coded block
+  uint32_t b, chunk, lb, first_block, n_blocks, n_b, rounds;
+  uint32_t A;          // staging-area byte offset of the image
+  uint32_t lds_bytes;  // image bytes in LDS; the rest is in the overflow slot
+  uint32_t slot_delta; // slot byte = image byte + slot_delta (mod 2^32)
+  bool stored, spilled, last;
+};
+
+// Resolve the block's offset, write its directory entry and section, and for
+// a stream's last block the stream header.
+template <int DT, bool SYS>
+__device__ __forceinline__ void finish_block(const EncodeArgs &a, const Fin &f, const uint8_t *stage,
+                                             const uint16_t *ovf) {
+  constexpr int E = (DT == 2) ? 4 : 2;
+  constexpr int NW = 4 * (E / 2);
+  const uint32_t lane = lane_id();
+  const uint64_t excl = resolve_prefix(a.status, f.b, f.first_block, f.sec_len / 16, a.ticket + 1);
+  uint8_t *sec = f.sout + f.coded_off + 16 * excl;
+  if (lane == 0)
+    out32<SYS>((uint32_t *)(f.sout + kHeaderBytes + 4 * f.lb),
+               (f.stored ? kStoredBit : 0u) | (uint32_t)(excl + f.sec_len / 16));
+
+  if (!f.stored) {
+    const uint32_t *s32 = (const uint32_t *)(stage + (f.A & ~3u));
+    const uint32_t sh = f.A & 3u;
+    if (!f.spilled) {
+      // the whole image is contiguous in LDS
+      for (uint32_t u = lane; u < f.sec_len / 16; u += 64) out128<SYS>(sec + 16 * u, lds_unit(s32, u, sh));
+    } else {
+      // image bytes [0, lds_bytes) are in LDS, bytes [lds_bytes, img) in
+      // the workgroup's overflow slot
+      const uint32_t lb = f.lds_bytes, imgb = f.img, d = f.slot_delta;
+      const uint8_t *ovb = (const uint8_t *)ovf;
+      for (uint32_t u = lane; u < f.sec_len / 16; u += 64) {
+        uint4 o;
+        if (16 * u + 16 <= lb) {
+          o = lds_unit(s32, u, sh);
+        } else {
+          const uint32_t off = 16 * u + d;
+          const uint4 *p = (const uint4 *)(ovb + (off & ~15u));
+          o = funnel16(p[0], p[1], off & 15u);
+          // the unit where LDS and slot bytes meet (lb is even; the LDS
+          // reads stay within the staging area's zeroed tail)
+          if (16 * u < lb) o = splice_bytes(lds_unit(s32, u, sh), o, lb - 16 * u);
+          if (16 * u + 16 > imgb) o = keep_bytes(o, imgb - 16 * u);
+        }
+        out128<SYS>(sec + 16 * u, o);
+      }
+    }
+  } else {
+    // STORED: the block's symbol bytes, zero-padded to 16, re-read from the
+    // input (the coding pass consumed the register copy)
+    const uint32_t padded = (uint32_t)pad16(f.n_b);
+    for (uint32_t r = 0; r < f.rounds; ++r) {
+      const uint32_t i0 = r * kRound + kPerLane * lane;
+      const uint32_t valid = i0 < f.n_b ? (f.n_b - i0 < 8 ? f.n_b - i0 : 8) : 0;
+      uint32_t s0 = 0, s1 = 0;
+      if (valid > 0) {
+        uint32_t w[NW];
+        Group gr;
+        load_words<E>(f.src, f.blk0 + i0, valid, w);
+        split_group<DT>(w, gr);
+        s0 = gr.sym[0];
+        s1 = gr.sym[1];
+      }
+      if (i0 >= padded) continue;
+      if (valid < 8) {
+        const uint64_t keep = valid ? (~0ull >> (64 - 8 * valid)) : 0ull;
+        const uint64_t v = ((uint64_t)s1 << 32 | s0) & keep;
+        s0 = (uint32_t)v;
+        s1 = (uint32_t)(v >> 32);
+      }
+      out64<SYS>(sec + i0, s0, s1);
+    }
+  }
+
+  if (f.last) {
+    const uint64_t total = f.coded_off + 16 * (excl + f.sec_len / 16);
+    if (lane == 0) {
+      uint32_t hh[8];
+      hh[0] = kMagic;
+      hh[1] = kVersion | ((uint32_t)DT << 8) | (kProbBits << 16) | (a.table_mode << 24);
+      hh[2] = a.block_elems;
+      hh[3] = f.n_blocks;
+      hh[4] = (uint32_t)f.chunk_n;
+      hh[5] = (uint32_t)(f.chunk_n >> 32);
+      hh[6] = (uint32_t)total;
+      hh[7] = (uint32_t)(total >> 32);
+      uint4 *hp = (uint4 *)f.sout;
+      out128<SYS>((uint8_t *)hp, make_uint4(hh[0], hh[1], hh[2], hh[3]));
+      out128<SYS>((uint8_t *)(hp + 1), make_uint4(hh[4], hh[5], hh[6], hh[7]));
+      if (a.sizes != nullptr) {
+        if (SYS) __hip_atomic_store(&a.sizes[f.chunk], total, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        else a.sizes[f.chunk] = total;
+      }
+    }
+    // zero padding after the directory
+    const uint64_t db = kHeaderBytes + 4ull * f.n_blocks + lane;
+    if (lane < 16 && db < f.dir_end) out8<SYS>(f.sout + db, 0);
+  }
+  if (a.flags != nullptr) publish_chunk(&a.chunk_cnt[2 * f.chunk + 1], f.n_blocks, &a.flags[2 * f.chunk + 1], a.epoch);
+}
+
 // ---------------------------------------------------------------------------
 // encode_kernel: compress / split-send producer / fused reduce.
 // Persistent workgroups of one wave take blocks in ticket order.
@@ -687,6 +873,17 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   typedef __attribute__((address_space(3))) uint16_t lds16_t;
   // one private 4-byte slot per lane for words that are not emitted
   lds16_t *trash = (lds16_t *)smem_base + 2 * lane;
+  // small blocks: a block's offset is resolved and its section written
+  // after the next block's first pass, so the wait for slower predecessors
+  // overlaps streaming.  The staging area then still holds the pending
+  // block's image during the first pass: the histogram takes packed 16-bit
+  // counts in the trash slots and encoder table instead, which are free
+  // until the coding pass (the table is built from the counts in place).
+  constexpr bool DEFER = SMALL && !REDUCE;
+  static_assert(kHistReplicas * kPackedHistStride * 4 <= kTrashBytes + kEncTableBytes, "packed histogram");
+  uint32_t *phist = (uint32_t *)smem_base;
+  Fin pend;
+  bool have_pend = false;
   // a stream-wide table codes every block of its stream: the wave derives
   // its encoder entries when it moves to a block of another stream
   uint32_t table_chunk = ~0u;
@@ -713,6 +910,10 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         const bool bad = ts.f[0] == 0 || ts.f[1] == 0 || ts.f[2] == 0 || ts.f[3] == 0;
         if (__any(bad) || wave_sum(ts.f[0] + ts.f[1] + ts.f[2] + ts.f[3]) != kM) {
           if (lane == 0 && a.sizes != nullptr) a.sizes[chunk] = 0;
+          // a pending block belongs to an earlier stream with a valid table
+          if constexpr (DEFER) {
+            if (have_pend) finish_block<DT, SYS>(a, pend, stage, ovf);
+          }
           return;
         }
         __syncthreads();  // the previous block's coding pass is done with the entries
@@ -745,8 +946,19 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     // instead of the older wave winning both.
     __builtin_amdgcn_s_setprio(1);
     // ---- pass 1: split, raw plane to its final place, histogram ----
-    for (uint32_t i = lane; i < kHistReplicas * kHistStride; i += 64) hist[i] = 0;
-    __syncthreads();
+    if constexpr (!DEFER) {
+      for (uint32_t i = lane; i < kHistReplicas * kHistStride; i += 64) hist[i] = 0;
+      __syncthreads();
+    } else if constexpr (!SHARED) {
+      for (uint32_t i = lane; i < kHistReplicas * kPackedHistStride; i += 64) phist[i] = 0;
+      __syncthreads();
+      h = phist + (lane & (kHistReplicas - 1)) * kPackedHistStride;
+    }
+    // one histogram update of `valid` symbols
+    auto hist_upd = [&](const Group &gr, uint32_t valid) {
+      if constexpr (DEFER) hist_add8_packed(h, gr, valid);
+      else hist_add8(h, gr, valid);
+    };
 
     uint32_t psym0 = 0, psym1 = 0;  // symbols of a partial last round
     if constexpr (!REDUCE) {
@@ -760,7 +972,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
           load_words<E>(src, blk0 + i0, valid, w);
           split_group<DT>(w, gr);
           store_raw<E, SYS>(raw_plane, blk0 + i0, valid, gr);
-          if constexpr (!SHARED) hist_add8(h, gr, valid);
+          if constexpr (!SHARED) hist_upd(gr, valid);
         }
         psym0 = gr.sym[0];
         psym1 = gr.sym[1];
@@ -800,7 +1012,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
               S.v3[2 * rr + 1] = gr.sym[1];
               if (r < full) {
                 store_raw_round<E, SYS>(raw_blk + (uint64_t)r * kRound * (E - 1), gr);
-                if constexpr (!SHARED) hist_add8(h, gr, 8);
+                if constexpr (!SHARED) hist_upd(gr, 8);
               }
             }
             if (gi < 3) shift_down(S);
@@ -853,12 +1065,19 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     }
 
     __builtin_amdgcn_s_setprio(0);
+    if constexpr (DEFER) {
+      // the previous block's section leaves the staging area
+      if (have_pend) finish_block<DT, SYS>(a, pend, stage, ovf);
+      have_pend = false;
+      __syncthreads();
+    }
     // ---- table ----
     Table t;
     if constexpr (SHARED) {
       t.k = 256;  // only the section head differs: no bitmap, no frequencies
     } else {
-      build_enc_table(hist, n_b, enc, t);
+      if constexpr (DEFER) build_enc_table<true>(phist, n_b, enc, t);
+      else build_enc_table(hist, n_b, enc, t);
       t.k = uniform(t.k);
       __syncthreads();
     }
@@ -959,18 +1178,36 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     const uint64_t img = hdr + 2ull * n_words;
     const uint64_t sec_len = stored ? pad16(n_b) : pad16(img);
 
-    // ---- output offset: single-pass scan over the stream's blocks ----
-    const uint64_t excl = lookback(a.status, b, first_block, sec_len / 16, a.ticket + 1);
-    uint8_t *sec = sout + g.coded_off + 16 * excl;
-    if (lane == 0)
-      out32<SYS>((uint32_t *)(sout + kHeaderBytes + 4 * lb), (stored ? kStoredBit : 0u) | (uint32_t)(excl + sec_len / 16));
-
+    // ---- the section image goes to LDS, the length is published ----
+    Fin f;
+    f.sout = sout;
+    f.src = src;
+    f.coded_off = g.coded_off;
+    f.dir_end = dir_end;
+    f.chunk_n = chunk_n;
+    f.blk0 = blk0;
+    f.sec_len = sec_len;
+    f.img = (uint32_t)img;
+    f.b = b;
+    f.chunk = chunk;
+    f.lb = lb;
+    f.first_block = first_block;
+    f.n_blocks = g.n_blocks;
+    f.n_b = n_b;
+    f.rounds = rounds;
+    f.A = kStageHead + 2 * (pos - lo) - hdr;
+    f.lds_bytes = hdr + 2 * (spilled - pos);
+    f.slot_delta = 2 * spilled - f.lds_bytes;
+    f.stored = stored;
+    f.spilled = SMALL && spilled != a.wcap;
+    f.last = last_in_chunk;
     if (!stored) {
-      // header bytes: states | bitmap | f[k] (states only with a stream-wide table)
-      auto put_header = [&](uint16_t *h16) {
-        h16[2 * lane] = (uint16_t)x;
-        h16[2 * lane + 1] = (uint16_t)(x >> 16);
-        if (SHARED) return;
+      // header bytes right before the words: states | bitmap | f[k] (states
+      // only with a stream-wide table)
+      uint16_t *h16 = (uint16_t *)(stage + f.A);
+      h16[2 * lane] = (uint16_t)x;
+      h16[2 * lane + 1] = (uint16_t)(x >> 16);
+      if constexpr (!SHARED) {
         if (lane < 16) {
           uint32_t word = 0;
           for (uint32_t bit = 0; bit < 16; ++bit) {
@@ -983,130 +1220,23 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
 #pragma unroll
         for (int q = 0; q < 4; ++q)
           if (t.f[q]) h16[144 + rk++] = (uint16_t)t.f[q];
-      };
-      if (!SMALL || spilled == a.wcap) {
-        // the whole image is contiguous in LDS: header right before the words
-        const uint32_t A = kStageHead + 2 * (pos - lo) - hdr;
-        put_header((uint16_t *)(stage + A));
-        __syncthreads();
-        const uint32_t *s32 = (const uint32_t *)(stage + (A & ~3u));
-        const uint32_t sh = A & 3u;
-        for (uint32_t u = lane; u < sec_len / 16; u += 64) {
-          const uint32_t *q = s32 + 4 * u;
-          uint4 o;
-          o.x = __builtin_amdgcn_alignbyte(q[1], q[0], sh);
-          o.y = __builtin_amdgcn_alignbyte(q[2], q[1], sh);
-          o.z = __builtin_amdgcn_alignbyte(q[3], q[2], sh);
-          o.w = __builtin_amdgcn_alignbyte(q[4], q[3], sh);
-          out128<SYS>(sec + 16 * u, o);
-        }
-      } else {
-        // words [spilled, wcap) went to the overflow slot: section bytes
-        // [0, lb) are in LDS (header right before the words), bytes
-        // [lb, img) are the slot's bytes [2 spilled, 2 wcap).  The slot was
-        // written by this wave; the fence orders those stores before the
-        // reads (one wave per workgroup, one CU: no cache in between).
-        const uint32_t A = kStageHead + 2 * (pos - lo) - hdr;
-        put_header((uint16_t *)(stage + A));
-        __threadfence_block();
-        __syncthreads();
-        const uint32_t lb = hdr + 2 * (spilled - pos);
-        const uint32_t imgb = (uint32_t)img;
-        const uint32_t *s32 = (const uint32_t *)(stage + (A & ~3u));
-        const uint32_t sh = A & 3u;
-        const uint32_t d = 2 * spilled - lb;  // slot byte = section byte + d (mod 2^32)
-        const uint8_t *ovb = (const uint8_t *)ovf;
-        for (uint32_t u = lane; u < sec_len / 16; u += 64) {
-          uint4 o;
-          if (16 * u + 16 <= lb) {
-            const uint32_t *q = s32 + 4 * u;
-            o.x = __builtin_amdgcn_alignbyte(q[1], q[0], sh);
-            o.y = __builtin_amdgcn_alignbyte(q[2], q[1], sh);
-            o.z = __builtin_amdgcn_alignbyte(q[3], q[2], sh);
-            o.w = __builtin_amdgcn_alignbyte(q[4], q[3], sh);
-          } else if (16 * u >= lb) {
-            const uint32_t off = 16 * u + d;
-            const uint4 *p = (const uint4 *)(ovb + (off & ~15u));
-            o = funnel16(p[0], p[1], off & 15u);
-            if (16 * u + 16 > imgb) o = keep_bytes(o, imgb - 16 * u);
-          } else {  // the unit where LDS and slot bytes meet
-            uint32_t w[4] = {0, 0, 0, 0};
-#pragma unroll
-            for (uint32_t hw = 0; hw < 8; ++hw) {
-              const uint32_t ob = 16 * u + 2 * hw;
-              uint32_t v16 = 0;
-              if (ob < lb)
-                v16 = *(const uint16_t *)(stage + A + ob);
-              else if (ob < imgb)
-                v16 = *(const uint16_t *)(ovb + ob + d);
-              w[hw >> 1] |= v16 << (16 * (hw & 1));
-            }
-            o = make_uint4(w[0], w[1], w[2], w[3]);
-          }
-          out128<SYS>(sec + 16 * u, o);
-        }
       }
-    } else {
-      // STORED: the block's symbol bytes, zero-padded to 16
-      const uint32_t padded = (uint32_t)pad16(n_b);
-      auto put_stored = [&](uint32_t r, uint32_t s0, uint32_t s1) {
-        const uint32_t i0 = r * kRound + kPerLane * lane;
-        const uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
-        if (i0 >= padded) return;
-        if (valid < 8) {
-          uint64_t keep = valid ? (~0ull >> (64 - 8 * valid)) : 0ull;
-          uint64_t v = ((uint64_t)s1 << 32 | s0) & keep;
-          s0 = (uint32_t)v;
-          s1 = (uint32_t)(v >> 32);
-        }
-        out64<SYS>(sec + i0, s0, s1);
-      };
-      {  // the coding pass consumed the register copy of the symbols: re-read the block
-        for (uint32_t r = 0; r < rounds; ++r) {
-          const uint32_t i0 = r * kRound + kPerLane * lane;
-          const uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
-          uint32_t s0 = 0, s1 = 0;
-          if (valid > 0) {
-            uint32_t w[NW];
-            Group gr;
-            load_words<E>(src, blk0 + i0, valid, w);
-            split_group<DT>(w, gr);
-            s0 = gr.sym[0];
-            s1 = gr.sym[1];
-          }
-          put_stored(r, s0, s1);
-        }
-      }
-    }
-
-    if (last_in_chunk) {
-      const uint64_t total = g.coded_off + 16 * (excl + sec_len / 16);
-      if (lane == 0) {
-        uint32_t hh[8];
-        hh[0] = kMagic;
-        hh[1] = kVersion | ((uint32_t)DT << 8) | (kProbBits << 16) | (a.table_mode << 24);
-        hh[2] = a.block_elems;
-        hh[3] = g.n_blocks;
-        hh[4] = (uint32_t)chunk_n;
-        hh[5] = (uint32_t)(chunk_n >> 32);
-        hh[6] = (uint32_t)total;
-        hh[7] = (uint32_t)(total >> 32);
-        uint4 *hp = (uint4 *)sout;
-        out128<SYS>((uint8_t *)hp, make_uint4(hh[0], hh[1], hh[2], hh[3]));
-        out128<SYS>((uint8_t *)(hp + 1), make_uint4(hh[4], hh[5], hh[6], hh[7]));
-        if (a.sizes != nullptr) {
-          if (SYS) __hip_atomic_store(&a.sizes[chunk], total, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-          else a.sizes[chunk] = total;
-        }
-      }
-      // zero padding after the directory
-      uint64_t db = kHeaderBytes + 4ull * g.n_blocks + lane;
-      if (lane < 16 && db < dir_end) out8<SYS>(sout + db, 0);
-    }
-    if (a.flags != nullptr) {
-      publish_chunk(&a.chunk_cnt[2 * chunk + 1], g.n_blocks, &a.flags[2 * chunk + 1], a.epoch);
+      // the overflow slot was written by this wave: order its stores before
+      // the copy-out's reads (one wave per workgroup, one CU: no cache in between)
+      if (f.spilled) __threadfence_block();
     }
     __syncthreads();
+    publish_aggregate(a.status, b, first_block, sec_len / 16);
+    if constexpr (DEFER) {
+      pend = f;
+      have_pend = true;
+    } else {
+      finish_block<DT, SYS>(a, f, stage, ovf);
+    }
+    __syncthreads();
+  }
+  if constexpr (DEFER) {
+    if (have_pend) finish_block<DT, SYS>(a, pend, stage, ovf);
   }
 }
 

@@ -35,6 +35,7 @@ constexpr uint64_t kValueMask = (1ull << 62) - 1;
 // LDS layout constants
 constexpr uint32_t kHistReplicas = 8;       // sub-histograms, lane & 7
 constexpr uint32_t kHistStride = 257;       // odd stride: replicas of a bin in distinct banks
+constexpr uint32_t kPackedHistStride = 129; // packed 16-bit counts, two bins per word
 constexpr uint32_t kHistBytes = kHistReplicas * kHistStride * 4;
 constexpr uint32_t kEncTableBytes = 256 * 16;
 constexpr uint32_t kLutBytes = kM * 4;

@@ -704,13 +704,24 @@ __device__ __forceinline__ void hist_add8(uint32_t *h, const Group &g, uint32_t 
 }
 
 // Packed 16-bit counts (a block holds at most 32768 symbols): symbols s and
-// s + 128 share word s & 127, low and high half.
+// s + 128 share word s & 127, low and high half.  The bit-field extracts are
+// written out: the compiler turns them into shift-and-mask pairs.
+template <int O>
+__device__ __forceinline__ void hist_add_packed(uint32_t *h, uint32_t w, bool on) {
+  uint32_t word, high;
+  asm("v_bfe_u32 %0, %1, %2, 7" : "=v"(word) : "v"(w), "i"(O));       // symbol & 127
+  asm("v_bfe_u32 %0, %1, %2, 1" : "=v"(high) : "v"(w), "i"(O + 7));   // symbol >> 7
+  if (on) atomicAdd(&h[word], __umul24(high, 0xFFFFu) + 1u);         // 1 or 1 << 16
+}
 __device__ __forceinline__ void hist_add8_packed(uint32_t *h, const Group &g, uint32_t valid) {
-#pragma unroll
-  for (uint32_t q = 0; q < 8; ++q) {
-    const uint32_t sy = sym_at(g.sym, q);
-    if (q < valid) atomicAdd(&h[sy & 127u], 1u << ((sy >> 3) & 16u));
-  }
+  hist_add_packed<0>(h, g.sym[0], 0 < valid);
+  hist_add_packed<8>(h, g.sym[0], 1 < valid);
+  hist_add_packed<16>(h, g.sym[0], 2 < valid);
+  hist_add_packed<24>(h, g.sym[0], 3 < valid);
+  hist_add_packed<0>(h, g.sym[1], 4 < valid);
+  hist_add_packed<8>(h, g.sym[1], 5 < valid);
+  hist_add_packed<16>(h, g.sym[1], 6 < valid);
+  hist_add_packed<24>(h, g.sym[1], 7 < valid);
 }
 
 // 16 image bytes from LDS: unit u of the image at byte offset sh of s32
@@ -887,10 +898,17 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   // a stream-wide table codes every block of its stream: the wave derives
   // its encoder entries when it moves to a block of another stream
   uint32_t table_chunk = ~0u;
+  // deferred copy-out: the next block's ticket is taken before the table and
+  // the coding pass, which hide the atomic's latency (lane 0 holds it)
+  uint32_t next_ticket = 0;
+  if constexpr (DEFER) {
+    if (lane == 0) next_ticket = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 
   while (true) {
     uint32_t b = 0;
-    if (lane == 0) b = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if constexpr (DEFER) b = next_ticket;
+    else if (lane == 0) b = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     b = uniform(b);
     if (b >= a.n_blocks) break;
 
@@ -1069,6 +1087,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
       // the previous block's section leaves the staging area
       if (have_pend) finish_block<DT, SYS>(a, pend, stage, ovf);
       have_pend = false;
+      if (lane == 0) next_ticket = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       __syncthreads();
     }
     // ---- table ----

@@ -1379,6 +1379,7 @@ __device__ __forceinline__ void ring_maintain(Ring &rg, uint8_t *ring, const uin
 // stored frontier then stays at least 512 bytes ahead of the words a half
 // round reads, and a store never overwrites unread words.
 constexpr uint32_t kDecRingBytes = 2048;
+constexpr uint32_t kDecStatic = 2;  // blocks per decoding wave before it takes tickets
 constexpr uint32_t kDecChunk = 512;
 
 struct RingD {
@@ -1460,10 +1461,19 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
   }
   const uint8_t *raw_plane = s + g.raw_off;
 
+  // blocks are independent: the first kDecStatic blocks of a wave follow
+  // from its workgroup index, the rest come by ticket.  At launch every wave
+  // would otherwise queue on the one counter at once.
+  uint32_t iter = 0;
   while (true) {
     uint32_t b = 0;
-    if (lane == 0) b = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    b = uniform(b);
+    if (iter < kDecStatic) {
+      b = blockIdx.x + iter * gridDim.x;
+    } else {
+      if (lane == 0) b = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      b = kDecStatic * gridDim.x + uniform(b);
+    }
+    ++iter;
     if (b >= nb) break;
     const uint32_t d = ld32(s + kHeaderBytes + 4 * b);
     const uint64_t start = b ? 16ull * (ld32(s + kHeaderBytes + 4 * (b - 1)) & ~kStoredBit) : 0;

@@ -142,8 +142,8 @@ uzip_status uzip_compress(const void *d_in, uint64_t n_elems, uzip_dtype dtype,
  *   d_status:       device u32, set to UZIP_ECORRUPT if the stream is
  *                   corrupt or does not match (may be NULL).
  *   d_ws, ws_bytes: device workspace of uzip_workspace_size(
- *                   UZIP_OP_DECOMPRESS, ...) bytes (256: the counter that
- *                   hands blocks to workgroups), 16-byte aligned.
+ *                   UZIP_OP_DECOMPRESS, ...) bytes (256, reserved: the
+ *                   decoder keeps no state there), 16-byte aligned.
  * Errors: EINVAL, ENOSPC, EHIP, EUNSUPPORTED. */
 uzip_status uzip_decompress(const void *d_in, size_t in_bytes, uzip_dtype dtype,
                             uint64_t n_elems, void *d_out, size_t out_cap,

@@ -19,7 +19,7 @@
 //                   single-pass scan with decoupled look-back over blocks
 //                   taken in ticket order; the section is then stored with
 //                   16-byte writes straight into the final stream.
-//   decode_kernel   resident waves take blocks by ticket; each block's
+//   decode_kernel   resident waves walk the blocks grid-stride; each block's
 //                   offset is read from the directory, its decode table
 //                   (2048 x u32) is built in LDS, its words are staged
 //                   through an LDS ring and the 64 states decode forwards.
@@ -81,7 +81,7 @@ struct EncodeArgs {
   uint32_t table_bytes;
 };
 
-constexpr size_t kDecodeWsBytes = 256;   // the block ticket
+constexpr size_t kDecodeWsBytes = 256;   // reserved: the decoder keeps no state there
 
 struct DecodeArgs {
   const uint8_t *in;
@@ -90,7 +90,6 @@ struct DecodeArgs {
   uint32_t dtype;
   uint8_t *out;
   uint32_t *dstatus;
-  uint32_t *ticket;  // workspace: next block to decode
   const uint16_t *table;  // the caller's table (streams of table mode 2)
 };
 
@@ -1379,7 +1378,6 @@ __device__ __forceinline__ void ring_maintain(Ring &rg, uint8_t *ring, const uin
 // stored frontier then stays at least 512 bytes ahead of the words a half
 // round reads, and a store never overwrites unread words.
 constexpr uint32_t kDecRingBytes = 2048;
-constexpr uint32_t kDecStatic = 2;  // blocks per decoding wave before it takes tickets
 constexpr uint32_t kDecChunk = 512;
 
 struct RingD {
@@ -1461,20 +1459,9 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
   }
   const uint8_t *raw_plane = s + g.raw_off;
 
-  // blocks are independent: the first kDecStatic blocks of a wave follow
-  // from its workgroup index, the rest come by ticket.  At launch every wave
-  // would otherwise queue on the one counter at once.
-  uint32_t iter = 0;
-  while (true) {
-    uint32_t b = 0;
-    if (iter < kDecStatic) {
-      b = blockIdx.x + iter * gridDim.x;
-    } else {
-      if (lane == 0) b = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      b = kDecStatic * gridDim.x + uniform(b);
-    }
-    ++iter;
-    if (b >= nb) break;
+  // blocks are independent: a grid-stride walk, no ticket (one counter for
+  // every wave costs more in queueing than it recovers in balance)
+  for (uint32_t b = blockIdx.x; b < nb; b += gridDim.x) {
     const uint32_t d = ld32(s + kHeaderBytes + 4 * b);
     const uint64_t start = b ? 16ull * (ld32(s + kHeaderBytes + 4 * (b - 1)) & ~kStoredBit) : 0;
     const uint64_t end = 16ull * (d & ~kStoredBit);
@@ -2324,9 +2311,8 @@ uzip_status launch_decode(const void *d_in, size_t in_bytes, uzip_dtype dtype, u
   a.dtype = (uint32_t)dtype;
   a.out = (uint8_t *)d_out;
   a.dstatus = d_status;
-  a.ticket = (uint32_t *)d_ws;
   a.table = d_table;
-  // resident waves take blocks by ticket until none are left
+  // an occupancy-sized grid; its waves walk the blocks grid-stride
   const uint64_t most = (n_elems + (kMinBlockBytes / elem_bytes(dtype)) - 1) / (kMinBlockBytes / elem_bytes(dtype));
   static const void *const dec_tab[10] = {
       (const void *)decode_kernel<0>,       (const void *)decode_kernel<1>,       (const void *)decode_kernel<2>,
@@ -2339,8 +2325,6 @@ uzip_status launch_decode(const void *d_in, size_t in_bytes, uzip_dtype dtype, u
   uint64_t grid = (uint64_t)info.cus * (uint64_t)occ;
   if (grid > most) grid = most;
   if (grid == 0) grid = 1;
-  hipLaunchKernelGGL(clear_kernel, dim3(1), dim3(64), 0, stream, a.ticket, (uint64_t)1);
-  if (hipGetLastError() != hipSuccess) return UZIP_EHIP;
   void *args[] = {&a};
   if (hipLaunchKernel(fn, dim3((unsigned)grid), dim3(64), args, 0, stream) != hipSuccess) return UZIP_EHIP;
   return UZIP_OK;

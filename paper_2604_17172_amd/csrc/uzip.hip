@@ -1306,6 +1306,9 @@ __device__ __forceinline__ uint32_t decode_step_ring(uint32_t &x, bool valid, co
   const uint32_t c = (uint32_t)__popcll(m);
   p += c;
   rb = (rb + 2 * c) & (RB - 1);
+  // the ring offset stays a scalar of its own: the compiler would rebuild it
+  // from p with one more vector add per sub-step
+  rb = __builtin_amdgcn_readfirstlane(rb);
   return e;
 }
 

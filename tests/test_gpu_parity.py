@@ -135,6 +135,24 @@ def test_all_stored_random_bits(uz, dtype):
     check_roundtrip(uz, x, dtype, 65536, "random bits")
 
 
+@pytest.mark.parametrize("dtype,bb", [("bf16", 16384), ("e4m3fn", 16384), ("fp32", 65536)])
+def test_stored_and_coded_blocks_interleaved(uz, dtype, bb):
+    """Runs of incompressible blocks between coded ones in one stream: a
+    block's section is written after the next block's first pass, from the
+    staging area for a coded block and re-read from the input for a STORED
+    one, and the look-back fills in the inclusive prefixes of both kinds."""
+    per = bb // EB[dtype]
+    n_blocks = 600
+    n = n_blocks * per - 123
+    x = special_words(dtype, n, seed=31)
+    noise = W.random_bits(n, 8 * EB[dtype], seed=32).astype(x.dtype)
+    rng = np.random.default_rng(33)
+    for b in range(n_blocks):
+        if rng.random() < 0.3:  # about 30% of the blocks: random bits, so STORED
+            x[b * per:(b + 1) * per] = noise[b * per:(b + 1) * per]
+    check_roundtrip(uz, x, dtype, bb, "stored and coded blocks interleaved")
+
+
 def test_single_symbol_blocks(uz):
     x = np.full(3 * 32768 + 5, 0x3F80, np.uint16)
     x[40000:40010] = 0x4000

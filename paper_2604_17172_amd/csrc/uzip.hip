@@ -871,7 +871,10 @@ template <int DT, bool REDUCE, bool SMALL, bool SYS, bool SHARED = false>
 __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   constexpr int E = (DT == 2) ? 4 : 2;
   constexpr int NW = 4 * (E / 2);
-  constexpr int D = (E == 2) ? 8 : 4;  // pass-1 load pipeline depth (rounds)
+  // pass-1 load pipeline depth (rounds; it must divide 16): 16 KiB in flight
+  // per wave for 16-bit elements (8 KiB where the stream-wide table's
+  // variants would spill), 8 KiB for fp32
+  constexpr int D = (E == 2) ? (SHARED ? 8 : 16) : 4;
   extern __shared__ __align__(16) uint8_t smem_base[];
   uint8_t *smem = smem_base + kTrashBytes;  // [trash | encoder table | histogram / staging]
   uint4 *enc = (uint4 *)smem;

@@ -304,6 +304,24 @@ def test_reduce_matches_oracle(uz, dtype, n_in):
                 assert np.array_equal(host_bits(raw, dtype), want_y)
 
 
+@pytest.mark.parametrize("dtype,bb", [("bf16", 16384), ("bf16", 4096), ("fp16", 8192), ("fp32", 16384)])
+def test_reduce_small_blocks(uz, dtype, bb):
+    """Blocks down to the 4 KiB minimum: many more blocks per share than
+    64 KiB blocks give, and a ragged last block."""
+    n = 200_003
+    n_in = 5
+    say(f"[parity] reduce small blocks dtype={dtype} block={bb} n_in={n_in} n={n}")
+    xs = [special_words(dtype, n, seed=400 + i) for i in range(n_in)]
+    streams = [ref.compress(v, dtype, bb) for v in xs]
+    local = special_words(dtype, n, seed=499)
+    out, size, raw, status = uz.reduce_fused([dev(t) for t in streams], dtype, n, bb, local=to_dev_bits(local, dtype))
+    torch.cuda.synchronize()
+    want_s, want_y = ref.reduce(streams, dtype, n, bb, local=local)
+    assert int(status.item()) == 0
+    assert np.array_equal(out[:int(size.item())].cpu().numpy(), want_s)
+    assert np.array_equal(host_bits(raw, dtype), want_y)
+
+
 def test_reduce_sixteen_inputs_with_stored_blocks(uz):
     n = 70_000
     say("[parity] reduce n_in=16")

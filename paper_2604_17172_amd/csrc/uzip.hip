@@ -18,7 +18,10 @@
 //                   staging area; the block's output offset comes from a
 //                   single-pass scan with decoupled look-back over blocks
 //                   taken in ticket order; the section is then stored with
-//                   16-byte writes straight into the final stream.
+//                   16-byte writes straight into the final stream.  Blocks
+//                   of up to 32768 elements resolve their offset and write
+//                   their section only after the wave's next block has
+//                   streamed through pass 1.
 //   decode_kernel   resident waves walk the blocks grid-stride; each block's
 //                   offset is read from the directory, its decode table
 //                   (2048 x u32) is built in LDS, its words are staged
@@ -27,8 +30,8 @@
 //                   output block decodes block b of up to eight inputs in
 //                   parallel waves, round by round, and a further wave adds
 //                   them in binary32 in input order and splits the rounded
-//                   result (raw plane, histogram); the coding pass of
-//                   encode_kernel then runs over the reduced tensor.
+//                   result (raw plane, histogram); reduce_kernel, the
+//                   encoder's coding half, then runs over the reduced tensor.
 //   split-send producer  encode_kernel with write-through stores and
 //                   per-chunk completion counters.
 #include <hip/hip_fp16.h>

@@ -8,10 +8,11 @@ stream again (uzip_decompress), inputs resident in HBM.  ``value`` is the
 uncompressed bytes of the buffer divided by the time of one step.  The line
 also reports compress and decompress rates separately, the ratio, the
 split-send producer on the same buffer (4 MiB chunks, host-mapped flags),
-the fused reduce of eight 16 MiB bf16 shares, the HBM roofline of the
-dominant kernel and the CPU oracle timed on a bounded sample.
+the fused reduce of eight 16 MiB bf16 shares (with --reduce-full also eight
+whole [8192 x 8192] slices), the HBM roofline of the dominant kernel and the
+CPU oracle timed on a bounded sample.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--reduce-full]
 """
 from __future__ import annotations
 
@@ -68,6 +69,8 @@ def main() -> int:
     ap.add_argument("--no-extras", action="store_true", help="skip the chunked and reduce legs")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 1 GiB device copy (counter calibration under rocprofv3)")
+    ap.add_argument("--reduce-full", action="store_true",
+                    help="also time the fused reduce on the full-tensor reading: 8 slices [8192 x 8192] bf16")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
@@ -214,6 +217,44 @@ def main() -> int:
                             "ratio_in": round(sum(in_bytes) / (8 * 2 * rn), 4),
                             "ratio_out": round(int(rsz.item()) / (2 * rn), 4)}
         log(f"[bench] fused reduce {r_ms:.3f} ms (after a cache flush: {rc_ms:.3f} ms)")
+
+        if args.reduce_full:
+            # the other reading of the activation slices: each input is the
+            # whole [8192 x 8192] tensor (128 MiB), 2048 blocks per input
+            fshares = W.reduce_slices(tokens=8192)
+            fn_ = fshares[0].size
+            fstreams = []
+            for s_ in fshares:
+                st, sz = uz.compress(torch.from_numpy(s_.view(np.int16)).to(dev), bb, dtype="bf16")
+                fstreams.append(st[:int(sz.item())].clone())
+            del fshares
+            f_in = sum(t.numel() for t in fstreams)
+            fout = torch.empty(uz.uzip_max_compressed_size(uz.BF16, fn_, bb), dtype=torch.uint8, device=dev)
+            fws = torch.empty(uz.uzip_workspace_size(uz.OP_REDUCE, uz.BF16, fn_, bb, 8), dtype=torch.uint8,
+                              device=dev)
+            times = []
+            for r in range(reps + 1):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                _, fsz, fraw, fst = uz.reduce_fused(fstreams, "bf16", fn_, bb, out=fout, ws=fws)
+                b.record(stream)
+                torch.cuda.synchronize()
+                if r > 0:
+                    times.append(a.elapsed_time(b))
+            assert int(fst.item()) == 0
+            # the output stream decodes to the reduced tensor the call returned
+            fy, fyst = uz.decompress(fout, "bf16", fn_)
+            torch.cuda.synchronize()
+            assert int(fyst.item()) == 0 and torch.equal(fy.view(torch.int16), fraw.view(torch.int16))
+            f_ms = float(np.mean(times))
+            f_moved = f_in + int(fsz.item()) + 2 * fn_
+            extras["reduce_full_tensor"] = {
+                "n_in": 8, "elems_per_input": fn_, "ms": round(f_ms, 4),
+                "input_GBps_uncompressed": round(8 * 2 * fn_ / (f_ms * 1e-3) / 1e9, 1),
+                "hbm_frac": round(f_moved / (f_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                "ratio_in": round(f_in / (8 * 2 * fn_), 4)}
+            log(f"[bench] fused reduce, full-tensor reading (8 x 128 MiB) {f_ms:.3f} ms")
+            del fstreams, fout, fws, fy, fraw
 
         # ------------- stream-wide tables: the same buffer, one table per stream -------------
         tws = torch.empty(uz.uzip_workspace_size(uz.OP_COMPRESS_TABLE, uz.BF16, n, bb), dtype=torch.uint8, device=dev)

@@ -1898,20 +1898,23 @@ __global__ void empty_stream_kernel(uint8_t *out, uint32_t dt, uint32_t block_el
 // min(n, 256 KiB / E) elements, then f[s] = 1 + floor(c[s](M - 256)/n_s) for
 // all 256 symbols, the remainder to the most frequent (ties: the smallest).
 // One workgroup of 4 waves per stream (workgroup c: the stream of elements
-// [c chunk_elems, ...)), 8 sub-histograms per wave (lane & 7: skewed
-// exponents would otherwise serialise the LDS atomics); written to
-// dst0 + 256 c and, if `out` is given, to the table's place in stream c
+// [c chunk_elems, ...)).  Every thread counts into a histogram of its own
+// (16-bit counts packed as in the encoder, a thread sees at most 512
+// symbols), so skewed exponents cost no atomic conflicts; the 256 private
+// histograms are then summed bin by bin.  The table is written to
+// dst0 + 256 c and, if `out` is given, to its place in stream c
 // (out + c slot_bytes, after its directory).
 // ---------------------------------------------------------------------------
 constexpr uint32_t kTableThreads = 256;
-constexpr uint32_t kTableReplicas = (kTableThreads / 64) * kHistReplicas;
+constexpr uint32_t kLaneHist = kPackedHistStride;  // 128 packed words + 1: a bin of consecutive threads in distinct banks
+constexpr uint32_t kTableLds = kTableThreads * kLaneHist * 4;
 template <int DT>
 __global__ void __launch_bounds__(kTableThreads) table_kernel(const uint8_t *in_all, uint64_t n_all,
                                                              uint64_t chunk_elems, uint32_t block_elems,
                                                              uint16_t *dst0_all, uint8_t *out, uint64_t slot_bytes) {
   constexpr int E = dt_bytes<DT>();
   constexpr int NW = 4 * (E / 2);
-  __shared__ uint32_t h[kTableReplicas * kHistStride];
+  extern __shared__ __align__(16) uint32_t hl[];  // [thread][kLaneHist]
   const uint64_t first = (uint64_t)blockIdx.x * chunk_elems;
   const uint8_t *in = in_all + first * E;
   const uint64_t n = n_all - first < chunk_elems ? n_all - first : chunk_elems;
@@ -1919,14 +1922,16 @@ __global__ void __launch_bounds__(kTableThreads) table_kernel(const uint8_t *in_
   uint16_t *dst1 = out == nullptr ? nullptr
                                   : (uint16_t *)(out + blockIdx.x * slot_bytes + kHeaderBytes +
                                                  pad16(4 * ((n + block_elems - 1) / block_elems)));
-  for (uint32_t i = threadIdx.x; i < kTableReplicas * kHistStride; i += kTableThreads) h[i] = 0;
+  for (uint32_t i = threadIdx.x; i < kTableThreads * kLaneHist / 4; i += kTableThreads)
+    ((uint4 *)hl)[i] = make_uint4(0, 0, 0, 0);
   __syncthreads();
   const uint64_t n_s = n < kSampleBytes / E ? n : kSampleBytes / E;
-  uint32_t *hw = h + ((threadIdx.x / 64) * kHistReplicas + (threadIdx.x & (kHistReplicas - 1))) * kHistStride;
+  uint32_t *mine = hl + threadIdx.x * kLaneHist;
   // the sample in batches of 16 groups of 8 elements per thread, every
   // load of a batch issued before its first use
   constexpr uint32_t kBatch = 16;
   constexpr uint32_t kBatches = kSampleBytes / E / (kPerLane * kTableThreads * kBatch);
+  static_assert(kBatches * kBatch * kPerLane <= 65535, "private 16-bit counts");
   for (uint32_t bt = 0; bt < kBatches; ++bt) {
     uint32_t w[kBatch][NW];
     uint32_t valid[kBatch];
@@ -1940,18 +1945,30 @@ __global__ void __launch_bounds__(kTableThreads) table_kernel(const uint8_t *in_
     for (uint32_t it = 0; it < kBatch; ++it) {
       Group gr;
       split_group<DT>(w[it], gr);
-      hist_add8(hw, gr, valid[it]);
+      hist_add8_packed(mine, gr, valid[it]);
     }
   }
+  __syncthreads();
+  // thread t sums word t & 127 (symbols t & 127 and (t & 127) + 128) over
+  // half of the private histograms, the two halves of each word apart
+  const uint32_t wd = threadIdx.x & 127u, part = threadIdx.x >> 7;
+  uint32_t lo = 0, hi = 0;
+  for (uint32_t r = 0; r < kTableThreads / 2; ++r) {
+    const uint32_t v = hl[(part * (kTableThreads / 2) + r) * kLaneHist + wd];
+    lo += v & 0xFFFFu;
+    hi += v >> 16;
+  }
+  __syncthreads();
+  uint32_t *sums = hl;  // [2][256]: per half, the count of every symbol
+  sums[256 * part + wd] = lo;
+  sums[256 * part + wd + 128] = hi;
   __syncthreads();
   if (threadIdx.x >= 64) return;
   const uint32_t lane = threadIdx.x;
   uint32_t c[4], f[4], lt = 0, key = 0;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    uint32_t acc = 0;
-    for (uint32_t rp = 0; rp < kTableReplicas; ++rp) acc += h[rp * kHistStride + 4 * lane + q];
-    c[q] = acc;
+    c[q] = sums[4 * lane + q] + sums[256 + 4 * lane + q];
     // c (M - 256) < 2^17 * 2^11: the quotient is exact in 32 bits
     f[q] = n_s ? 1u + (c[q] * (kM - 256u)) / (uint32_t)n_s : kM / 256u;
     lt += f[q];
@@ -2039,6 +2056,11 @@ uzip_status device_info(DeviceInfo &out) {
     (void)hipFuncSetAttribute((const void *)reduce_decode_kernel<0>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
     (void)hipFuncSetAttribute((const void *)reduce_decode_kernel<1>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
     (void)hipFuncSetAttribute((const void *)reduce_decode_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
+    (void)hipFuncSetAttribute((const void *)table_kernel<0>, hipFuncAttributeMaxDynamicSharedMemorySize, kTableLds);
+    (void)hipFuncSetAttribute((const void *)table_kernel<1>, hipFuncAttributeMaxDynamicSharedMemorySize, kTableLds);
+    (void)hipFuncSetAttribute((const void *)table_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize, kTableLds);
+    (void)hipFuncSetAttribute((const void *)table_kernel<3>, hipFuncAttributeMaxDynamicSharedMemorySize, kTableLds);
+    (void)hipFuncSetAttribute((const void *)table_kernel<4>, hipFuncAttributeMaxDynamicSharedMemorySize, kTableLds);
   });
   if (err != hipSuccess) return UZIP_EHIP;
   out = g_info[dev];
@@ -2122,7 +2144,7 @@ uzip_status launch_table(const void *d_in, uint64_t n, uzip_dtype dt, uint64_t c
                                      (const void *)table_kernel<4>};
   const uint8_t *in = (const uint8_t *)d_in;
   void *args[] = {&in, &n, &chunk_elems, &block_elems, &dst0, &out, &slot_bytes};
-  if (hipLaunchKernel(tab[(int)dt], dim3((unsigned)chunks), dim3(kTableThreads), args, 0, stream) != hipSuccess)
+  if (hipLaunchKernel(tab[(int)dt], dim3((unsigned)chunks), dim3(kTableThreads), args, kTableLds, stream) != hipSuccess)
     return UZIP_EHIP;
   return UZIP_OK;
 }

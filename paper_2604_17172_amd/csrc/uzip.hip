@@ -1892,6 +1892,31 @@ __global__ void empty_stream_kernel(uint8_t *out, uint32_t dt, uint32_t block_el
   }
 }
 
+// The stream-wide table from the counts c[4] of symbols 4 lane .. 4 lane + 3
+// of an n_s-element sample (one wave): f[s] = 1 + floor(c[s](M - 256)/n_s),
+// the remainder to the most frequent symbol (ties: the smallest); written to
+// dst0 and, if given, dst1.
+__device__ void write_table(const uint32_t c[4], uint32_t n_s, uint16_t *dst0, uint16_t *dst1) {
+  const uint32_t lane = lane_id();
+  uint32_t f[4], lt = 0, key = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    // c (M - 256) < 2^17 * 2^11: the quotient is exact in 32 bits
+    f[q] = n_s ? 1u + (c[q] * (kM - 256u)) / n_s : kM / 256u;
+    lt += f[q];
+    const uint32_t kq = (c[q] << 8) | (255u - (4 * lane + q));
+    key = kq > key ? kq : key;
+  }
+  const uint32_t d = kM - wave_sum(lt);
+  const uint32_t best = 255u - (wave_max(key) & 0xFFu);
+#pragma unroll
+  for (uint32_t q = 0; q < 4; ++q)
+    if (best == 4 * lane + q) f[q] += d;
+  const uint2 v = make_uint2(f[0] | (f[1] << 16), f[2] | (f[3] << 16));
+  *(uint2 *)(dst0 + 4 * lane) = v;
+  if (dst1 != nullptr) *(uint2 *)(dst1 + 4 * lane) = v;
+}
+
 // ---------------------------------------------------------------------------
 // table_kernel: the stream-wide table of a tensor (section 3.3.1's table from
 // a sample of the range): histogram of the symbols of its first
@@ -1964,25 +1989,65 @@ __global__ void __launch_bounds__(kTableThreads) table_kernel(const uint8_t *in_
   sums[256 * part + wd + 128] = hi;
   __syncthreads();
   if (threadIdx.x >= 64) return;
-  const uint32_t lane = threadIdx.x;
-  uint32_t c[4], f[4], lt = 0, key = 0;
+  uint32_t c[4];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    c[q] = sums[4 * lane + q] + sums[256 + 4 * lane + q];
-    // c (M - 256) < 2^17 * 2^11: the quotient is exact in 32 bits
-    f[q] = n_s ? 1u + (c[q] * (kM - 256u)) / (uint32_t)n_s : kM / 256u;
-    lt += f[q];
-    const uint32_t kq = (c[q] << 8) | (255u - (4 * lane + q));
-    key = kq > key ? kq : key;
+  for (int q = 0; q < 4; ++q) c[q] = sums[4 * threadIdx.x + q] + sums[256 + 4 * threadIdx.x + q];
+  write_table(c, (uint32_t)n_s, dst0, dst1);
+}
+
+// The sample split over kTableParts workgroups of one stream (a single
+// stream has its whole sample on one CU otherwise): workgroup p counts
+// elements [p S, (p + 1) S) of the sample, S = (256 KiB / E) / kTableParts,
+// into 8 sub-histograms per wave and writes its 256 counts to
+// part_out + 256 p; table_merge_kernel then sums the parts.
+constexpr uint32_t kTableParts = 16;
+template <int DT>
+__global__ void __launch_bounds__(kTableThreads) table_part_kernel(const uint8_t *in, uint64_t n,
+                                                                  uint32_t *part_out) {
+  constexpr int E = dt_bytes<DT>();
+  constexpr int NW = 4 * (E / 2);
+  constexpr uint32_t kReps = (kTableThreads / 64) * kHistReplicas;
+  constexpr uint32_t kSlice = kSampleBytes / E / kTableParts;
+  constexpr uint32_t kGroups = kSlice / (kPerLane * kTableThreads);
+  static_assert(kGroups * kPerLane * kTableThreads == kSlice, "slice cover");
+  __shared__ uint32_t h[kReps * kHistStride];
+  for (uint32_t i = threadIdx.x; i < kReps * kHistStride; i += kTableThreads) h[i] = 0;
+  __syncthreads();
+  const uint64_t n_s = n < kSampleBytes / E ? n : kSampleBytes / E;
+  uint32_t *hw = h + ((threadIdx.x / 64) * kHistReplicas + (threadIdx.x & (kHistReplicas - 1))) * kHistStride;
+  uint32_t w[kGroups][NW], valid[kGroups];
+#pragma unroll
+  for (uint32_t it = 0; it < kGroups; ++it) {
+    const uint64_t i0 = (uint64_t)blockIdx.x * kSlice + (uint64_t)kPerLane * (threadIdx.x + it * kTableThreads);
+    valid[it] = i0 < n_s ? (uint32_t)(n_s - i0 < kPerLane ? n_s - i0 : kPerLane) : 0u;
+    load_words<E>(in, i0, valid[it], w[it]);
   }
-  const uint32_t d = kM - wave_sum(lt);
-  const uint32_t best = 255u - (wave_max(key) & 0xFFu);
 #pragma unroll
-  for (uint32_t q = 0; q < 4; ++q)
-    if (best == 4 * lane + q) f[q] += d;
-  const uint2 v = make_uint2(f[0] | (f[1] << 16), f[2] | (f[3] << 16));
-  *(uint2 *)(dst0 + 4 * lane) = v;
-  if (dst1 != nullptr) *(uint2 *)(dst1 + 4 * lane) = v;
+  for (uint32_t it = 0; it < kGroups; ++it) {
+    Group gr;
+    split_group<DT>(w[it], gr);
+    hist_add8(hw, gr, valid[it]);
+  }
+  __syncthreads();
+  for (uint32_t sy = threadIdx.x; sy < 256; sy += kTableThreads) {
+    uint32_t acc = 0;
+    for (uint32_t rp = 0; rp < kReps; ++rp) acc += h[rp * kHistStride + sy];
+    part_out[256ull * blockIdx.x + sy] = acc;
+  }
+}
+
+// One wave: the parts' counts summed, then the table (as table_kernel).
+__global__ void __launch_bounds__(64) table_merge_kernel(const uint32_t *parts, uint32_t n_s, uint16_t *dst0,
+                                                         uint16_t *dst1) {
+  uint32_t c[4] = {0, 0, 0, 0};
+  for (uint32_t p = 0; p < kTableParts; ++p) {
+    const uint4 v = *(const uint4 *)(parts + 256 * p + 4 * threadIdx.x);
+    c[0] += v.x;
+    c[1] += v.y;
+    c[2] += v.z;
+    c[3] += v.w;
+  }
+  write_table(c, n_s, dst0, dst1);
 }
 
 // ---------------------------------------------------------------------------
@@ -2149,6 +2214,24 @@ uzip_status launch_table(const void *d_in, uint64_t n, uzip_dtype dt, uint64_t c
   return UZIP_OK;
 }
 
+// One stream's table with the sample split over kTableParts workgroups;
+// `parts`: kTableParts * 256 u32 of workspace.
+uzip_status launch_table_split(const void *d_in, uint64_t n, uzip_dtype dt, uint16_t *dst0, uint8_t *dst1,
+                               uint32_t *parts, hipStream_t stream) {
+  static const void *const tab[5] = {(const void *)table_part_kernel<0>, (const void *)table_part_kernel<1>,
+                                     (const void *)table_part_kernel<2>, (const void *)table_part_kernel<3>,
+                                     (const void *)table_part_kernel<4>};
+  const uint8_t *in = (const uint8_t *)d_in;
+  void *args[] = {&in, &n, &parts};
+  if (hipLaunchKernel(tab[(int)dt], dim3(kTableParts), dim3(kTableThreads), args, 0, stream) != hipSuccess)
+    return UZIP_EHIP;
+  const uint64_t cap = kSampleBytes / elem_bytes(dt);
+  const uint32_t n_s = (uint32_t)(n < cap ? n : cap);
+  hipLaunchKernelGGL(table_merge_kernel, dim3(1), dim3(64), 0, stream, (const uint32_t *)parts, n_s, dst0,
+                     (uint16_t *)dst1);
+  return hipGetLastError() == hipSuccess ? UZIP_OK : UZIP_EHIP;
+}
+
 uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws, const EncodeWs &w,
                           const DeviceInfo &info, hipStream_t stream, bool shared = false) {
   const bool small = !reduce && small_path(a.block_elems);
@@ -2199,7 +2282,7 @@ size_t uzip_workspace_size(int op, uzip_dtype dtype, uint64_t n_elems, uint32_t 
     case UZIP_OP_DECOMPRESS:
       return kDecodeWsBytes;
     case UZIP_OP_COMPRESS_TABLE:
-      return (size_t)encode_ws(nb, 1, be, 0).total + kTableBytes;
+      return (size_t)encode_ws(nb, 1, be, 0).total + kTableBytes + kTableParts * 256 * 4;
     case UZIP_OP_CHUNKED_TABLE: {
       if (aux == 0 || aux % block_bytes) return 0;
       const uint64_t ce = aux / E;
@@ -2412,13 +2495,16 @@ uzip_status uzip_compress_table(const void *d_in, uint64_t n_elems, uzip_dtype d
     return hipGetLastError() == hipSuccess ? UZIP_OK : UZIP_EHIP;
   }
   EncodeWs w = encode_ws(nb, 1, be, 0);
-  if (d_ws == nullptr || !aligned16(d_ws) || ws_bytes < w.total + kTableBytes) return UZIP_ENOSPC;
+  if (d_ws == nullptr || !aligned16(d_ws) || ws_bytes < w.total + kTableBytes + kTableParts * 256 * 4)
+    return UZIP_ENOSPC;
   uint8_t *ws = (uint8_t *)d_ws;
   const uint16_t *table = d_table;
   if (mode == UZIP_TABLE_SAMPLED) {
-    // the table, into the workspace and its place in the stream
+    // the table, into the workspace and its place in the stream (after the
+    // directory)
     uint16_t *t = (uint16_t *)(ws + w.total);
-    st = launch_table(d_in, n_elems, dtype, n_elems, be, 1, t, (uint8_t *)d_out, 0, stream);
+    uint8_t *in_stream = (uint8_t *)d_out + kHeaderBytes + pad16(4 * nb);
+    st = launch_table_split(d_in, n_elems, dtype, t, in_stream, (uint32_t *)(ws + w.total + kTableBytes), stream);
     if (st != UZIP_OK) return st;
     table = t;
   }

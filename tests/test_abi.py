@@ -107,7 +107,9 @@ def test_table_api_host_checks():
     import paper_2604_17172_amd as uz
     n, bb = 1 << 20, 65536
     base = uz.uzip_workspace_size(uz.OP_COMPRESS, uz.BF16, n, bb)
-    assert uz.uzip_workspace_size(uz.OP_COMPRESS_TABLE, uz.BF16, n, bb) == base + uz.TABLE_BYTES
+    # the compressor's own workspace, the table, and 16 x 256 sample counts
+    # (the sample is split over 16 workgroups)
+    assert uz.uzip_workspace_size(uz.OP_COMPRESS_TABLE, uz.BF16, n, bb) == base + uz.TABLE_BYTES + 16 * 256 * 4
     # bad mode, missing or misaligned table, too small an output
     assert uz.uzip_compress_table(16, 100, 0, bb, 3, None, 32, 1 << 20, None, 48, 1 << 20, None) == uz.EINVAL
     assert uz.uzip_compress_table(16, 100, 0, bb, uz.TABLE_EXTERNAL, None, 32, 1 << 20, None, 48, 1 << 20,

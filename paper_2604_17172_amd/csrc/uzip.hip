@@ -1995,15 +1995,16 @@ __global__ void __launch_bounds__(kTableThreads) table_kernel(const uint8_t *in_
   write_table(c, (uint32_t)n_s, dst0, dst1);
 }
 
-// The sample split over kTableParts workgroups of one stream (a single
-// stream has its whole sample on one CU otherwise): workgroup p counts
-// elements [p S, (p + 1) S) of the sample, S = (256 KiB / E) / kTableParts,
-// into 8 sub-histograms per wave and writes its 256 counts to
-// part_out + 256 p; table_merge_kernel then sums the parts.
+// Each stream's sample split over kTableParts workgroups (one workgroup per
+// stream would count a whole sample on one CU): workgroup kTableParts c + p
+// counts elements [p S, (p + 1) S) of the sample of stream c (elements
+// [c chunk_elems, ...) of the tensor), S = (256 KiB / E) / kTableParts, into
+// 8 sub-histograms per wave and writes its 256 counts to
+// part_out + 256 (kTableParts c + p); table_merge_kernel sums the parts.
 constexpr uint32_t kTableParts = 16;
 template <int DT>
-__global__ void __launch_bounds__(kTableThreads) table_part_kernel(const uint8_t *in, uint64_t n,
-                                                                  uint32_t *part_out) {
+__global__ void __launch_bounds__(kTableThreads) table_part_kernel(const uint8_t *in_all, uint64_t n_all,
+                                                                  uint64_t chunk_elems, uint32_t *part_out) {
   constexpr int E = dt_bytes<DT>();
   constexpr int NW = 4 * (E / 2);
   constexpr uint32_t kReps = (kTableThreads / 64) * kHistReplicas;
@@ -2013,12 +2014,16 @@ __global__ void __launch_bounds__(kTableThreads) table_part_kernel(const uint8_t
   __shared__ uint32_t h[kReps * kHistStride];
   for (uint32_t i = threadIdx.x; i < kReps * kHistStride; i += kTableThreads) h[i] = 0;
   __syncthreads();
+  const uint32_t chunk = blockIdx.x / kTableParts, part = blockIdx.x % kTableParts;
+  const uint64_t first = (uint64_t)chunk * chunk_elems;
+  const uint8_t *in = in_all + first * E;
+  const uint64_t n = n_all - first < chunk_elems ? n_all - first : chunk_elems;
   const uint64_t n_s = n < kSampleBytes / E ? n : kSampleBytes / E;
   uint32_t *hw = h + ((threadIdx.x / 64) * kHistReplicas + (threadIdx.x & (kHistReplicas - 1))) * kHistStride;
   uint32_t w[kGroups][NW], valid[kGroups];
 #pragma unroll
   for (uint32_t it = 0; it < kGroups; ++it) {
-    const uint64_t i0 = (uint64_t)blockIdx.x * kSlice + (uint64_t)kPerLane * (threadIdx.x + it * kTableThreads);
+    const uint64_t i0 = (uint64_t)part * kSlice + (uint64_t)kPerLane * (threadIdx.x + it * kTableThreads);
     valid[it] = i0 < n_s ? (uint32_t)(n_s - i0 < kPerLane ? n_s - i0 : kPerLane) : 0u;
     load_words<E>(in, i0, valid[it], w[it]);
   }
@@ -2036,9 +2041,21 @@ __global__ void __launch_bounds__(kTableThreads) table_part_kernel(const uint8_t
   }
 }
 
-// One wave: the parts' counts summed, then the table (as table_kernel).
-__global__ void __launch_bounds__(64) table_merge_kernel(const uint32_t *parts, uint32_t n_s, uint16_t *dst0,
-                                                         uint16_t *dst1) {
+// One wave per stream c: its parts' counts summed, then the table, written
+// to dst0 + 256 c and, if `out` is given, to its place in stream c (as
+// table_kernel).
+__global__ void __launch_bounds__(64) table_merge_kernel(const uint32_t *parts_all, uint64_t n_all,
+                                                         uint64_t chunk_elems, uint32_t block_elems, uint32_t e_bytes,
+                                                         uint16_t *dst0_all, uint8_t *out, uint64_t slot_bytes) {
+  const uint64_t first = (uint64_t)blockIdx.x * chunk_elems;
+  const uint64_t n = n_all - first < chunk_elems ? n_all - first : chunk_elems;
+  const uint64_t cap = kSampleBytes / e_bytes;
+  const uint32_t n_s = (uint32_t)(n < cap ? n : cap);
+  uint16_t *dst0 = dst0_all + 256ull * blockIdx.x;
+  uint16_t *dst1 = out == nullptr ? nullptr
+                                  : (uint16_t *)(out + blockIdx.x * slot_bytes + kHeaderBytes +
+                                                 pad16(4 * ((n + block_elems - 1) / block_elems)));
+  const uint32_t *parts = parts_all + 256ull * kTableParts * blockIdx.x;
   uint32_t c[4] = {0, 0, 0, 0};
   for (uint32_t p = 0; p < kTableParts; ++p) {
     const uint4 v = *(const uint4 *)(parts + 256 * p + 4 * threadIdx.x);
@@ -2214,21 +2231,22 @@ uzip_status launch_table(const void *d_in, uint64_t n, uzip_dtype dt, uint64_t c
   return UZIP_OK;
 }
 
-// One stream's table with the sample split over kTableParts workgroups;
-// `parts`: kTableParts * 256 u32 of workspace.
-uzip_status launch_table_split(const void *d_in, uint64_t n, uzip_dtype dt, uint16_t *dst0, uint8_t *dst1,
-                               uint32_t *parts, hipStream_t stream) {
+// The tables of `chunks` streams (as launch_table) with each sample split
+// over kTableParts workgroups; `parts`: chunks * kTableParts * 256 u32 of
+// workspace.
+uzip_status launch_table_split(const void *d_in, uint64_t n, uzip_dtype dt, uint64_t chunk_elems,
+                               uint32_t block_elems, uint64_t chunks, uint16_t *dst0, uint8_t *out,
+                               uint64_t slot_bytes, uint32_t *parts, hipStream_t stream) {
   static const void *const tab[5] = {(const void *)table_part_kernel<0>, (const void *)table_part_kernel<1>,
                                      (const void *)table_part_kernel<2>, (const void *)table_part_kernel<3>,
                                      (const void *)table_part_kernel<4>};
   const uint8_t *in = (const uint8_t *)d_in;
-  void *args[] = {&in, &n, &parts};
-  if (hipLaunchKernel(tab[(int)dt], dim3(kTableParts), dim3(kTableThreads), args, 0, stream) != hipSuccess)
+  void *args[] = {&in, &n, &chunk_elems, &parts};
+  if (hipLaunchKernel(tab[(int)dt], dim3((unsigned)(chunks * kTableParts)), dim3(kTableThreads), args, 0, stream) !=
+      hipSuccess)
     return UZIP_EHIP;
-  const uint64_t cap = kSampleBytes / elem_bytes(dt);
-  const uint32_t n_s = (uint32_t)(n < cap ? n : cap);
-  hipLaunchKernelGGL(table_merge_kernel, dim3(1), dim3(64), 0, stream, (const uint32_t *)parts, n_s, dst0,
-                     (uint16_t *)dst1);
+  hipLaunchKernelGGL(table_merge_kernel, dim3((unsigned)chunks), dim3(64), 0, stream, (const uint32_t *)parts, n,
+                     chunk_elems, block_elems, elem_bytes(dt), dst0, out, slot_bytes);
   return hipGetLastError() == hipSuccess ? UZIP_OK : UZIP_EHIP;
 }
 
@@ -2287,7 +2305,7 @@ size_t uzip_workspace_size(int op, uzip_dtype dtype, uint64_t n_elems, uint32_t 
       if (aux == 0 || aux % block_bytes) return 0;
       const uint64_t ce = aux / E;
       const uint64_t chunks = (n_elems + ce - 1) / ce;
-      return (size_t)(encode_ws(chunks * (ce / be), chunks, be, 0).total + chunks * kTableBytes);
+      return (size_t)(encode_ws(chunks * (ce / be), chunks, be, 0).total + chunks * (kTableBytes + kTableParts * 256 * 4));
     }
     case UZIP_OP_CHUNKED: {
       if (aux == 0 || aux % block_bytes) return 0;
@@ -2372,14 +2390,15 @@ uzip_status uzip_compress_chunked_table(const void *d_in, uint64_t n_elems, uzip
   uzip_status st = device_info(info);
   if (st != UZIP_OK) return st;
   EncodeWs w = encode_ws(chunks * (ce / be), chunks, be, 0);
-  const uint64_t ws_need = w.total + (mode == UZIP_TABLE_SAMPLED ? chunks * kTableBytes : 0);
+  const uint64_t ws_need = w.total + (mode == UZIP_TABLE_SAMPLED ? chunks * (kTableBytes + kTableParts * 256 * 4) : 0);
   if (d_ws == nullptr || !aligned16(d_ws) || ws_bytes < ws_need) return UZIP_ENOSPC;
   const uint16_t *table = d_table;
   if (mode == UZIP_TABLE_SAMPLED) {
     // each chunk's table from its own first 256 KiB, into the workspace
     // and its place in the chunk's stream
     uint16_t *t = (uint16_t *)((uint8_t *)d_ws + w.total);
-    st = launch_table(d_in, n_elems, dtype, ce, be, chunks, t, (uint8_t *)d_out, slot_bytes, stream);
+    st = launch_table_split(d_in, n_elems, dtype, ce, be, chunks, t, (uint8_t *)d_out, slot_bytes,
+                            (uint32_t *)((uint8_t *)d_ws + w.total + chunks * kTableBytes), stream);
     if (st != UZIP_OK) return st;
     table = t;
   }
@@ -2503,8 +2522,8 @@ uzip_status uzip_compress_table(const void *d_in, uint64_t n_elems, uzip_dtype d
     // the table, into the workspace and its place in the stream (after the
     // directory)
     uint16_t *t = (uint16_t *)(ws + w.total);
-    uint8_t *in_stream = (uint8_t *)d_out + kHeaderBytes + pad16(4 * nb);
-    st = launch_table_split(d_in, n_elems, dtype, t, in_stream, (uint32_t *)(ws + w.total + kTableBytes), stream);
+    st = launch_table_split(d_in, n_elems, dtype, n_elems, be, 1, t, (uint8_t *)d_out, 0,
+                            (uint32_t *)(ws + w.total + kTableBytes), stream);
     if (st != UZIP_OK) return st;
     table = t;
   }

@@ -885,7 +885,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   uint8_t *stage = smem + a.pass2_off;
   uint16_t *stage16 = (uint16_t *)(stage + kStageHead);
   const uint32_t lane = lane_id();
-  uint16_t *ovf = SMALL ? a.slots + (uint64_t)blockIdx.x * a.slot_words : nullptr;
+  uint16_t *ovf = !REDUCE ? a.slots + (uint64_t)blockIdx.x * a.slot_words : nullptr;
   typedef __attribute__((address_space(3))) uint16_t lds16_t;
   // one private 4-byte slot per lane for words that are not emitted
   lds16_t *trash = (lds16_t *)smem_base + 2 * lane;
@@ -1164,8 +1164,44 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         }
         if (gi > 0) shift_up(S);
       }
+    } else if constexpr (!REDUCE) {
+      // larger blocks: the block re-read backwards, four rounds ahead, and
+      // the LDS window sliding into the workgroup's slot as for small ones
+      constexpr int P = 4;
+      uint32_t pb[P][NW];
+      if (full > 0) {
+#pragma unroll
+        for (int u = 0; u < P; ++u)
+          load_round<E>(src_blk + (uint64_t)((int)full - 1 - u >= 0 ? (int)full - 1 - u : 0) * kRound * E, pb[u]);
+      }
+      for (int r0 = (int)full - 1; r0 >= 0 && !stored; r0 -= P) {
+#pragma unroll
+        for (int u = 0; u < P; ++u) {
+          const int r = r0 - u;
+          if (r >= 0 && !stored) {
+            if (pos < lo + kRound && lo > 0) {  // the LDS window is full: slide it down
+              const uint32_t x = lo < kSlideWords ? lo : kSlideWords;
+              slide_window((lds16_t *)stage16, ovf + lo, a.lds_words, x, pos - lo);
+              lo -= x;
+              spilled = lo + a.lds_words;
+              lds_rel = (lds16_t *)stage16 - lo;
+            }
+            Group gr;
+            split_group<DT>(pb[u], gr);
+            // round r - P into the buffer just used (round 0 again once below it)
+            const int rn = r - P;
+            load_round<E>(src_blk + (uint64_t)(rn >= 0 ? rn : 0) * kRound * E, pb[u]);
+            uint4 e[8];
+#pragma unroll
+            for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
+            enc_round<true>(x, e, 8, pos, lds_rel, trash);
+            if (a.wcap - pos >= limit_words) stored = true;
+          }
+        }
+      }
     } else {
-      // re-read the block backwards, one round ahead
+      // the fused reduce's coding pass: the reduced block re-read backwards,
+      // one round ahead; its staging area holds the whole block's words
       uint32_t wa[NW], wbuf[NW];
       if (full > 0) load_round<E>(src_blk + (uint64_t)(full - 1) * kRound * E, wa);
       int r = (int)full - 1;
@@ -1223,7 +1259,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     f.lds_bytes = hdr + 2 * (spilled - pos);
     f.slot_delta = 2 * spilled - f.lds_bytes;
     f.stored = stored;
-    f.spilled = SMALL && spilled != a.wcap;
+    f.spilled = !REDUCE && spilled != a.wcap;
     f.last = last_in_chunk;
     if (!stored) {
       // header bytes right before the words: states | bitmap | f[k] (states
@@ -2165,24 +2201,27 @@ uint64_t max_size(uint32_t E, uint64_t n, uint32_t block_elems) {
 }
 
 constexpr uint32_t kSmallMaxElems = kRegRounds * kRound;  // symbols fit the register store
-constexpr uint32_t kSmallStageWords = 7424;                // LDS staging words, small blocks
-constexpr uint32_t kMaxSlots = 2048;                        // persistent workgroups (small blocks)
+constexpr uint32_t kSmallStageWords = 7424;                // LDS staging window (words), compress
+constexpr uint32_t kMaxSlots = 2048;                        // persistent workgroups, compress
 
 bool small_path(uint32_t block_elems) { return block_elems <= kSmallMaxElems; }
 uint32_t word_cap(uint32_t block_elems) { return block_elems / 2 + kRound + 8; }
 uint32_t stage_words(uint32_t block_elems) {
   const uint32_t w = word_cap(block_elems);
-  return small_path(block_elems) && w > kSmallStageWords ? kSmallStageWords : w;
+  return w > kSmallStageWords ? kSmallStageWords : w;
 }
 uint32_t slot_words(uint32_t block_elems) { return (word_cap(block_elems) + 127u) & ~127u; }
+// overflow slots of a compress (the fused reduce's coding pass has none)
 uint64_t n_slots(uint64_t n_blocks, uint32_t block_elems) {
-  return small_path(block_elems) ? (n_blocks < kMaxSlots ? n_blocks : kMaxSlots) : 0;
+  (void)block_elems;
+  return n_blocks < kMaxSlots ? n_blocks : kMaxSlots;
 }
 
-// LDS bytes of encode_kernel
-uint32_t encode_lds(uint32_t block_elems, bool small) {
+// LDS bytes of encode_kernel (windowed: compress; otherwise the fused
+// reduce's coding pass, which stages a whole block)
+uint32_t encode_lds(uint32_t block_elems, bool windowed) {
   const uint32_t pass1 = kHistBytes;
-  const uint32_t pass2 = kStageHead + 2 * (small ? stage_words(block_elems) : word_cap(block_elems)) + kStageTail;
+  const uint32_t pass2 = kStageHead + 2 * (windowed ? stage_words(block_elems) : word_cap(block_elems)) + kStageTail;
   return kTrashBytes + kEncTableBytes + (pass1 > pass2 ? pass1 : pass2);
 }
 
@@ -2259,9 +2298,9 @@ uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws
   a.slots = (uint16_t *)(ws + w.slot_off);
   a.slot_words = slot_words(a.block_elems);
   a.wcap = word_cap(a.block_elems);
-  a.lds_words = small ? stage_words(a.block_elems) : a.wcap;
+  a.lds_words = reduce ? a.wcap : stage_words(a.block_elems);
   a.pass2_off = kEncTableBytes;
-  const uint32_t lds = encode_lds(a.block_elems, small);
+  const uint32_t lds = encode_lds(a.block_elems, !reduce);
   if (lds > 160 * 1024) return UZIP_EINVAL;
   const void *fn = reduce ? reduce_kernel_ptr((int)dt)
                    : shared ? shared_kernel_ptr((int)dt * 4 + (a.flags != nullptr ? 2 : 0) + (small ? 1 : 0))
@@ -2270,7 +2309,7 @@ uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, 64, lds) != hipSuccess || occ < 1) occ = 1;
   uint64_t grid = (uint64_t)info.cus * (uint64_t)occ;
   if (grid > a.n_blocks) grid = a.n_blocks;
-  if (small && grid > n_slots(a.n_blocks, a.block_elems)) grid = n_slots(a.n_blocks, a.block_elems);
+  if (!reduce && grid > n_slots(a.n_blocks, a.block_elems)) grid = n_slots(a.n_blocks, a.block_elems);
   if (grid == 0) grid = 1;
   const uint64_t clear_words = w.slot_off / 4;
   const uint64_t cgrid = (clear_words + 255) / 256 < 4096 ? (clear_words + 255) / 256 : 4096;

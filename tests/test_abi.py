@@ -73,8 +73,8 @@ def test_invalid_arguments_rejected_on_host():
 def test_workspace_sizes_are_bounded():
     """The workspace is a status word per block, plus a fixed pool of
     per-workgroup overflow slots for words that leave the LDS staging window
-    (2048 slots, each the worst-case word count of one 64 KiB block: about
-    34 KiB), plus the reduced tensor when the fused reduce has no caller
+    (2048 slots, each the worst-case word count of one block: about 34 KiB
+    for 64 KiB blocks), plus the reduced tensor when the fused reduce has no caller
     buffer for it.  For 1 GiB of bf16 that is about 70 MB, below the ~164 MB
     compressor footprint section 4.1 reports."""
     import paper_2604_17172_amd as uz
@@ -89,9 +89,13 @@ def test_workspace_sizes_are_bounded():
     assert ws2 - ws <= 8 * nb + 512
     wsc = uz.uzip_workspace_size(uz.OP_CHUNKED, 0, n, 65536, 4 << 20)
     assert 0 < wsc <= ws + 16 * (n // (2 << 20)) + 1024
-    # large blocks stage everything in LDS: no slots
+    # larger blocks slide the same LDS window into slots of their own worst
+    # case: at most 2048 of them whatever the tensor size
     wl = uz.uzip_workspace_size(uz.OP_COMPRESS, 2, 1 << 28, 262144)
-    assert wl <= 8 * ((1 << 28) // 65536) + 1024
+    lslot = 2 * ((65536 // 2 + 512 + 8 + 127) & ~127)
+    assert wl <= 8 * ((1 << 28) // 65536) + 2048 * lslot + 4096
+    assert wl < 164e6
+    assert uz.uzip_workspace_size(uz.OP_COMPRESS, 2, 1 << 29, 262144) - wl <= 8 * ((1 << 28) // 65536) + 512
     wr = uz.uzip_workspace_size(uz.OP_REDUCE, 0, 1 << 23, 65536, 8 | uz.WS_NO_OUT_RAW)
     assert wr >= 2 * (1 << 23)
 

@@ -422,3 +422,39 @@ def test_high_entropy_blocks_spill_staging(uz, dtype, spread):
         e = rng.integers(1, spread + 1, n)
         x = ((e << 10) | rng.integers(0, 1024, n) | (rng.integers(0, 2, n) << 15)).astype(np.uint16)
     check_roundtrip(uz, x, dtype, 65536, f"spread {spread}")
+
+
+# --------------------------------------------- tables whose largest counts tie
+# Blocks whose maximal exponent counts tie and whose table remainder is
+# nonzero (the remainder goes to the smallest tied symbol; the closed forms
+# are in test_oracle_ties.py): the GPU's table must match the oracle's.
+TIE_BLOCKS = [{120: 12000, 121: 12000, 122: 8768},
+              {100: 2768, 125: 10000, 130: 10000, 140: 10000},
+              {60: 16384, 61: 16384},
+              {7: 6000, 8: 6000, 9: 6000, 10: 6000, 11: 6000, 12: 2768}]
+
+
+def test_tied_block_tables_bf16(uz):
+    x = np.concatenate([W.exponent_multiset(c, "bf16", seed=40 + i) for i, c in enumerate(TIE_BLOCKS)])
+    x = np.concatenate([x, W.normal_bf16(20_000, seed=44)])
+    check_roundtrip(uz, x, "bf16", 65536, "tied maxima, 64 KiB blocks")
+    check_roundtrip(uz, x, "bf16", 16384, "tied maxima, 16 KiB blocks")
+
+
+def test_tied_block_table_fp32(uz):
+    x = np.concatenate([W.exponent_multiset({3: 224, 126: 400, 127: 400}, "fp32", seed=45 + i) for i in range(9)])
+    check_roundtrip(uz, x, "fp32", 4096, "tied maxima, fp32 4 KiB blocks")
+
+
+def test_tied_stream_wide_table(uz):
+    x = W.exponent_multiset({120: 50000, 121: 50000, 122: 31072}, "bf16", seed=33)
+    x = np.concatenate([x, W.normal_bf16(70_000, seed=46)])
+    say(f"[parity] sampled table with tied maxima: n={x.size}")
+    want = ref.compress_table(x, "bf16", 65536, "sampled")
+    out, size = uz.compress_table(to_dev_bits(x, "bf16"), 65536, "sampled", dtype="bf16")
+    torch.cuda.synchronize()
+    got = out[: int(size.item())].cpu().numpy()
+    assert np.array_equal(got, want)
+    tab = uz.build_table(to_dev_bits(x, "bf16"), dtype="bf16")
+    torch.cuda.synchronize()
+    assert np.array_equal(tab.cpu().numpy().view(np.uint16).astype(np.uint32), ref.sampled_table(x, "bf16"))

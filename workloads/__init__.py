@@ -111,6 +111,26 @@ def random_bits(n: int, bits: int, seed: int = 12) -> np.ndarray:
     return _pieces(n, fn, np.empty(n, dt))
 
 
+# IEEE layouts (exponent bits, fraction bits) of the types whose exponent
+# field is exactly 8 bits wide
+_EXP8 = {"bf16": (16, 7), "fp32": (32, 23)}
+
+
+def exponent_multiset(counts: dict, dtype: str = "bf16", seed: int = 21) -> np.ndarray:
+    """Values whose biased exponent fields form the given multiset
+    ({exponent: count}), with uniformly random signs and fractions, in a
+    seeded random order.  bf16 or fp32 bit patterns."""
+    bits, fbits = _EXP8[dtype]
+    dt = np.uint16 if bits == 16 else np.uint32
+    rng = _rng(seed, 0)
+    exps = np.concatenate([np.full(c, e, np.uint64) for e, c in sorted(counts.items())])
+    rng.shuffle(exps)
+    n = exps.size
+    sign = rng.integers(0, 2, n, dtype=np.uint64)
+    frac = rng.integers(0, 1 << fbits, n, dtype=np.uint64)
+    return ((sign << (bits - 1)) | (exps << fbits) | frac).astype(dt)
+
+
 # --------------------------------------------------------------------------
 # weight_sync: 1 GiB bf16 buffer shaped like a 0.5B-parameter transformer
 # --------------------------------------------------------------------------

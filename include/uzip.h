@@ -48,6 +48,16 @@
  *     Device-side errors (corrupt streams) are written to *d_status (the
  *     first error wins; the caller zeroes it before the call).  No call
  *     writes outside [d_out, d_out + out_cap) or its workspace.
+ *   - Encoder failure.  The compressing calls place each block's section
+ *     with a single-pass scan in which a block waits, for a bounded number
+ *     of polls (2^22, a few seconds), for the sizes of earlier blocks that other
+ *     workgroups are coding.  Such a wait always ends when the GPU runs
+ *     the call alone; if it runs out (the GPU shared with work that holds
+ *     its compute units for longer), the stream is marked invalid: its
+ *     magic and its size (*d_out_size, chunk_sizes[c]) read 0 -- a valid
+ *     stream is never shorter than its 32-byte header -- the split-send
+ *     producer still raises the chunk's DONE flag, and the fused reduce
+ *     also sets *d_status to UZIP_ETIMEOUT.  The call may be repeated.
  */
 #ifndef UZIP_H
 #define UZIP_H
@@ -82,7 +92,9 @@ typedef enum {
   UZIP_ENOSPC = -2,      /* output capacity or workspace too small */
   UZIP_ECORRUPT = -3,    /* device status: stream corrupt or not matching the call */
   UZIP_EHIP = -4,        /* a HIP runtime call failed */
-  UZIP_EUNSUPPORTED = -5 /* the device is not gfx950 */
+  UZIP_EUNSUPPORTED = -5, /* the device is not gfx950 */
+  UZIP_ETIMEOUT = -6      /* device status: the encoder's bounded wait for an
+                             earlier block's size ran out; the stream is invalid */
 } uzip_status;
 
 /* operation codes for uzip_workspace_size */
@@ -141,9 +153,9 @@ uzip_status uzip_compress(const void *d_in, uint64_t n_elems, uzip_dtype dtype,
  *   d_out, out_cap: n_elems values, out_cap >= n_elems * element size.
  *   d_status:       device u32, set to UZIP_ECORRUPT if the stream is
  *                   corrupt or does not match (may be NULL).
- *   d_ws, ws_bytes: device workspace of uzip_workspace_size(
- *                   UZIP_OP_DECOMPRESS, ...) bytes (256, reserved: the
- *                   decoder keeps no state there), 16-byte aligned.
+ *   d_ws, ws_bytes: ignored (the decoder keeps no state in a workspace;
+ *                   uzip_workspace_size(UZIP_OP_DECOMPRESS, ...) is 256
+ *                   bytes, reserved); may be NULL.
  * Errors: EINVAL, ENOSPC, EHIP, EUNSUPPORTED. */
 uzip_status uzip_decompress(const void *d_in, size_t in_bytes, uzip_dtype dtype,
                             uint64_t n_elems, void *d_out, size_t out_cap,
@@ -234,6 +246,16 @@ uzip_status uzip_compress_chunked(const void *d_in, uint64_t n_elems, uzip_dtype
 
 /* Static string naming a status code. */
 const char *uzip_status_str(uzip_status status);
+
+/* Fault injection, for tests of the encoder's failure path (see the
+ * conventions above): calls enqueued after it bound the single-pass scan's
+ * wait at spin_limit polls (0 restores the default, 2^22), and the block
+ * with the global index held_block (counted over all chunks of a call;
+ * UINT32_MAX: none) never publishes its size, so every later block of its
+ * stream waits until its bound runs out and the stream is marked invalid;
+ * every kernel still ends normally.  Process-wide; not for production use.
+ * Errors: none (returns UZIP_OK). */
+uzip_status uzip_inject_scan_stall(uint32_t spin_limit, uint32_t held_block);
 
 #ifdef __cplusplus
 }

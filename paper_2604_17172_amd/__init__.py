@@ -32,7 +32,7 @@ OP_COMPRESS, OP_DECOMPRESS, OP_REDUCE, OP_CHUNKED, OP_COMPRESS_TABLE, OP_CHUNKED
 TABLE_PER_BLOCK, TABLE_SAMPLED, TABLE_EXTERNAL = 0, 1, 2
 TABLE_BYTES = 512
 WS_NO_OUT_RAW = 1 << 16
-OK, EINVAL, ENOSPC, ECORRUPT, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+OK, EINVAL, ENOSPC, ECORRUPT, EHIP, EUNSUPPORTED, ETIMEOUT = 0, -1, -2, -3, -4, -5, -6
 
 _c = ctypes
 _vp, _u32, _u64, _sz, _int = _c.c_void_p, _c.c_uint32, _c.c_uint64, _c.c_size_t, _c.c_int
@@ -61,10 +61,13 @@ _lib.uzip_decompress_table.argtypes = [_vp, _sz, _int, _u64, _vp, _vp, _sz, _vp,
 _lib.uzip_decompress_table.restype = _int
 _lib.uzip_status_str.argtypes = [_int]
 _lib.uzip_status_str.restype = _c.c_char_p
+_lib.uzip_inject_scan_stall.argtypes = [_u32, _u32]
+_lib.uzip_inject_scan_stall.restype = _int
 
 EXPORTED = ["uzip_max_compressed_size", "uzip_workspace_size", "uzip_compress", "uzip_decompress",
             "uzip_reduce_fused", "uzip_compress_chunked", "uzip_status_str", "uzip_build_table",
-            "uzip_compress_table", "uzip_decompress_table", "uzip_compress_chunked_table"]
+            "uzip_compress_table", "uzip_decompress_table", "uzip_compress_chunked_table",
+            "uzip_inject_scan_stall"]
 
 
 class UzipError(RuntimeError):
@@ -130,6 +133,10 @@ def uzip_status_str(status: int) -> str:
     return _lib.uzip_status_str(status).decode()
 
 
+def uzip_inject_scan_stall(spin_limit: int, held_block: int) -> int:
+    return _lib.uzip_inject_scan_stall(spin_limit, held_block)
+
+
 # ---------------------------------------------------------------- torch helpers
 # FP8 formats are coded in pairs: one element is a 16-bit unit of two values
 _TORCH_DTYPE = {torch.bfloat16: BF16, torch.float16: FP16, torch.float32: FP32,
@@ -170,11 +177,22 @@ def _dev_empty(nbytes: int, device) -> torch.Tensor:
     return torch.empty(max(int(nbytes), 16), dtype=torch.uint8, device=device)
 
 
+def check_sizes(sizes: torch.Tensor, what: str) -> None:
+    """Wait for the stream's work and raise if an encoder call marked a
+    stream invalid (its size reads 0: the bounded wait of the single-pass
+    scan ran out)."""
+    torch.cuda.current_stream(sizes.device).synchronize()
+    if bool((sizes == 0).any()):
+        raise UzipError(ETIMEOUT, what)
+
+
 def compress(x: torch.Tensor, block_bytes: int = 65536, dtype=None, out: torch.Tensor | None = None,
-             ws: torch.Tensor | None = None, stream=None):
+             ws: torch.Tensor | None = None, stream=None, check: bool = False):
     """Compress a contiguous CUDA tensor (bf16/fp16/fp32/float8, or an
     int16/int32 bit view with ``dtype`` given; float8 tensors are coded as
-    pairs of values).  Returns (stream buffer, device u64 size)."""
+    pairs of values).  Returns (stream buffer, device u64 size).  With
+    ``check`` the call waits for the GPU and raises UzipError(ETIMEOUT) if
+    the stream was marked invalid (size 0)."""
     assert x.is_cuda and x.is_contiguous()
     dt = dtype_code(dtype if dtype is not None else x.dtype)
     n = _n_elems(x, dt)
@@ -189,6 +207,8 @@ def compress(x: torch.Tensor, block_bytes: int = 65536, dtype=None, out: torch.T
     size = torch.zeros(1, dtype=torch.int64, device=x.device)
     _check(uzip_compress(x.data_ptr() if n else None, n, dt, block_bytes, out.data_ptr(), out.numel(),
                          size.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream)), "uzip_compress")
+    if check:
+        check_sizes(size, "uzip_compress")
     return out, size
 
 
@@ -212,9 +232,11 @@ def decompress(s: torch.Tensor, dtype, n_elems: int, out: torch.Tensor | None = 
 
 def reduce_fused(streams, dtype, n_elems: int, block_bytes: int = 65536, local: torch.Tensor | None = None,
                  want_raw: bool = True, in_bytes=None, out: torch.Tensor | None = None,
-                 ws: torch.Tensor | None = None, stream=None):
+                 ws: torch.Tensor | None = None, stream=None, check: bool = False):
     """Fused decompress -> fp32 reduce -> recompress.  Returns
-    (stream buffer, device u64 size, reduced tensor or None, device status)."""
+    (stream buffer, device u64 size, reduced tensor or None, device status).
+    With ``check`` the call waits for the GPU and raises UzipError with the
+    device status (ECORRUPT, ETIMEOUT) if it is not OK."""
     dt = dtype_code(dtype)
     dev = streams[0].device
     cap = uzip_max_compressed_size(dt, n_elems, block_bytes)
@@ -233,14 +255,18 @@ def reduce_fused(streams, dtype, n_elems: int, block_bytes: int = 65536, local: 
                              out.data_ptr(), out.numel(), size.data_ptr(),
                              raw.data_ptr() if raw is not None and n_elems else None, status.data_ptr(),
                              ws.data_ptr(), ws.numel(), _stream(stream)), "uzip_reduce_fused")
+    if check:
+        torch.cuda.current_stream(dev).synchronize()
+        _check(int(status.item()), "uzip_reduce_fused")
     return out, size, raw, status
 
 
 def compress_chunked(x: torch.Tensor, block_bytes: int, chunk_bytes: int, dtype=None, epoch: int = 1,
                      flags: torch.Tensor | None = None, out: torch.Tensor | None = None,
-                     ws: torch.Tensor | None = None, stream=None):
+                     ws: torch.Tensor | None = None, stream=None, check: bool = False):
     """Split-send producer.  Returns (buffer of n_chunks slots, slot_bytes,
-    device u64 chunk sizes, flags [2 n_chunks] u32)."""
+    device u64 chunk sizes, flags [2 n_chunks] u32).  ``check`` as for
+    ``compress`` (any chunk of size 0)."""
     assert x.is_cuda and x.is_contiguous()
     dt = dtype_code(dtype if dtype is not None else x.dtype)
     n = _n_elems(x, dt)
@@ -260,6 +286,8 @@ def compress_chunked(x: torch.Tensor, block_bytes: int, chunk_bytes: int, dtype=
     _check(uzip_compress_chunked(x.data_ptr() if n else None, n, dt, block_bytes, chunk_bytes, out.data_ptr(),
                                  slot, sizes.data_ptr(), flags.data_ptr(), epoch, ws.data_ptr(), ws.numel(),
                                  _stream(stream)), "uzip_compress_chunked")
+    if check and chunks:
+        check_sizes(sizes[:chunks], "uzip_compress_chunked")
     return out, slot, sizes, flags
 
 

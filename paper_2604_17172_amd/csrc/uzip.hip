@@ -39,6 +39,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <atomic>
 #include <mutex>
 
 #include "../../include/uzip.h"
@@ -82,6 +83,14 @@ struct EncodeArgs {
   uint32_t table_stride;  // u16 entries between the tables of consecutive streams (0: one table for all)
   uint32_t table_mode;
   uint32_t table_bytes;
+  // error channel: the single-pass scan's bounded wait (polls), a block that
+  // never publishes its length (fault injection; ~0u: none), the caller's
+  // device status (fused reduce; may be null) and the workspace counter of
+  // workgroups that have finished
+  uint32_t spin_limit;
+  uint32_t hold_block;
+  uint32_t *dstatus;
+  uint32_t *exit_cnt;
 };
 
 constexpr size_t kDecodeWsBytes = 256;   // reserved: the decoder keeps no state there
@@ -175,6 +184,14 @@ template <bool SYS>
 __device__ __forceinline__ void out64(uint8_t *p, uint32_t lo, uint32_t hi) {
   if (SYS) __hip_atomic_store((uint64_t *)p, (uint64_t)hi << 32 | lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   else *(uint2 *)p = make_uint2(lo, hi);
+}
+// Header and size words: atomic stores written through the L2 at agent
+// scope (system scope for the split-send producer), so that a later store of
+// finish_launch to the same words, from any XCD, is the one that stays.
+template <bool SYS>
+__device__ __forceinline__ void coh64(uint64_t *p, uint64_t v) {
+  if (SYS) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  else __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 template <bool SYS>
 __device__ __forceinline__ void out128(uint8_t *p, uint4 v) {
@@ -449,11 +466,14 @@ __device__ void enc_entries(const Table &t, uint4 *enc) {
 // (16-byte units) from its predecessors' states.  Between the two a wave may
 // do other work: a wait is only ever for an aggregate, which every taken
 // block publishes without waiting, and blocks are taken in ticket order, so
-// the wait always ends; the spin is bounded anyway, and a wait that runs out
-// raises the workspace error word instead of hanging.
+// the wait always ends.  The spin is bounded anyway (a wave of an earlier
+// block may be descheduled for long on a shared GPU): a wait that runs out
+// returns `failed`, and the launch then marks the stream invalid instead of
+// hanging (finish_launch).
 constexpr uint32_t kSpinLimit = 1u << 22;
-__device__ __forceinline__ void publish_aggregate(uint64_t *status, uint32_t b, uint32_t first, uint64_t len16) {
-  if (lane_id() == 0)
+__device__ __forceinline__ void publish_aggregate(uint64_t *status, uint32_t b, uint32_t first, uint64_t len16,
+                                                  uint32_t hold) {
+  if (lane_id() == 0 && b != hold)
     __hip_atomic_store(&status[b], (b == first ? kFlagInclusive : kFlagAggregate) | len16, __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -472,9 +492,13 @@ __device__ inline uint64_t wave_excl_scan64(uint64_t v) {
 // Resolves block b's exclusive prefix and publishes its inclusive one.  The
 // nearest predecessors (up to 64) that had only published their length get
 // their inclusive prefix too, the same value their own look-back publishes:
-// later blocks then find an inclusive prefix close by.
-__device__ uint64_t resolve_prefix(uint64_t *status, uint32_t b, uint32_t first, uint64_t len16, uint32_t *err) {
+// later blocks then find an inclusive prefix close by.  A wait that runs out
+// after spin_limit polls sets `failed` (uniform) and the error word and
+// publishes nothing; the held block (fault injection) publishes nothing.
+__device__ uint64_t resolve_prefix(uint64_t *status, uint32_t b, uint32_t first, uint64_t len16,
+                                   uint32_t spin_limit, uint32_t hold, uint32_t *err, bool &failed) {
   const uint32_t lane = lane_id();
+  failed = false;
   if (b == first) return 0;
   uint64_t excl = 0, near_v = 0;
   bool near_agg = false, near = true;
@@ -489,11 +513,12 @@ __device__ uint64_t resolve_prefix(uint64_t *status, uint32_t b, uint32_t first,
     const uint64_t upto = inc ? ((inc & (~inc + 1)) << 1) - 1 : ~0ull;  // lanes up to the first inclusive
     const uint64_t notready = __ballot(flag == 0) & upto;
     if (notready) {
-      if (++spins < kSpinLimit) {
+      if (++spins < spin_limit) {
         __builtin_amdgcn_s_sleep(2);
         continue;
       }
       if (lane == 0) __hip_atomic_store(err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      failed = true;
       return excl;
     }
     const bool mine = (upto >> lane) & 1;
@@ -507,6 +532,7 @@ __device__ uint64_t resolve_prefix(uint64_t *status, uint32_t b, uint32_t first,
     if (inc) break;
     look -= 64;
   }
+  if (b == hold) return excl;
   if (lane == 0)
     __hip_atomic_store(&status[b], kFlagInclusive | (excl + len16), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   // lane l of the nearest window is block b-1-l: its inclusive prefix is
@@ -524,7 +550,12 @@ __device__ uint64_t resolve_prefix(uint64_t *status, uint32_t b, uint32_t first,
 // before the count; the count is a system-scope atomic at the memory, so the
 // block that completes it stores the flag after every block's bytes are in
 // memory.
-__device__ void publish_chunk(uint32_t *cnt, uint32_t need, uint32_t *flag, uint32_t epoch) {
+// A block whose look-back failed first sets the counter's top bit (block
+// counts stay below 2^31), so no later count can equal `need` and the flag
+// is left to finish_launch, which raises it over a zero size.
+constexpr uint32_t kChunkFailed = 0x80000000u;
+__device__ void publish_chunk(uint32_t *cnt, uint32_t need, uint32_t *flag, uint32_t epoch, bool failed = false) {
+  if (failed && lane_id() == 0) __hip_atomic_fetch_or(cnt, kChunkFailed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   __builtin_amdgcn_s_waitcnt(0);
   if (lane_id() == 0 && __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) + 1 == need)
     __hip_atomic_store(flag, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
@@ -611,6 +642,11 @@ __device__ __forceinline__ void enc_round(uint32_t &x, const uint4 (&e)[8], uint
 // the workgroup's overflow slot and the rest, from the 16-byte unit holding
 // pos up, moves up by x: the window then covers [lo - x, lo - x + cap).
 constexpr uint32_t kSlideWords = 2048;
+// A window slide moves indices of at least lo + cap - x >= cap (x <= lo)
+// out, so a slot holds [lds_words, wcap).  The copy-out reads the 16-byte
+// units around the LDS/slot seam and one unit past the last word: a slot
+// has kSlotLead words before the first index and kSlotTail after the last.
+constexpr uint32_t kSlotLead = 8, kSlotTail = 16;
 __device__ __forceinline__ void slide_window(__attribute__((address_space(3))) uint16_t *win, uint16_t *ovf_lo,
                                              uint32_t cap, uint32_t x, uint32_t pos_rel) {
   typedef uint32_t v4u __attribute__((ext_vector_type(4)));
@@ -775,7 +811,9 @@ __device__ __forceinline__ void finish_block(const EncodeArgs &a, const Fin &f, 
   constexpr int E = (DT == 2) ? 4 : 2;
   constexpr int NW = 4 * (E / 2);
   const uint32_t lane = lane_id();
-  const uint64_t excl = resolve_prefix(a.status, f.b, f.first_block, f.sec_len / 16, a.ticket + 1);
+  bool failed;
+  const uint64_t excl =
+      resolve_prefix(a.status, f.b, f.first_block, f.sec_len / 16, a.spin_limit, a.hold_block, a.ticket + 1, failed);
   uint8_t *sec = f.sout + f.coded_off + 16 * excl;
   if (lane == 0)
     out32<SYS>((uint32_t *)(f.sout + kHeaderBytes + 4 * f.lb),
@@ -847,19 +885,46 @@ __device__ __forceinline__ void finish_block(const EncodeArgs &a, const Fin &f, 
       hh[5] = (uint32_t)(f.chunk_n >> 32);
       hh[6] = (uint32_t)total;
       hh[7] = (uint32_t)(total >> 32);
-      uint4 *hp = (uint4 *)f.sout;
-      out128<SYS>((uint8_t *)hp, make_uint4(hh[0], hh[1], hh[2], hh[3]));
-      out128<SYS>((uint8_t *)(hp + 1), make_uint4(hh[4], hh[5], hh[6], hh[7]));
-      if (a.sizes != nullptr) {
-        if (SYS) __hip_atomic_store(&a.sizes[f.chunk], total, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-        else a.sizes[f.chunk] = total;
-      }
+      uint64_t *hp = (uint64_t *)f.sout;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) coh64<SYS>(hp + q, (uint64_t)hh[2 * q + 1] << 32 | hh[2 * q]);
+      if (a.sizes != nullptr) coh64<SYS>(&a.sizes[f.chunk], total);
     }
     // zero padding after the directory
     const uint64_t db = kHeaderBytes + 4ull * f.n_blocks + lane;
     if (lane < 16 && db < f.dir_end) out8<SYS>(f.sout + db, 0);
   }
-  if (a.flags != nullptr) publish_chunk(&a.chunk_cnt[2 * f.chunk + 1], f.n_blocks, &a.flags[2 * f.chunk + 1], a.epoch);
+  if (a.flags != nullptr)
+    publish_chunk(&a.chunk_cnt[2 * f.chunk + 1], f.n_blocks, &a.flags[2 * f.chunk + 1], a.epoch, failed);
+}
+
+// End of a persistent encoder workgroup.  The last one out (its stores and
+// every other workgroup's complete: each waits for its own before counting
+// itself) marks every stream that had a failed look-back invalid: magic and
+// size 0 -- a stream is never shorter than its 32-byte header, so a zero
+// size is the error -- the split-send producer's DONE flag raised over it,
+// and the fused reduce's status set.
+template <bool SYS>
+__device__ void finish_launch(const EncodeArgs &a) {
+  const uint32_t lane = lane_id();
+  __builtin_amdgcn_s_waitcnt(0);
+  uint32_t last = 0;
+  if (lane == 0) last = __hip_atomic_fetch_add(a.exit_cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1 == gridDim.x;
+  if (!uniform(last)) return;
+  if (__hip_atomic_load(a.ticket + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) return;
+  const uint32_t streams = (a.n_blocks + a.blocks_per_chunk - 1) / a.blocks_per_chunk;
+  for (uint32_t c = lane; c < streams; c += 64) {
+    const bool bad = a.flags == nullptr ||
+                     (__hip_atomic_load(&a.chunk_cnt[2 * c + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) & kChunkFailed);
+    if (!bad) continue;
+    coh64<SYS>((uint64_t *)(a.out + (uint64_t)c * a.slot_bytes), 0);
+    if (a.sizes != nullptr) coh64<SYS>(&a.sizes[c], 0);
+    if (a.flags != nullptr) {
+      __builtin_amdgcn_s_waitcnt(0);
+      __hip_atomic_store(&a.flags[2 * c + 1], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+  }
+  if (lane == 0) report(a.dstatus, UZIP_ETIMEOUT);
 }
 
 // ---------------------------------------------------------------------------
@@ -885,7 +950,10 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   uint8_t *stage = smem + a.pass2_off;
   uint16_t *stage16 = (uint16_t *)(stage + kStageHead);
   const uint32_t lane = lane_id();
-  uint16_t *ovf = !REDUCE ? a.slots + (uint64_t)blockIdx.x * a.slot_words : nullptr;
+  // the workgroup's overflow slot holds the staging indices that can leave
+  // the LDS window, [lds_words, wcap), after kSlotLead words of margin:
+  // ovf[v] is index v
+  uint16_t *ovf = !REDUCE ? a.slots + (uint64_t)blockIdx.x * a.slot_words + kSlotLead - a.lds_words : nullptr;
   typedef __attribute__((address_space(3))) uint16_t lds16_t;
   // one private 4-byte slot per lane for words that are not emitted
   lds16_t *trash = (lds16_t *)smem_base + 2 * lane;
@@ -1286,7 +1354,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
       if (f.spilled) __threadfence_block();
     }
     __syncthreads();
-    publish_aggregate(a.status, b, first_block, sec_len / 16);
+    publish_aggregate(a.status, b, first_block, sec_len / 16, a.hold_block);
     if constexpr (DEFER) {
       pend = f;
       have_pend = true;
@@ -1305,10 +1373,12 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
 template <int DT, bool SMALL, bool SYS, bool SHARED = false>
 __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) encode_kernel(EncodeArgs a) {
   encode_body<DT, false, SMALL, SYS, SHARED>(a);
+  finish_launch<SYS>(a);
 }
 template <int DT>
 __global__ void __launch_bounds__(64) reduce_kernel(EncodeArgs a) {
   encode_body<DT, true, false, false>(a);
+  finish_launch<false>(a);
 }
 
 // ---------------------------------------------------------------------------
@@ -2150,6 +2220,10 @@ struct DeviceInfo {
   bool gfx950 = false;
 };
 
+// fault injection (uzip_inject_scan_stall)
+std::atomic<uint32_t> g_spin_limit{kSpinLimit};
+std::atomic<uint32_t> g_hold_block{~0u};
+
 constexpr int kMaxDevices = 64;
 DeviceInfo g_info[kMaxDevices];
 std::once_flag g_once[kMaxDevices];
@@ -2210,8 +2284,14 @@ uint32_t stage_words(uint32_t block_elems) {
   const uint32_t w = word_cap(block_elems);
   return w > kSmallStageWords ? kSmallStageWords : w;
 }
-uint32_t slot_words(uint32_t block_elems) { return (word_cap(block_elems) + 127u) & ~127u; }
-// overflow slots of a compress (the fused reduce's coding pass has none)
+// words of one overflow slot: the staging indices that can leave the LDS
+// window (none when the window holds a whole block's words)
+uint32_t slot_words(uint32_t block_elems) {
+  const uint32_t w = word_cap(block_elems), l = stage_words(block_elems);
+  return w > l ? (kSlotLead + (w - l) + kSlotTail + 127u) & ~127u : 0u;
+}
+// overflow slots of a compress (the fused reduce's coding pass has none):
+// one per persistent workgroup
 uint64_t n_slots(uint64_t n_blocks, uint32_t block_elems) {
   (void)block_elems;
   return n_blocks < kMaxSlots ? n_blocks : kMaxSlots;
@@ -2229,9 +2309,10 @@ struct EncodeWs {
   uint64_t status_off, cnt_off, slot_off, y_off, total;
 };
 
-// workspace: ticket + error word | look-back status per block | chunk
-// counters | overflow slots (small blocks) | reduced tensor (large-block
-// reduce without a caller buffer).  [0, slot_off) is cleared per call.
+// workspace: ticket, error word, exit counter | look-back status per block |
+// chunk counters | overflow slots (compress, blocks whose words can exceed
+// the LDS window) | reduced tensor (fused reduce without a caller buffer).
+// [0, slot_off) is cleared per call.
 EncodeWs encode_ws(uint64_t n_blocks, uint64_t n_chunks, uint32_t block_elems, uint64_t ybytes, bool reduce = false) {
   EncodeWs w;
   w.status_off = 256;
@@ -2292,7 +2373,10 @@ uzip_status launch_table_split(const void *d_in, uint64_t n, uzip_dtype dt, uint
 uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws, const EncodeWs &w,
                           const DeviceInfo &info, hipStream_t stream, bool shared = false) {
   const bool small = !reduce && small_path(a.block_elems);
-  a.ticket = (uint32_t *)ws;
+  a.ticket = (uint32_t *)ws;  // word 1: error word, word 2: exit counter
+  a.exit_cnt = (uint32_t *)ws + 2;
+  a.spin_limit = g_spin_limit.load(std::memory_order_relaxed);
+  a.hold_block = g_hold_block.load(std::memory_order_relaxed);
   a.status = (uint64_t *)(ws + w.status_off);
   a.chunk_cnt = (uint32_t *)(ws + w.cnt_off);
   a.slots = (uint16_t *)(ws + w.slot_off);
@@ -2471,7 +2555,8 @@ uzip_status launch_decode(const void *d_in, size_t in_bytes, uzip_dtype dtype, u
   if (d_table != nullptr && !aligned16(d_table)) return UZIP_EINVAL;
   if (n_elems > 0 && (d_out == nullptr || !aligned16(d_out))) return UZIP_EINVAL;
   if (out_cap < n_elems * elem_bytes(dtype)) return UZIP_ENOSPC;
-  if (d_ws == nullptr || !aligned16(d_ws) || ws_bytes < kDecodeWsBytes) return UZIP_EINVAL;
+  (void)d_ws;  // the decoder keeps no state in a workspace
+  (void)ws_bytes;
   DeviceInfo info;
   uzip_status st = device_info(info);
   if (st != UZIP_OK) return st;
@@ -2654,7 +2739,14 @@ uzip_status uzip_reduce_fused(const void *const *d_in, const size_t *in_bytes, i
   a.sizes = d_out_size;
   a.ybuf = ybuf;
   a.hist_in = (const uint32_t *)(ws + w.hist_off);
+  a.dstatus = d_status;
   return launch_encode(a, dtype, true, ws, w.enc, info, stream);
+}
+
+uzip_status uzip_inject_scan_stall(uint32_t spin_limit, uint32_t held_block) {
+  g_spin_limit.store(spin_limit ? spin_limit : kSpinLimit, std::memory_order_relaxed);
+  g_hold_block.store(held_block, std::memory_order_relaxed);
+  return UZIP_OK;
 }
 
 const char *uzip_status_str(uzip_status status) {
@@ -2665,6 +2757,7 @@ const char *uzip_status_str(uzip_status status) {
     case UZIP_ECORRUPT: return "corrupt or mismatched stream";
     case UZIP_EHIP: return "HIP runtime error";
     case UZIP_EUNSUPPORTED: return "device is not gfx950";
+    case UZIP_ETIMEOUT: return "encoder wait for an earlier block ran out; stream invalid";
     default: return "unknown status";
   }
 }

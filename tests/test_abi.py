@@ -47,9 +47,7 @@ def test_invalid_arguments_rejected_on_host():
     assert uz.uzip_compress(16, 1000, 0, 65536, 32, 100, None, 48, 1 << 20, None) == uz.ENOSPC
     assert uz.uzip_decompress(16, 100, 9, 10, 32, 100, None, None, 0, None) == uz.EINVAL
     assert uz.uzip_decompress(16, 100, 0, 1000, 32, 100, None, None, 0, None) == uz.ENOSPC
-    # the decoder's block counter lives in the workspace
-    assert uz.uzip_decompress(16, 100, 0, 10, 32, 100, None, None, 0, None) == uz.EINVAL
-    assert uz.uzip_decompress(16, 100, 0, 10, 32, 100, None, 48, 16, None) == uz.EINVAL
+    # the decoder keeps no state in a workspace: 256 reserved bytes, NULL accepted
     assert uz.uzip_workspace_size(uz.OP_DECOMPRESS, 0, 1 << 29, 65536, 0) == 256
     assert uz.uzip_reduce_fused([16] * 17, [64] * 17, 17, None, 0, 10, 65536, 32, 1 << 20, None, None,
                                 None, 48, 1 << 20, None) == uz.EINVAL
@@ -72,30 +70,34 @@ def test_invalid_arguments_rejected_on_host():
 
 def test_workspace_sizes_are_bounded():
     """The workspace is a status word per block, plus a fixed pool of
-    per-workgroup overflow slots for words that leave the LDS staging window
-    (2048 slots, each the worst-case word count of one block: about 34 KiB
-    for 64 KiB blocks), plus the reduced tensor when the fused reduce has no caller
-    buffer for it.  For 1 GiB of bf16 that is about 70 MB, below the ~164 MB
-    compressor footprint section 4.1 reports."""
+    per-workgroup overflow slots for the words of a block that can leave the
+    LDS staging window (at most 2048 slots whatever the tensor size; a slot
+    holds a block's worst-case word count less the window's 7424 words),
+    plus the reduced tensor when the fused reduce has no caller buffer for
+    it.  Section 4.1 reports a compressor footprint of about 164 MB (0.1% of
+    an H200's memory)."""
     import paper_2604_17172_amd as uz
     n = 1 << 29
     nb = n // 32768
     ws = uz.uzip_workspace_size(uz.OP_COMPRESS, 0, n, 65536)
-    slot = 2 * (32768 // 2 + 512 + 8 + 127)
-    assert 0 < ws <= 8 * nb + 2048 * slot + 4096
-    assert ws < 164e6
+    assert 0 < ws <= 8 * nb + 40e6            # 1 GiB bf16, 64 KiB blocks: 39.5 MB
     # the slot pool does not grow with the tensor
     ws2 = uz.uzip_workspace_size(uz.OP_COMPRESS, 0, 2 * n, 65536)
     assert ws2 - ws <= 8 * nb + 512
     wsc = uz.uzip_workspace_size(uz.OP_CHUNKED, 0, n, 65536, 4 << 20)
     assert 0 < wsc <= ws + 16 * (n // (2 << 20)) + 1024
-    # larger blocks slide the same LDS window into slots of their own worst
-    # case: at most 2048 of them whatever the tensor size
+    # blocks whose words fit the window need no slots at all
+    assert uz.uzip_workspace_size(uz.OP_COMPRESS, 0, n, 16384) <= 8 * (n // 8192) + 4096
+    # 256 KiB blocks: fp32 (65536 elements) 1 GiB, 106.6 MB
     wl = uz.uzip_workspace_size(uz.OP_COMPRESS, 2, 1 << 28, 262144)
-    lslot = 2 * ((65536 // 2 + 512 + 8 + 127) & ~127)
-    assert wl <= 8 * ((1 << 28) // 65536) + 2048 * lslot + 4096
-    assert wl < 164e6
+    assert wl <= 8 * ((1 << 28) // 65536) + 107e6 and wl < 164e6
     assert uz.uzip_workspace_size(uz.OP_COMPRESS, 2, 1 << 29, 262144) - wl <= 8 * ((1 << 28) // 65536) + 512
+    # 16-bit elements in 256 KiB blocks (131072 elements, up to 65536 words a
+    # block): 2048 slots of 117.5 KB, 241 MB -- 0.08% of the MI355X's 288 GB
+    for dt in (uz.BF16, uz.FP16, uz.E4M3FN):
+        wh = uz.uzip_workspace_size(uz.OP_COMPRESS, dt, 1 << 28, 262144)
+        assert wh <= 8 * ((1 << 28) // 131072) + 241e6 + 4096
+        assert uz.uzip_workspace_size(uz.OP_COMPRESS, dt, 1 << 30, 262144) - wh <= 8 * 3 * 2048 + 512
     wr = uz.uzip_workspace_size(uz.OP_REDUCE, 0, 1 << 23, 65536, 8 | uz.WS_NO_OUT_RAW)
     assert wr >= 2 * (1 << 23)
 
@@ -104,6 +106,9 @@ def test_status_strings():
     import paper_2604_17172_amd as uz
     assert uz.uzip_status_str(0) == "ok"
     assert "corrupt" in uz.uzip_status_str(uz.ECORRUPT)
+    assert "invalid" in uz.uzip_status_str(uz.ETIMEOUT)
+    # fault injection only stores settings on the host; restore the defaults
+    assert uz.uzip_inject_scan_stall(0, 0xFFFFFFFF) == uz.OK
     assert uz.uzip_status_str(123) == "unknown status"
 
 
@@ -128,4 +133,3 @@ def test_table_api_host_checks():
     assert uz.uzip_build_table(16, 100, 0, 24, None) == uz.EINVAL
     assert uz.uzip_build_table(16, 100, 9, 32, None) == uz.EINVAL
     assert uz.uzip_decompress_table(16, 100, 0, 10, 24, 32, 100, None, 48, 256, None) == uz.EINVAL
-    assert uz.uzip_decompress_table(16, 100, 0, 10, None, 32, 100, None, None, 0, None) == uz.EINVAL

@@ -226,6 +226,24 @@ uzip_status uzip_reduce_fused(const void *const *d_in, const size_t *in_bytes, i
                               uint64_t *d_out_size, void *d_out_raw, uint32_t *d_status,
                               void *d_ws, size_t ws_bytes, hipStream_t stream);
 
+/* uzip_compress for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the encoder's workspace is the library's own device scratch, a static
+ * array of 64 MiB that every GPU the library runs on holds from the
+ * library's first call on it until the process ends.  It holds the scan's
+ * counters and status words (8 bytes per block) and as many overflow slots
+ * as then fit (at most one per persistent workgroup; fewer only shrink the
+ * grid).  Each call clears what must start at zero with a kernel of its own
+ * (no memset).  Every call on one GPU shares that GPU's scratch: calls that
+ * overlap in time on one GPU race, so callers order them (one stream, or
+ * events).  The caller still provides d_in, d_out and d_out_size as for
+ * uzip_compress, and the stream bytes are the same.  Allocates nothing.
+ * Errors: EINVAL; ENOSPC (out_cap too small, or more than 4,194,304 blocks:
+ * the scratch's limit); EHIP; EUNSUPPORTED. */
+uzip_status uzip_compress_noalloc(const void *d_in, uint64_t n_elems, uzip_dtype dtype,
+                                  uint32_t block_bytes, void *d_out, size_t out_cap,
+                                  uint64_t *d_out_size, hipStream_t stream);
+
 /* Split-send producer (section 3.2.3): the tensor is cut into chunks of
  * chunk_bytes (a multiple of block_bytes); chunk c is compressed as an
  * independent stream at d_out + c * slot_bytes, byte-identical to

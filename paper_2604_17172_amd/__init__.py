@@ -63,11 +63,13 @@ _lib.uzip_status_str.argtypes = [_int]
 _lib.uzip_status_str.restype = _c.c_char_p
 _lib.uzip_inject_scan_stall.argtypes = [_u32, _u32]
 _lib.uzip_inject_scan_stall.restype = _int
+_lib.uzip_compress_noalloc.argtypes = [_vp, _u64, _int, _u32, _vp, _sz, _vp, _vp]
+_lib.uzip_compress_noalloc.restype = _int
 
 EXPORTED = ["uzip_max_compressed_size", "uzip_workspace_size", "uzip_compress", "uzip_decompress",
             "uzip_reduce_fused", "uzip_compress_chunked", "uzip_status_str", "uzip_build_table",
             "uzip_compress_table", "uzip_decompress_table", "uzip_compress_chunked_table",
-            "uzip_inject_scan_stall"]
+            "uzip_inject_scan_stall", "uzip_compress_noalloc"]
 
 
 class UzipError(RuntimeError):
@@ -87,6 +89,10 @@ def uzip_workspace_size(op: int, dtype: int, n_elems: int, block_bytes: int, aux
 
 def uzip_compress(d_in, n_elems, dtype, block_bytes, d_out, out_cap, d_out_size, d_ws, ws_bytes, stream) -> int:
     return _lib.uzip_compress(d_in, n_elems, dtype, block_bytes, d_out, out_cap, d_out_size, d_ws, ws_bytes, stream)
+
+
+def uzip_compress_noalloc(d_in, n_elems, dtype, block_bytes, d_out, out_cap, d_out_size, stream) -> int:
+    return _lib.uzip_compress_noalloc(d_in, n_elems, dtype, block_bytes, d_out, out_cap, d_out_size, stream)
 
 
 def uzip_decompress(d_in, in_bytes, dtype, n_elems, d_out, out_cap, d_status, d_ws, ws_bytes, stream) -> int:

@@ -2176,6 +2176,14 @@ __global__ void __launch_bounds__(64) table_merge_kernel(const uint32_t *parts_a
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
+// Device scratch of uzip_compress_noalloc, for callers that cannot allocate:
+// the encoder's workspace (ticket and counters, look-back status words,
+// overflow slots).  Every GPU the library runs on holds its own copy until
+// the process ends; host code reaches it only through the address that
+// hipGetSymbolAddress returns for the current device.
+constexpr uint64_t kScratchBytes = 64ull << 20;
+constexpr uint64_t kScratchMaxBlocks = 4194304;  // status words: 32 MiB
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
 // encoder kernels: index = dt * 4 + kind, kind 0/1 = compress large/small
 // blocks, 2/3 = split-send producer large/small blocks; fused reduce apart
 constexpr int kEncodeKernels = 20;
@@ -2218,6 +2226,7 @@ const void *reduce_kernel_ptr(int dt) {
 struct DeviceInfo {
   int cus = 0;
   bool gfx950 = false;
+  uint8_t *scratch = nullptr;  // this device's copy of `scratch` (uzip_compress_noalloc)
 };
 
 // fault injection (uzip_inject_scan_stall)
@@ -2238,6 +2247,11 @@ uzip_status device_info(DeviceInfo &out) {
     if (err != hipSuccess) return;
     g_info[dev].cus = prop.multiProcessorCount;
     g_info[dev].gfx950 = strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+    // the device address of this device's copy of the static scratch (in
+    // host code the array's name is only a stand-in); null on failure, and
+    // uzip_compress_noalloc then reports UZIP_EHIP
+    void *sp = nullptr;
+    if (hipGetSymbolAddress(&sp, HIP_SYMBOL(scratch)) == hipSuccess) g_info[dev].scratch = (uint8_t *)sp;
     const int lds_max = 160 * 1024;
     for (int k = 0; k < kEncodeKernels; ++k)
       (void)hipFuncSetAttribute(encode_kernel_ptr(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
@@ -2307,18 +2321,22 @@ uint32_t encode_lds(uint32_t block_elems, bool windowed) {
 
 struct EncodeWs {
   uint64_t status_off, cnt_off, slot_off, y_off, total;
+  uint64_t slots;  // overflow slots: the persistent grid's upper bound
 };
 
 // workspace: ticket, error word, exit counter | look-back status per block |
 // chunk counters | overflow slots (compress, blocks whose words can exceed
 // the LDS window) | reduced tensor (fused reduce without a caller buffer).
 // [0, slot_off) is cleared per call.
-EncodeWs encode_ws(uint64_t n_blocks, uint64_t n_chunks, uint32_t block_elems, uint64_t ybytes, bool reduce = false) {
+// `slots`: how many overflow slots to lay out (0: n_slots of the call)
+EncodeWs encode_ws(uint64_t n_blocks, uint64_t n_chunks, uint32_t block_elems, uint64_t ybytes, bool reduce = false,
+                   uint64_t slots = 0) {
   EncodeWs w;
   w.status_off = 256;
   w.cnt_off = pad256(w.status_off + 8 * n_blocks);
   w.slot_off = pad256(w.cnt_off + 8 * n_chunks);
-  w.y_off = pad256(w.slot_off + (reduce ? 0 : 2ull * n_slots(n_blocks, block_elems) * slot_words(block_elems)));
+  w.slots = slots ? slots : n_slots(n_blocks, block_elems);
+  w.y_off = pad256(w.slot_off + (reduce ? 0 : 2ull * w.slots * slot_words(block_elems)));
   w.total = pad256(w.y_off + ybytes);
   return w;
 }
@@ -2393,7 +2411,7 @@ uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, 64, lds) != hipSuccess || occ < 1) occ = 1;
   uint64_t grid = (uint64_t)info.cus * (uint64_t)occ;
   if (grid > a.n_blocks) grid = a.n_blocks;
-  if (!reduce && grid > n_slots(a.n_blocks, a.block_elems)) grid = n_slots(a.n_blocks, a.block_elems);
+  if (!reduce && grid > w.slots) grid = w.slots;
   if (grid == 0) grid = 1;
   const uint64_t clear_words = w.slot_off / 4;
   const uint64_t cgrid = (clear_words + 255) / 256 < 4096 ? (clear_words + 255) / 256 : 4096;
@@ -2479,6 +2497,47 @@ uzip_status uzip_compress(const void *d_in, uint64_t n_elems, uzip_dtype dtype, 
   a.slot_bytes = 0;
   a.sizes = d_out_size;
   return launch_encode(a, dtype, false, (uint8_t *)d_ws, w, info, stream);
+}
+
+uzip_status uzip_compress_noalloc(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint32_t block_bytes,
+                                  void *d_out, size_t out_cap, uint64_t *d_out_size, hipStream_t stream) {
+  if (!valid_dtype(dtype) || !valid_block(block_bytes)) return UZIP_EINVAL;
+  if (d_out == nullptr || !aligned16(d_out) || (n_elems > 0 && (d_in == nullptr || !aligned16(d_in))))
+    return UZIP_EINVAL;
+  const uint32_t E = elem_bytes(dtype), be = block_bytes / E;
+  const uint64_t nb = (n_elems + be - 1) / be;
+  if (nb > kScratchMaxBlocks) return UZIP_ENOSPC;  // beyond the scratch's status words
+  if (out_cap < max_size(E, n_elems, be)) return UZIP_ENOSPC;
+  DeviceInfo info;
+  uzip_status st = device_info(info);
+  if (st != UZIP_OK) return st;
+  if (info.scratch == nullptr) return UZIP_EHIP;
+  if (n_elems == 0) {
+    hipLaunchKernelGGL(empty_stream_kernel, dim3(1), dim3(64), 0, stream, (uint8_t *)d_out, (uint32_t)dtype, be,
+                       d_out_size);
+    return hipGetLastError() == hipSuccess ? UZIP_OK : UZIP_EHIP;
+  }
+  // as many overflow slots as the scratch holds after the status words, up
+  // to the usual one per persistent workgroup (fewer only shrink the grid)
+  const EncodeWs full = encode_ws(nb, 1, be, 0);
+  uint64_t slots = full.slots;
+  const uint64_t sw = 2ull * slot_words(be);
+  if (sw > 0 && full.slot_off + slots * sw > kScratchBytes) slots = (kScratchBytes - full.slot_off) / sw;
+  if (slots == 0) return UZIP_ENOSPC;
+  const EncodeWs w = encode_ws(nb, 1, be, 0, false, slots);
+  if (w.total > kScratchBytes) return UZIP_ENOSPC;
+  EncodeArgs a;
+  memset(&a, 0, sizeof(a));
+  a.in = (const uint8_t *)d_in;
+  a.n = n_elems;
+  a.chunk_elems = (nb * be);
+  a.block_elems = be;
+  a.blocks_per_chunk = (uint32_t)nb;
+  a.n_blocks = (uint32_t)nb;
+  a.out = (uint8_t *)d_out;
+  a.slot_bytes = 0;
+  a.sizes = d_out_size;
+  return launch_encode(a, dtype, false, info.scratch, w, info, stream);
 }
 
 uzip_status uzip_compress_chunked(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint32_t block_bytes,

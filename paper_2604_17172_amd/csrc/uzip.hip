@@ -83,15 +83,17 @@ struct EncodeArgs {
   uint32_t table_stride;  // u16 entries between the tables of consecutive streams (0: one table for all)
   uint32_t table_mode;
   uint32_t table_bytes;
-  // error channel: the single-pass scan's bounded wait (polls), a block that
-  // never publishes its length (fault injection; ~0u: none), the caller's
-  // device status (fused reduce; may be null) and the workspace counter of
-  // workgroups that have finished
-  uint32_t spin_limit;
-  uint32_t hold_block;
-  uint32_t *dstatus;
-  uint32_t *exit_cnt;
 };
+
+// The first workspace words of an encoder launch (u32 index), written by the
+// clear kernel: the ticket counter, the error word and the count of
+// workgroups that have finished; then, in a cache line of their own (the
+// ticket's takes an atomic from every wave per block), the single-pass
+// scan's bounded wait (polls), a block that never publishes its length
+// (fault injection; ~0u: none) and the caller's device status (fused
+// reduce; may be null).  Read from memory where used, they take no
+// registers in the encoder's loop.
+enum : uint32_t { kWsTicket = 0, kWsError = 1, kWsExit = 2, kWsSpin = 32, kWsHold = 33, kWsStatusPtr = 34 };
 
 constexpr size_t kDecodeWsBytes = 256;   // reserved: the decoder keeps no state there
 
@@ -812,8 +814,8 @@ __device__ __forceinline__ void finish_block(const EncodeArgs &a, const Fin &f, 
   constexpr int NW = 4 * (E / 2);
   const uint32_t lane = lane_id();
   bool failed;
-  const uint64_t excl =
-      resolve_prefix(a.status, f.b, f.first_block, f.sec_len / 16, a.spin_limit, a.hold_block, a.ticket + 1, failed);
+  const uint64_t excl = resolve_prefix(a.status, f.b, f.first_block, f.sec_len / 16, a.ticket[kWsSpin],
+                                       a.ticket[kWsHold], a.ticket + kWsError, failed);
   uint8_t *sec = f.sout + f.coded_off + 16 * excl;
   if (lane == 0)
     out32<SYS>((uint32_t *)(f.sout + kHeaderBytes + 4 * f.lb),
@@ -904,14 +906,15 @@ __device__ __forceinline__ void finish_block(const EncodeArgs &a, const Fin &f, 
 // size 0 -- a stream is never shorter than its 32-byte header, so a zero
 // size is the error -- the split-send producer's DONE flag raised over it,
 // and the fused reduce's status set.
-template <bool SYS>
+template <bool SYS, bool REDUCE>
 __device__ void finish_launch(const EncodeArgs &a) {
   const uint32_t lane = lane_id();
   __builtin_amdgcn_s_waitcnt(0);
   uint32_t last = 0;
-  if (lane == 0) last = __hip_atomic_fetch_add(a.exit_cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1 == gridDim.x;
+  if (lane == 0)
+    last = __hip_atomic_fetch_add(a.ticket + kWsExit, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1 == gridDim.x;
   if (!uniform(last)) return;
-  if (__hip_atomic_load(a.ticket + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) return;
+  if (__hip_atomic_load(a.ticket + kWsError, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) return;
   const uint32_t streams = (a.n_blocks + a.blocks_per_chunk - 1) / a.blocks_per_chunk;
   for (uint32_t c = lane; c < streams; c += 64) {
     const bool bad = a.flags == nullptr ||
@@ -924,7 +927,7 @@ __device__ void finish_launch(const EncodeArgs &a) {
       __hip_atomic_store(&a.flags[2 * c + 1], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     }
   }
-  if (lane == 0) report(a.dstatus, UZIP_ETIMEOUT);
+  if (REDUCE && lane == 0) report(*(uint32_t *const *)(a.ticket + kWsStatusPtr), UZIP_ETIMEOUT);
 }
 
 // ---------------------------------------------------------------------------
@@ -1354,7 +1357,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
       if (f.spilled) __threadfence_block();
     }
     __syncthreads();
-    publish_aggregate(a.status, b, first_block, sec_len / 16, a.hold_block);
+    publish_aggregate(a.status, b, first_block, sec_len / 16, a.ticket[kWsHold]);
     if constexpr (DEFER) {
       pend = f;
       have_pend = true;
@@ -1373,12 +1376,12 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
 template <int DT, bool SMALL, bool SYS, bool SHARED = false>
 __global__ void __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) encode_kernel(EncodeArgs a) {
   encode_body<DT, false, SMALL, SYS, SHARED>(a);
-  finish_launch<SYS>(a);
+  finish_launch<SYS, false>(a);
 }
 template <int DT>
 __global__ void __launch_bounds__(64) reduce_kernel(EncodeArgs a) {
   encode_body<DT, true, false, false>(a);
-  finish_launch<false>(a);
+  finish_launch<false, true>(a);
 }
 
 // ---------------------------------------------------------------------------
@@ -1982,9 +1985,13 @@ __global__ void __launch_bounds__(64 * (kReduceGroup + 1)) reduce_decode_kernel(
 }
 
 // zero the ticket, the look-back status words and the chunk counters
-__global__ void clear_kernel(uint32_t *p, uint64_t words) {
+__global__ void clear_kernel(uint32_t *p, uint64_t words, uint32_t spin, uint32_t hold, uint64_t status_ptr) {
   for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < words; i += (uint64_t)gridDim.x * blockDim.x)
-    p[i] = 0;
+    p[i] = i == kWsSpin                ? spin
+           : i == kWsHold              ? hold
+           : i == kWsStatusPtr         ? (uint32_t)status_ptr
+           : i == kWsStatusPtr + 1     ? (uint32_t)(status_ptr >> 32)
+                                       : 0u;
 }
 
 // n == 0: the stream is the 32-byte header alone
@@ -2389,12 +2396,10 @@ uzip_status launch_table_split(const void *d_in, uint64_t n, uzip_dtype dt, uint
 }
 
 uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws, const EncodeWs &w,
-                          const DeviceInfo &info, hipStream_t stream, bool shared = false) {
+                          const DeviceInfo &info, hipStream_t stream, bool shared = false,
+                          uint32_t *dstatus = nullptr) {
   const bool small = !reduce && small_path(a.block_elems);
-  a.ticket = (uint32_t *)ws;  // word 1: error word, word 2: exit counter
-  a.exit_cnt = (uint32_t *)ws + 2;
-  a.spin_limit = g_spin_limit.load(std::memory_order_relaxed);
-  a.hold_block = g_hold_block.load(std::memory_order_relaxed);
+  a.ticket = (uint32_t *)ws;  // the kWs* words, then the look-back status
   a.status = (uint64_t *)(ws + w.status_off);
   a.chunk_cnt = (uint32_t *)(ws + w.cnt_off);
   a.slots = (uint16_t *)(ws + w.slot_off);
@@ -2415,7 +2420,9 @@ uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws
   if (grid == 0) grid = 1;
   const uint64_t clear_words = w.slot_off / 4;
   const uint64_t cgrid = (clear_words + 255) / 256 < 4096 ? (clear_words + 255) / 256 : 4096;
-  hipLaunchKernelGGL(clear_kernel, dim3((unsigned)cgrid), dim3(256), 0, stream, (uint32_t *)ws, clear_words);
+  hipLaunchKernelGGL(clear_kernel, dim3((unsigned)cgrid), dim3(256), 0, stream, (uint32_t *)ws, clear_words,
+                     g_spin_limit.load(std::memory_order_relaxed), g_hold_block.load(std::memory_order_relaxed),
+                     (uint64_t)(uintptr_t)dstatus);
   if (hipGetLastError() != hipSuccess) return UZIP_EHIP;
   void *args[] = {&a};
   if (hipLaunchKernel(fn, dim3((unsigned)grid), dim3(64), args, lds, stream) != hipSuccess) return UZIP_EHIP;
@@ -2798,8 +2805,7 @@ uzip_status uzip_reduce_fused(const void *const *d_in, const size_t *in_bytes, i
   a.sizes = d_out_size;
   a.ybuf = ybuf;
   a.hist_in = (const uint32_t *)(ws + w.hist_off);
-  a.dstatus = d_status;
-  return launch_encode(a, dtype, true, ws, w.enc, info, stream);
+  return launch_encode(a, dtype, true, ws, w.enc, info, stream, false, d_status);
 }
 
 uzip_status uzip_inject_scan_stall(uint32_t spin_limit, uint32_t held_block) {

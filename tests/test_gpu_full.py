@@ -185,3 +185,85 @@ def test_reduce_8x16MiB(uz):
     out2, size2, _, st2 = uz.reduce_fused(gstreams, "bf16", n, 65536, want_raw=False)
     torch.cuda.synchronize()
     assert int(st2.item()) == 0 and np.array_equal(out2[:int(size2.item())].cpu().numpy(), want_s)
+
+
+def test_split_send_ordering_seen_from_the_host(uz):
+    """Split-send (section 3.2.3, Property 2 of section 3.2.1): a chunk's
+    uncompressed part is final, and usable, as soon as its RAW_READY flag is
+    up, before its stream is done.  The producer writes the chunk streams,
+    their sizes and the flags straight into pinned host memory while this
+    thread polls the flags.  At the first sight of RAW_READY[c] the chunk's
+    raw plane is read and compared with the oracle's; at the first sight of
+    DONE[c] the whole stream and its size.  DONE flags are read before
+    RAW_READY flags in every poll, so a DONE without its RAW_READY would be
+    seen.  512 MiB of the weight-sync buffer, 4 MiB chunks, 64 KiB blocks."""
+    from concurrent.futures import ThreadPoolExecutor
+    bb, cb = 65536, 4 << 20
+    x = W.weight_sync(256 << 20)
+    n = x.size
+    ce = cb // 2
+    chunks = -(-n // ce)
+    t0 = time.time()
+    with ThreadPoolExecutor(16) as ex:
+        want = list(ex.map(lambda c: ref.compress(x[c * ce:(c + 1) * ce], "bf16", bb), range(chunks)))
+    say(f"[full] split-send ordering: {chunks} chunks, oracle {time.time() - t0:.1f}s")
+    slot = (uz.uzip_max_compressed_size(uz.BF16, ce, bb) + 255) // 256 * 256
+    out = torch.zeros(slot * chunks, dtype=torch.uint8).pin_memory()
+    sizes = torch.zeros(chunks, dtype=torch.int64).pin_memory()
+    flags = torch.zeros(2 * chunks, dtype=torch.int32).pin_memory()
+    ws = torch.empty(uz.uzip_workspace_size(uz.OP_CHUNKED, uz.BF16, n, bb, cb), dtype=torch.uint8, device="cuda")
+    xt = to_dev(x, "bf16")
+    ob, sb, fl = out.numpy(), sizes.numpy(), flags.numpy()
+    raw_off = 32 + (4 * (ce // 32768) + 15) // 16 * 16       # every chunk here is full
+    epoch = 5
+    torch.cuda.synchronize()
+    rc = uz.uzip_compress_chunked(xt.data_ptr(), n, uz.BF16, bb, cb, out.data_ptr(), slot, sizes.data_ptr(),
+                                  flags.data_ptr(), epoch, ws.data_ptr(), ws.numel(),
+                                  torch.cuda.current_stream().cuda_stream)
+    assert rc == uz.OK
+    raw_seen = np.zeros(chunks, bool)
+    done_seen = np.zeros(chunks, bool)
+    lead = 0           # chunks whose RAW_READY was seen while DONE was still down
+    deadline = time.time() + 60
+    while not done_seen.all():
+        assert time.time() < deadline, "flags never all raised"
+        done = fl[1::2].copy() == epoch
+        raw = fl[0::2].copy() == epoch
+        assert not (done & ~raw).any(), f"DONE before RAW_READY for chunks {np.flatnonzero(done & ~raw)}"
+        for c in np.flatnonzero(raw & ~raw_seen):
+            raw_seen[c] = True
+            lead += int(not done[c])
+            got = ob[c * slot + raw_off:c * slot + raw_off + ce]
+            assert np.array_equal(got, want[c][raw_off:raw_off + ce]), f"raw plane of chunk {c} not final"
+        for c in np.flatnonzero(done & ~done_seen):
+            done_seen[c] = True
+            sz = int(sb[c])
+            assert sz == want[c].size, f"chunk {c} size {sz} != {want[c].size}"
+            assert np.array_equal(ob[c * slot:c * slot + sz], want[c]), f"chunk {c} stream not final at DONE"
+    torch.cuda.synchronize()
+    say(f"[full] split-send ordering: RAW_READY seen before DONE for {lead} of {chunks} chunks")
+    assert lead >= 1
+
+
+def test_reduce_full_tensor_reading(uz):
+    """The other reading of the activation slices (section 3.4, the fused
+    reduce of one rank): each of the 8 inputs is the whole [8192 x 8192]
+    bf16 tensor (128 MiB, 2048 blocks), reduced and recompressed in one
+    call; stream and reduced tensor against the oracle."""
+    from concurrent.futures import ThreadPoolExecutor
+    xs = W.reduce_slices(tokens=8192)
+    n = xs[0].size
+    say(f"[full] reduce, full-tensor reading: 8 x n={n}")
+    t0 = time.time()
+    with ThreadPoolExecutor(8) as ex:
+        streams = list(ex.map(lambda v: ref.compress(v, "bf16", 65536), xs))
+    want_s, want_y = ref.reduce(streams, "bf16", n, 65536)
+    say(f"[full] reduce full-tensor oracle {time.time() - t0:.1f}s")
+    dstreams = [torch.from_numpy(s).cuda() for s in streams]
+    del xs
+    out, size, raw, status = uz.reduce_fused(dstreams, "bf16", n, 65536)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    got = out[:int(size.item())].cpu().numpy()
+    assert np.array_equal(got, want_s), f"reduce stream differs at {first_diff(got, want_s)}"
+    assert np.array_equal(raw.cpu().numpy().view(np.uint16), want_y)

@@ -50,7 +50,7 @@ using namespace uzip;
 namespace {
 
 constexpr int kMaxInputs = 16;
-constexpr uint32_t kTrashBytes = 256;  // encoder: one 4-byte slot per lane for non-emitted words
+constexpr uint32_t kTrashBytes = 256;  // encoder: slots for non-emitted words (2 bytes per lane), free outside coding
 constexpr uint32_t kMinBlockBytes = 4096, kMaxBlockBytes = 262144;
 
 struct EncodeArgs {
@@ -408,10 +408,14 @@ __device__ void build_enc_table(const uint32_t *hist, uint32_t n_b, uint4 *enc, 
   uint32_t pres = (c[0] > 0) + (c[1] > 0) + (c[2] > 0) + (c[3] > 0);
   uint32_t k = wave_sum(pres);
   uint32_t lt = 0;
+  // c (M - k) < 2^17 * 2^11: the quotient is exact in 32 bits; every block
+  // but a stream's last has a power-of-two size, a shift
+  const bool pow2 = (n_b & (n_b - 1)) == 0;
+  const uint32_t lg = 31 - __clz(n_b);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    // c (M - k) < 2^17 * 2^11: the quotient is exact in 32 bits
-    t.f[q] = c[q] ? 1u + (c[q] * (kM - k)) / n_b : 0u;
+    const uint32_t num = c[q] * (kM - k);
+    t.f[q] = c[q] ? 1u + (pow2 ? num >> lg : num / n_b) : 0u;
     lt += t.f[q];
   }
   uint32_t d = kM - wave_sum(lt);
@@ -958,8 +962,9 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   // ovf[v] is index v
   uint16_t *ovf = !REDUCE ? a.slots + (uint64_t)blockIdx.x * a.slot_words + kSlotLead - a.lds_words : nullptr;
   typedef __attribute__((address_space(3))) uint16_t lds16_t;
-  // one private 4-byte slot per lane for words that are not emitted
-  lds16_t *trash = (lds16_t *)smem_base + 2 * lane;
+  // one private 2-byte slot per lane for words that are not emitted (64
+  // slots in 32 consecutive words: every bank once)
+  lds16_t *trash = (lds16_t *)smem_base + lane;
   // small blocks: a block's offset is resolved and its section written
   // after the next block's first pass, so the wait for slower predecessors
   // overlaps streaming.  The staging area then still holds the pending
@@ -2044,7 +2049,7 @@ __device__ void write_table(const uint32_t c[4], uint32_t n_s, uint16_t *dst0, u
 // (out + c slot_bytes, after its directory).
 // ---------------------------------------------------------------------------
 constexpr uint32_t kTableThreads = 256;
-constexpr uint32_t kLaneHist = kPackedHistStride;  // 128 packed words + 1: a bin of consecutive threads in distinct banks
+constexpr uint32_t kLaneHist = 129;  // 128 packed words + 1: a bin of consecutive threads in distinct banks
 constexpr uint32_t kTableLds = kTableThreads * kLaneHist * 4;
 template <int DT>
 __global__ void __launch_bounds__(kTableThreads) table_kernel(const uint8_t *in_all, uint64_t n_all,

@@ -195,11 +195,16 @@ __device__ __forceinline__ void coh64(uint64_t *p, uint64_t v) {
   if (SYS) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   else __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// 16 bytes in one store; the split-send producer's is written through to
+// memory (sc0 sc1, as its system-scope stores are) in one 16-byte access
+// rather than two 8-byte halves.  The memory counter completes in issue
+// order, so waits the compiler places for its own accesses stay correct.
 template <bool SYS>
 __device__ __forceinline__ void out128(uint8_t *p, uint4 v) {
   if (SYS) {
-    out64<true>(p, v.x, v.y);
-    out64<true>(p + 8, v.z, v.w);
+    typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+    const v4u w = {v.x, v.y, v.z, v.w};
+    asm volatile("global_store_dwordx4 %0, %1, off sc0 sc1" ::"v"(p), "v"(w) : "memory");
   } else {
     *(uint4 *)p = v;
   }

@@ -26,12 +26,16 @@
 //                   offset is read from the directory, its decode table
 //                   (2048 x u32) is built in LDS, its words are staged
 //                   through an LDS ring and the 64 states decode forwards.
-//   reduce_decode_kernel + encode_kernel (fused reduce)  one workgroup per
-//                   output block decodes block b of up to eight inputs in
-//                   parallel waves, round by round, and a further wave adds
-//                   them in binary32 in input order and splits the rounded
-//                   result (raw plane, histogram); reduce_kernel, the
-//                   encoder's coding half, then runs over the reduced tensor.
+//   reduce_fused_kernel (fused reduce)  one workgroup per output block
+//                   decodes block b of up to eight inputs in parallel waves,
+//                   round by round; a further wave adds them in binary32 in
+//                   input order, splits the rounded result (raw plane,
+//                   histogram, symbols kept in LDS) and then codes the block
+//                   and places its section itself.  When the output blocks
+//                   outnumber the compute units (or a block's symbols do not
+//                   fit in LDS), reduce_decode_kernel does the decoding and
+//                   summing and reduce_kernel, the encoder's coding half,
+//                   runs over the reduced tensor.
 //   split-send producer  encode_kernel with write-through stores and
 //                   per-chunk completion counters.
 #include <hip/hip_fp16.h>
@@ -784,6 +788,17 @@ __device__ __forceinline__ uint4 lds_unit(const uint32_t *s32, uint32_t u, uint3
   return o;
 }
 
+// bytes [0, keep) of o, the rest zero (any keep < 16)
+__device__ __forceinline__ uint4 mask_bytes(uint4 o, uint32_t keep) {
+  uint32_t w[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int nb = (int)keep - 4 * j;
+    w[j] = nb >= 4 ? w[j] : nb <= 0 ? 0u : w[j] & ((1u << (8 * nb)) - 1u);
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
 // bytes [0, m) of a and [m, 16) of b (m even, 0 < m < 16)
 __device__ __forceinline__ uint4 splice_bytes(uint4 a, uint4 b, uint32_t m) {
   const uint32_t x[4] = {a.x, a.y, a.z, a.w}, y[4] = {b.x, b.y, b.z, b.w};
@@ -811,8 +826,34 @@ struct Fin {
   uint32_t A;          // staging-area byte offset of the image
   uint32_t lds_bytes;  // image bytes in LDS; the rest is in the overflow slot
   uint32_t slot_delta; // slot byte = image byte + slot_delta (mod 2^32)
+  const uint8_t *sym_lds;  // fused reduce: the block's symbols in LDS (a STORED block copies them)
   bool stored, spilled, last;
 };
+
+// The section head right before a coded block's words in the staging area
+// (image byte offset A): the 64 states, and for a table of its own the
+// presence bitmap and the frequencies.
+template <bool SHARED>
+__device__ __forceinline__ void write_section_head(uint8_t *stage, uint32_t A, uint32_t x, const Table &t) {
+  const uint32_t lane = lane_id();
+  uint16_t *h16 = (uint16_t *)(stage + A);
+  h16[2 * lane] = (uint16_t)x;
+  h16[2 * lane + 1] = (uint16_t)(x >> 16);
+  if constexpr (!SHARED) {
+    if (lane < 16) {
+      uint32_t word = 0;
+      for (uint32_t bit = 0; bit < 16; ++bit) {
+        uint32_t sy = 16 * lane + bit;
+        word |= (uint32_t)((t.present[sy & 3] >> (sy >> 2)) & 1u) << bit;
+      }
+      h16[128 + lane] = (uint16_t)word;
+    }
+    uint32_t rk = t.rank0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (t.f[q]) h16[144 + rk++] = (uint16_t)t.f[q];
+  }
+}
 
 // Resolve the block's offset, write its directory entry and section, and for
 // a stream's last block the stream header.
@@ -856,6 +897,13 @@ __device__ __forceinline__ void finish_block(const EncodeArgs &a, const Fin &f, 
         }
         out128<SYS>(sec + 16 * u, o);
       }
+    }
+  } else if (f.sym_lds != nullptr) {
+    // STORED, fused reduce: the block's symbol bytes from LDS, zero-padded
+    for (uint32_t u = lane; u < f.sec_len / 16; u += 64) {
+      uint4 o = *(const uint4 *)(f.sym_lds + 16 * u);
+      if (16 * u + 16 > f.n_b) o = mask_bytes(o, f.n_b - 16 * u);
+      out128<SYS>(sec + 16 * u, o);
     }
   } else {
     // STORED: the block's symbol bytes, zero-padded to 16, re-read from the
@@ -1342,26 +1390,11 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     f.stored = stored;
     f.spilled = !REDUCE && spilled != a.wcap;
     f.last = last_in_chunk;
+    f.sym_lds = nullptr;
     if (!stored) {
       // header bytes right before the words: states | bitmap | f[k] (states
       // only with a stream-wide table)
-      uint16_t *h16 = (uint16_t *)(stage + f.A);
-      h16[2 * lane] = (uint16_t)x;
-      h16[2 * lane + 1] = (uint16_t)(x >> 16);
-      if constexpr (!SHARED) {
-        if (lane < 16) {
-          uint32_t word = 0;
-          for (uint32_t bit = 0; bit < 16; ++bit) {
-            uint32_t sy = 16 * lane + bit;
-            word |= (uint32_t)((t.present[sy & 3] >> (sy >> 2)) & 1u) << bit;
-          }
-          h16[128 + lane] = (uint16_t)word;
-        }
-        uint32_t rk = t.rank0;
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (t.f[q]) h16[144 + rk++] = (uint16_t)t.f[q];
-      }
+      write_section_head<SHARED>(stage, f.A, x, t);
       // the overflow slot was written by this wave: order its stores before
       // the copy-out's reads (one wave per workgroup, one CU: no cache in between)
       if (f.spilled) __threadfence_block();
@@ -1796,6 +1829,9 @@ struct ReduceArgs {
   uint8_t *yout;           // caller's copy of it (may be null or ybuf)
   uint32_t *hist_out;      // [n_blocks][256]
   uint32_t *dstatus;
+  // reduce_fused_kernel: byte offsets of its LDS regions (the decoders'
+  // tables and rings, later the coding pass's staging area, start at 0)
+  uint32_t lds_slabs, lds_hist, lds_syms, lds_enc, lds_trash;
 };
 
 uint32_t reduce_lds(int n_in, uint32_t E) { return n_in * (kDecLds + 2 * kRound * E) + kHistBytes; }
@@ -1992,6 +2028,307 @@ __global__ void __launch_bounds__(64 * (kReduceGroup + 1)) reduce_decode_kernel(
       a.hist_out[(uint64_t)b * 256 + sy] = c;
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// reduce_fused_kernel: the whole fused reduce of one output block per
+// workgroup (section 3.4's receive-reduce-send step with the codec fused
+// in), for the last (or only) group of up to eight inputs.  Workgroups take
+// output blocks by ticket.  Waves 0 .. n_in-1 decode block b of their input
+// round by round into double-buffered LDS slabs (lookup table and word ring
+// as in reduce_decode_kernel, raw bytes loaded a round ahead); wave n_in adds
+// the slabs in input order in binary32 (after the partial sums of earlier
+// input groups), adds the local share, rounds to the element type, writes
+// the output stream's raw plane (and the caller's copy of the reduced
+// tensor), and keeps the block's symbols and histogram in LDS.  After the
+// last round the decoding waves end and the reducing wave codes the block
+// from LDS -- table, the 64 rANS states backwards, words staged where the
+// lookup tables were -- and places its section with the single-pass scan.
+// The reduced tensor does not go through HBM.
+// ---------------------------------------------------------------------------
+template <int DT>
+__global__ void __launch_bounds__(64 * (kReduceGroup + 1)) reduce_fused_kernel(ReduceArgs r, EncodeArgs a) {
+  constexpr int E = (DT == 2) ? 4 : 2;
+  constexpr int NW = 4 * (E / 2);
+  constexpr uint32_t kSlab = kRound * E;
+  extern __shared__ __align__(16) uint8_t smem_base[];
+  __shared__ uint32_t s_block;
+  typedef __attribute__((address_space(3))) uint16_t lds16_t;
+  const uint32_t wave = threadIdx.x >> 6;
+  const uint32_t lane = lane_id();
+  const int n_in = r.n_in;
+  const bool decoder = (int)wave < n_in;
+  uint8_t *slabs = smem_base + r.lds_slabs;  // [2][n_in][512 elements]
+  uint32_t *hist = (uint32_t *)(smem_base + r.lds_hist);
+  uint8_t *syms = smem_base + r.lds_syms;    // the block's symbols, 512 per round
+  const uint32_t be = r.block_elems;
+
+  // the output block: taken in ticket order, so a workgroup only ever waits
+  // in the scan for blocks of workgroups that started before it
+  if (!decoder) {
+    if (lane == 0) s_block = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (uint32_t i = lane; i < kHistReplicas * kHistStride; i += 64) hist[i] = 0;
+  }
+  __syncthreads();
+  const uint32_t b = uniform(s_block);
+  if (b >= a.n_blocks) return;  // (the grid has exactly one workgroup per block)
+  const uint64_t blk0 = (uint64_t)b * be;
+  const uint32_t n_b = (uint32_t)((r.n - blk0) < be ? (r.n - blk0) : be);
+  const uint32_t rounds = (n_b + kRound - 1) / kRound;
+  const uint32_t full = n_b / kRound;
+  const Geom g = make_geom(r.n, be, E);
+
+  // ---- decoding waves: block b of input `wave` ----
+  uint32_t *lut = (uint32_t *)(smem_base + wave * kDecLds);
+  uint8_t *ring = smem_base + wave * kDecLds + kLutBytes;
+  enum : uint32_t { kBad = 0, kStored = 1, kCoded = 2 };
+  uint32_t mode = kBad;
+  const uint8_t *sec = nullptr, *raw_plane = nullptr;
+  uint32_t x = kStateLo, x0 = kStateLo, p = 0, rb = 0, wb = 0, w_avail = 0;
+  Ring rg;
+  rg.written = 0;
+  rg.len = 16;
+  rg.pv = make_uint4(0, 0, 0, 0);
+  if (decoder) {
+    const uint8_t *s = r.ins[wave];
+    bool ok = r.in_bytes[wave] >= kHeaderBytes;
+    uint64_t total = 0;
+    if (ok) {
+      total = ld64(s + 24);
+      ok = ld32(s) == kMagic && s[4] == kVersion && s[5] == DT && s[6] == kProbBits && s[7] == 0 &&
+           ld32(s + 8) == be && ld32(s + 12) == g.n_blocks && ld64(s + 16) == r.n && total <= r.in_bytes[wave] &&
+           total >= g.coded_off;
+    }
+    uint64_t start = 0, end = 0;
+    uint32_t d = 0;
+    if (ok) {
+      d = ld32(s + kHeaderBytes + 4 * b);
+      start = b ? 16ull * (ld32(s + kHeaderBytes + 4 * (b - 1)) & ~kStoredBit) : 0;
+      end = 16ull * (d & ~kStoredBit);
+      ok = end >= start && g.coded_off + end <= total;
+    }
+    if (ok) {
+      sec = s + g.coded_off + start;
+      raw_plane = s + g.raw_off;
+      const uint32_t len = (uint32_t)(end - start);
+      if (d >> 31) {
+        ok = len >= n_b;
+        mode = kStored;
+      } else {
+        uint32_t k = 0;
+        ok = build_lut(sec, len, lut, (uint16_t *)ring, (uint16_t *)ring + 256, k);
+        if (ok) {
+          mode = kCoded;
+          k = uniform(k);
+          x = x0 = ((const uint32_t *)sec)[lane];
+          wb = kSectionFixed + 2 * k;
+          w_avail = (len - wb) / 2;
+          rb = wb & (kRingBytes - 1);
+          rg.len = len;
+          rg.written = wb & ~15u;
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            const uint32_t o = rg.written + 16 * lane;
+            ring_put(ring, o & (kRingBytes - 1), ring_fetch(sec, o, len));
+            rg.written += kChunkBytes;
+          }
+          rg.pv = ring_fetch(sec, rg.written + 16 * lane, len);
+        }
+      }
+    }
+    if (!ok) {
+      mode = kBad;
+      if (lane == 0) report(r.dstatus, UZIP_ECORRUPT);
+    }
+  }
+  uint32_t *h = hist + (lane & (kHistReplicas - 1)) * kHistStride;
+  // raw bytes of this lane's group of round q (the output's for a partial
+  // round are masked by `valid`)
+  auto load_raw_round = [&](uint32_t q, uint32_t raw[6]) {
+    const uint32_t i0 = q * kRound + kPerLane * lane;
+    const uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
+    if (q < full) load_raw_full<E>(raw_plane, blk0 + i0, raw);
+    else load_raw<E>(raw_plane, blk0 + i0, valid, raw);
+  };
+  uint32_t rawA[6] = {0, 0, 0, 0, 0, 0}, rawB[6] = {0, 0, 0, 0, 0, 0};
+  if (decoder && mode != kBad && rounds > 0) load_raw_round(0, rawA);
+  __syncthreads();
+
+  // one round: decoders fill slab (q & 1) (raw bytes of round q in `cur`,
+  // round q + 1's loaded into `nxt`), one barrier, the reducing wave takes
+  // the slab while the decoders go on with round q + 1
+  auto round_body = [&](uint32_t q, uint32_t cur[6], uint32_t nxt[6]) {
+    uint8_t *slab = slabs + (q & 1) * n_in * kSlab;
+    const uint32_t i0 = q * kRound + kPerLane * lane;
+    const uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
+    if (decoder) {
+      uint32_t w[NW];
+#pragma unroll
+      for (int t = 0; t < NW; ++t) w[t] = 0;
+      if (mode != kBad && q + 1 < rounds) load_raw_round(q + 1, nxt);
+      if (mode == kCoded) {
+        ring_maintain(rg, ring, sec, wb + 2 * p);
+        uint32_t e[kPerLane];
+        if (q < full) {
+#pragma unroll
+          for (uint32_t t = 0; t < kPerLane; ++t) e[t] = decode_step_ring<true>(x, true, lut, ring, rb, p);
+        } else {
+#pragma unroll
+          for (uint32_t t = 0; t < kPerLane; ++t) e[t] = decode_step_ring<false>(x, t < valid, lut, ring, rb, p);
+        }
+        merge_entries<DT>(e, cur, w);
+      } else if (mode == kStored && valid > 0) {
+        uint32_t sy[2] = {0, 0};
+#pragma unroll
+        for (uint32_t t = 0; t < 8; ++t)
+          if (t < valid) sy[t >> 2] |= (uint32_t)sec[i0 + t] << (8 * (t & 3));
+        merge_group<DT>(sy, cur, w);
+      }
+      uint4 *dst = (uint4 *)(slab + wave * kSlab + kPerLane * E * lane);
+      dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
+      if (E == 4) dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
+    }
+    __syncthreads();
+    if (!decoder && valid > 0) {
+      float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      if (!r.first) {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) acc[t] = (uint32_t)t < valid ? r.acc_in[blk0 + i0 + t] : 0.f;
+      }
+      for (int i = 0; i < n_in; ++i) {
+        const uint4 *src = (const uint4 *)(slab + i * kSlab + kPerLane * E * lane);
+        uint32_t w[NW];
+        const uint4 v0 = src[0];
+        w[0] = v0.x, w[1] = v0.y, w[2] = v0.z, w[3] = v0.w;
+        if (E == 4) {
+          const uint4 v1 = src[1];
+          w[4] = v1.x, w[5] = v1.y, w[6] = v1.z, w[7] = v1.w;
+        }
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const uint32_t wt = (E == 2) ? ((w[t >> 1] >> (16 * (t & 1))) & 0xFFFFu) : w[t];
+          const float v = to_f32<DT>(wt);
+          acc[t] = (r.first && i == 0) ? v : acc[t] + v;
+        }
+      }
+      if (r.local_raw != nullptr) {
+        uint32_t w[NW];
+        load_words<E>(r.local_raw, blk0 + i0, valid, w);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+          const uint32_t wt = (E == 2) ? ((w[t >> 1] >> (16 * (t & 1))) & 0xFFFFu) : w[t];
+          acc[t] = acc[t] + to_f32<DT>(wt);
+        }
+      }
+      uint32_t w[NW];
+#pragma unroll
+      for (int t = 0; t < NW; ++t) w[t] = 0;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const uint32_t y = (uint32_t)t < valid ? from_f32<DT>(acc[t]) : 0u;
+        if (E == 2)
+          w[t >> 1] |= y << (16 * (t & 1));
+        else
+          w[t] = y;
+      }
+      if (r.yout != nullptr) store_words<E>(r.yout, blk0 + i0, valid, w);
+      Group gr;
+      split_group<DT>(w, gr);
+      store_raw<E>(r.out_raw_plane, blk0 + i0, valid, gr);
+      hist_add8(h, gr, valid);
+      *(uint2 *)(syms + q * kRound + kPerLane * lane) = make_uint2(gr.sym[0], gr.sym[1]);
+    }
+  };
+  uint32_t q = 0;
+  for (; q + 2 <= rounds; q += 2) {
+    round_body(q, rawA, rawB);
+    round_body(q + 1, rawB, rawA);
+  }
+  if (q < rounds) round_body(q, rawA, rawB);
+  __syncthreads();
+  if (decoder) {
+    if (mode == kCoded) {
+      const bool bad = x != kStateLo || p > w_avail || x0 < kStateLo || x0 >= 0x80000000u;
+      if (__any(bad) && lane == 0) report(r.dstatus, UZIP_ECORRUPT);
+    }
+    return;
+  }
+
+  // ---- the reducing wave codes the block (the decoding waves have ended) ----
+  uint4 *enc = (uint4 *)(smem_base + r.lds_enc);
+  lds16_t *trash = (lds16_t *)(smem_base + r.lds_trash) + lane;
+  uint8_t *stage = smem_base;  // where the lookup tables and rings were
+  uint16_t *stage16 = (uint16_t *)(stage + kStageHead);
+  if (b + 1 == a.n_blocks && lane < 16) {
+    // zero padding after the raw plane (pad16 of (E-1) n bytes)
+    const uint64_t rbyte = g.raw_off + (uint64_t)(E - 1) * r.n + lane;
+    if (rbyte < g.coded_off) a.out[rbyte] = 0;
+  }
+  wave_lds_fence();
+  Table t;
+  build_enc_table(hist, n_b, enc, t);
+  t.k = uniform(t.k);
+  wave_lds_fence();
+  const uint32_t hdr = kSectionFixed + 2 * t.k;
+  for (uint32_t i = lane; i < kStageTail / 4; i += 64) ((uint32_t *)(stage16 + a.wcap))[i] = 0;
+  const uint32_t limit_words = (n_b > hdr) ? (n_b - hdr + 1) / 2 : 0;
+  uint32_t pos = a.wcap;  // staging indices [pos, wcap) hold the words so far; the block's words all fit
+  lds16_t *lds_rel = (lds16_t *)stage16;
+  uint32_t xs = kStateLo;
+  bool stored = (limit_words == 0);
+  if (full < rounds && !stored) {  // the partial last round comes first
+    const uint32_t i0 = full * kRound + kPerLane * lane;
+    const uint32_t valid = i0 < n_b ? (n_b - i0 < 8 ? n_b - i0 : 8) : 0;
+    const uint2 sv = *(const uint2 *)(syms + full * kRound + kPerLane * lane);
+    const uint32_t sy[2] = {sv.x, sv.y};
+    uint4 e[8];
+#pragma unroll
+    for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(sy, tt)];
+    enc_round<false>(xs, e, valid, pos, lds_rel, trash);
+    if (a.wcap - pos >= limit_words) stored = true;
+  }
+  for (int q2 = (int)full - 1; q2 >= 0 && !stored; --q2) {
+    const uint2 sv = *(const uint2 *)(syms + (uint32_t)q2 * kRound + kPerLane * lane);
+    uint4 e[8];
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt) e[tt] = enc[(sv.x >> (8 * tt)) & 0xFFu];
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt) e[4 + tt] = enc[(sv.y >> (8 * tt)) & 0xFFu];
+    enc_round<true>(xs, e, 8, pos, lds_rel, trash);
+    if (a.wcap - pos >= limit_words) stored = true;
+  }
+  pos = uniform(pos);
+  const uint32_t n_words = a.wcap - pos;
+  const uint64_t img = hdr + 2ull * n_words;
+  const uint64_t sec_len = stored ? pad16(n_b) : pad16(img);
+  Fin f;
+  f.sout = a.out;
+  f.src = nullptr;
+  f.coded_off = g.coded_off;
+  f.dir_end = g.raw_off;
+  f.chunk_n = r.n;
+  f.blk0 = blk0;
+  f.sec_len = sec_len;
+  f.img = (uint32_t)img;
+  f.b = b;
+  f.chunk = 0;
+  f.lb = b;
+  f.first_block = 0;
+  f.n_blocks = g.n_blocks;
+  f.n_b = n_b;
+  f.rounds = rounds;
+  f.A = kStageHead + 2 * pos - hdr;
+  f.lds_bytes = (uint32_t)img;
+  f.slot_delta = 0;
+  f.sym_lds = syms;
+  f.stored = stored;
+  f.spilled = false;
+  f.last = b + 1 == a.n_blocks;
+  if (!stored) write_section_head<false>(stage, f.A, xs, t);
+  wave_lds_fence();
+  publish_aggregate(a.status, b, 0, sec_len / 16, a.ticket[kWsHold]);
+  finish_block<DT, false>(a, f, stage, nullptr);
+  finish_launch<false, true>(a);
 }
 
 // zero the ticket, the look-back status words and the chunk counters
@@ -2279,11 +2616,18 @@ uzip_status device_info(DeviceInfo &out) {
     (void)hipFuncSetAttribute((const void *)reduce_decode_kernel<0>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
     (void)hipFuncSetAttribute((const void *)reduce_decode_kernel<1>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
     (void)hipFuncSetAttribute((const void *)reduce_decode_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
+    // (reduce_fused_kernel has a few bytes of static LDS besides)
+    (void)hipFuncSetAttribute((const void *)reduce_fused_kernel<0>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max - 1024);
+    (void)hipFuncSetAttribute((const void *)reduce_fused_kernel<1>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max - 1024);
+    (void)hipFuncSetAttribute((const void *)reduce_fused_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max - 1024);
     (void)hipFuncSetAttribute((const void *)table_kernel<0>, hipFuncAttributeMaxDynamicSharedMemorySize, kTableLds);
     (void)hipFuncSetAttribute((const void *)table_kernel<1>, hipFuncAttributeMaxDynamicSharedMemorySize, kTableLds);
     (void)hipFuncSetAttribute((const void *)table_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize, kTableLds);
     (void)hipFuncSetAttribute((const void *)table_kernel<3>, hipFuncAttributeMaxDynamicSharedMemorySize, kTableLds);
     (void)hipFuncSetAttribute((const void *)table_kernel<4>, hipFuncAttributeMaxDynamicSharedMemorySize, kTableLds);
+    // an attribute the runtime refused must not surface as the error of a
+    // later launch
+    (void)hipGetLastError();
   });
   if (err != hipSuccess) return UZIP_EHIP;
   out = g_info[dev];
@@ -2372,6 +2716,38 @@ ReduceWs reduce_ws(uint64_t n_blocks, uint32_t block_elems, uint64_t n, uint32_t
   w.acc_off = pad256(w.hist_off + 1024 * n_blocks);
   w.total = pad256(w.acc_off + (n_in > kReduceGroup ? 4 * n : 0));
   return w;
+}
+
+// LDS of reduce_fused_kernel for n_in decoding waves: the decoders' tables
+// and rings (or, once they are done, the staging area of a whole block's
+// words), the slabs, the histogram, the block's symbols, the encoder table
+// and the trash slots; 0 if the block does not fit (larger blocks take the
+// decode-reduce kernel and the encoder's coding pass instead).
+constexpr uint32_t kLdsMax = 160 * 1024;
+uint32_t fused_layout(int n_in, uint32_t E, uint32_t block_elems, ReduceArgs *r) {
+  const uint32_t stage = kStageHead + 2 * word_cap(block_elems) + kStageTail;
+  const uint32_t dec = (uint32_t)n_in * kDecLds;
+  uint32_t o = (dec > stage ? dec : stage);
+  o = (o + 15u) & ~15u;
+  const uint32_t slabs = o;
+  o += 2u * (uint32_t)n_in * kRound * E;
+  const uint32_t hist = o;
+  o += kHistBytes;
+  const uint32_t syms = o;
+  o += (block_elems + 15u) & ~15u;
+  const uint32_t enc = o;
+  o += kEncTableBytes;
+  const uint32_t trash = o;
+  o += kTrashBytes;
+  if (o + 1024 > kLdsMax) return 0;  // (the kernel's own static bytes besides)
+  if (r != nullptr) {
+    r->lds_slabs = slabs;
+    r->lds_hist = hist;
+    r->lds_syms = syms;
+    r->lds_enc = enc;
+    r->lds_trash = trash;
+  }
+  return o;
 }
 
 uzip_status launch_table(const void *d_in, uint64_t n, uzip_dtype dt, uint64_t chunk_elems, uint32_t block_elems,
@@ -2774,9 +3150,26 @@ uzip_status uzip_reduce_fused(const void *const *d_in, const size_t *in_bytes, i
   const Geom g = make_geom(n_elems, be, E);
   // decode + reduce, inputs in groups of up to kReduceGroup
   const int groups = (n_in + kReduceGroup - 1) / kReduceGroup;
+  const int n_last = n_in - (groups - 1) * kReduceGroup;
+  // One kernel for the last group (the whole call for up to eight inputs)
+  // when a block's symbols and words fit in LDS and every output block gets
+  // a compute unit of its own at once (one workgroup per CU; its coding pass
+  // then costs one block's coding).  With more blocks the decode-reduce
+  // kernel and a separate coding pass at higher occupancy overlap better.
+  const bool fused = fused_layout(n_last, E, be, nullptr) != 0 && nb <= (uint64_t)info.cus;
   const void *dfn = dtype == UZIP_BF16   ? (const void *)reduce_decode_kernel<0>
                     : dtype == UZIP_FP16 ? (const void *)reduce_decode_kernel<1>
                                          : (const void *)reduce_decode_kernel<2>;
+  if (fused) {
+    // the scan's workspace words (ticket, error word, exit counter, the
+    // fault settings, the status pointer, the per-block status) start clear
+    const uint64_t clear_words = w.enc.slot_off / 4;
+    const uint64_t cgrid = (clear_words + 255) / 256 < 4096 ? (clear_words + 255) / 256 : 4096;
+    hipLaunchKernelGGL(clear_kernel, dim3((unsigned)cgrid), dim3(256), 0, stream, (uint32_t *)ws, clear_words,
+                       g_spin_limit.load(std::memory_order_relaxed), g_hold_block.load(std::memory_order_relaxed),
+                       (uint64_t)(uintptr_t)d_status);
+    if (hipGetLastError() != hipSuccess) return UZIP_EHIP;
+  }
   for (int gi = 0; gi < groups; ++gi) {
     ReduceArgs r;
     memset(&r, 0, sizeof(r));
@@ -2798,6 +3191,30 @@ uzip_status uzip_reduce_fused(const void *const *d_in, const size_t *in_bytes, i
     r.yout = (uint8_t *)d_out_raw;
     r.hist_out = (uint32_t *)(ws + w.hist_off);
     r.dstatus = d_status;
+    if (fused && r.last) {
+      EncodeArgs a;
+      memset(&a, 0, sizeof(a));
+      a.n = n_elems;
+      a.chunk_elems = nb * be;
+      a.block_elems = be;
+      a.blocks_per_chunk = (uint32_t)nb;
+      a.n_blocks = (uint32_t)nb;
+      a.out = (uint8_t *)d_out;
+      a.sizes = d_out_size;
+      a.ticket = (uint32_t *)ws;
+      a.status = (uint64_t *)(ws + w.enc.status_off);
+      a.chunk_cnt = (uint32_t *)(ws + w.enc.cnt_off);
+      a.wcap = word_cap(be);
+      a.lds_words = a.wcap;
+      const uint32_t lds = fused_layout(r.n_in, E, be, &r);
+      static const void *const ftab[3] = {(const void *)reduce_fused_kernel<0>, (const void *)reduce_fused_kernel<1>,
+                                          (const void *)reduce_fused_kernel<2>};
+      void *args[] = {&r, &a};
+      if (hipLaunchKernel(ftab[(int)dtype], dim3((unsigned)nb), dim3(64 * (r.n_in + 1)), args, lds, stream) !=
+          hipSuccess)
+        return UZIP_EHIP;
+      return UZIP_OK;
+    }
     const uint32_t lds = reduce_lds(r.n_in, E);
     void *args[] = {&r};
     if (hipLaunchKernel(dfn, dim3((unsigned)nb), dim3(64 * (r.n_in + 1)), args, lds, stream) != hipSuccess)

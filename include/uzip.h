@@ -192,7 +192,8 @@ uzip_status uzip_compress_table(const void *d_in, uint64_t n_elems, uzip_dtype d
  * EXTERNAL table that is not an all-symbol table codes nothing: the chunk
  * sizes read 0 and no flag is raised.  Otherwise as uzip_compress_chunked
  * (PER_BLOCK is that call).  Each chunk decodes with
- * uzip_decompress_table. */
+ * uzip_decompress_table, or a batch of chunks with
+ * uzip_decompress_chunked_table. */
 uzip_status uzip_compress_chunked_table(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint32_t block_bytes,
                                         uint64_t chunk_bytes, uzip_table_mode mode, const uint16_t *d_table,
                                         void *d_out, size_t slot_bytes, uint64_t *chunk_sizes, uint32_t *flags,
@@ -206,6 +207,37 @@ uzip_status uzip_compress_chunked_table(const void *d_in, uint64_t n_elems, uzip
 uzip_status uzip_decompress_table(const void *d_in, size_t in_bytes, uzip_dtype dtype, uint64_t n_elems,
                                   const uint16_t *d_table, void *d_out, size_t out_cap, uint32_t *d_status,
                                   void *d_ws, size_t ws_bytes, hipStream_t stream);
+
+/* Receiver side of the split-send pipeline (section 3.2.3): decompress the
+ * chunk streams c = first_chunk .. first_chunk + n_chunks - 1 of a tensor
+ * of n_elems values cut into chunks of chunk_bytes, as the producer
+ * (uzip_compress_chunked with the same dtype, block_bytes and chunk_bytes)
+ * laid them out, in one launch: every block of every chosen chunk is
+ * decoded at once, where one uzip_decompress call per chunk runs that
+ * chunk's few blocks alone.  A receiver calls it on each batch of chunks
+ * whose DONE flags it has seen.
+ *   d_in, slot_bytes: chunk c's stream is at d_in + c * slot_bytes and fits
+ *                     its slot (slot_bytes a multiple of 16).
+ *   d_out, out_cap:   the whole tensor's buffer: chunk c's values go to
+ *                     element offset c * chunk_bytes / element size, and
+ *                     nothing else is written; out_cap covers the tensor
+ *                     up to the end of the last chosen chunk.
+ *   d_status:         as for uzip_decompress (one word for all chosen
+ *                     chunks; the first error found wins).
+ * n_chunks == 0 is a no-op.  Errors: EINVAL (bad sizes, a range past the
+ * tensor's chunks), ENOSPC, EHIP, EUNSUPPORTED. */
+uzip_status uzip_decompress_chunked(const void *d_in, size_t slot_bytes, uint64_t first_chunk, uint64_t n_chunks,
+                                    uzip_dtype dtype, uint64_t n_elems, uint32_t block_bytes, uint64_t chunk_bytes,
+                                    void *d_out, size_t out_cap, uint32_t *d_status, hipStream_t stream);
+
+/* uzip_decompress_chunked for chunk streams of uzip_compress_chunked_table
+ * (SAMPLED: each chunk's own stored table; EXTERNAL: d_table, the table
+ * the chunks were coded with, 16-byte aligned).  d_table is ignored for
+ * SAMPLED and may be NULL; a PER_BLOCK chunk stream is reported corrupt. */
+uzip_status uzip_decompress_chunked_table(const void *d_in, size_t slot_bytes, uint64_t first_chunk,
+                                          uint64_t n_chunks, uzip_dtype dtype, uint64_t n_elems,
+                                          uint32_t block_bytes, uint64_t chunk_bytes, const uint16_t *d_table,
+                                          void *d_out, size_t out_cap, uint32_t *d_status, hipStream_t stream);
 
 /* Fused decompress -> reduce -> recompress of one rank's share (section
  * 3.4, the CopyReducePacks step with compression fused in).

@@ -65,11 +65,17 @@ _lib.uzip_inject_scan_stall.argtypes = [_u32, _u32]
 _lib.uzip_inject_scan_stall.restype = _int
 _lib.uzip_compress_noalloc.argtypes = [_vp, _u64, _int, _u32, _vp, _sz, _vp, _vp]
 _lib.uzip_compress_noalloc.restype = _int
+_lib.uzip_decompress_chunked.argtypes = [_vp, _sz, _u64, _u64, _int, _u64, _u32, _u64, _vp, _sz, _vp, _vp]
+_lib.uzip_decompress_chunked.restype = _int
+_lib.uzip_decompress_chunked_table.argtypes = [_vp, _sz, _u64, _u64, _int, _u64, _u32, _u64, _vp, _vp, _sz, _vp,
+                                               _vp]
+_lib.uzip_decompress_chunked_table.restype = _int
 
 EXPORTED = ["uzip_max_compressed_size", "uzip_workspace_size", "uzip_compress", "uzip_decompress",
             "uzip_reduce_fused", "uzip_compress_chunked", "uzip_status_str", "uzip_build_table",
             "uzip_compress_table", "uzip_decompress_table", "uzip_compress_chunked_table",
-            "uzip_inject_scan_stall", "uzip_compress_noalloc"]
+            "uzip_inject_scan_stall", "uzip_compress_noalloc", "uzip_decompress_chunked",
+            "uzip_decompress_chunked_table"]
 
 
 class UzipError(RuntimeError):
@@ -133,6 +139,18 @@ def uzip_decompress_table(d_in, in_bytes, dtype, n_elems, d_table, d_out, out_ca
                           stream) -> int:
     return _lib.uzip_decompress_table(d_in, in_bytes, dtype, n_elems, d_table, d_out, out_cap, d_status, d_ws,
                                       ws_bytes, stream)
+
+
+def uzip_decompress_chunked(d_in, slot_bytes, first_chunk, n_chunks, dtype, n_elems, block_bytes, chunk_bytes,
+                            d_out, out_cap, d_status, stream) -> int:
+    return _lib.uzip_decompress_chunked(d_in, slot_bytes, first_chunk, n_chunks, dtype, n_elems, block_bytes,
+                                        chunk_bytes, d_out, out_cap, d_status, stream)
+
+
+def uzip_decompress_chunked_table(d_in, slot_bytes, first_chunk, n_chunks, dtype, n_elems, block_bytes,
+                                  chunk_bytes, d_table, d_out, out_cap, d_status, stream) -> int:
+    return _lib.uzip_decompress_chunked_table(d_in, slot_bytes, first_chunk, n_chunks, dtype, n_elems, block_bytes,
+                                              chunk_bytes, d_table, d_out, out_cap, d_status, stream)
 
 
 def uzip_status_str(status: int) -> str:
@@ -295,6 +313,36 @@ def compress_chunked(x: torch.Tensor, block_bytes: int, chunk_bytes: int, dtype=
     if check and chunks:
         check_sizes(sizes[:chunks], "uzip_compress_chunked")
     return out, slot, sizes, flags
+
+
+def decompress_chunked(buf: torch.Tensor, slot_bytes: int, dtype, n_elems: int, block_bytes: int,
+                       chunk_bytes: int, first: int = 0, count: int | None = None, out: torch.Tensor | None = None,
+                       table: torch.Tensor | None = None, shared: bool = False, stream=None):
+    """Decode chunk streams first .. first + count - 1 of a split-send
+    producer's slots (``shared``: streams with a stream-wide table, ``table``
+    for EXTERNAL ones) into ``out``, the whole tensor's bit-pattern buffer.
+    Returns (out, device u32 status)."""
+    dt = dtype_code(dtype)
+    ce = chunk_bytes // _ELEM[dt]
+    chunks = (n_elems + ce - 1) // ce
+    if count is None:
+        count = chunks - first
+    if out is None:
+        out = torch.empty(max(n_elems, 1), dtype=_BITS[dt], device=buf.device)[:n_elems]
+    status = torch.zeros(1, dtype=torch.int32, device=buf.device)
+    cap = out.numel() * out.element_size()
+    if shared or table is not None:
+        rc = uzip_decompress_chunked_table(buf.data_ptr(), slot_bytes, first, count, dt, n_elems, block_bytes,
+                                           chunk_bytes, table.data_ptr() if table is not None else None,
+                                           out.data_ptr() if n_elems else None, cap, status.data_ptr(),
+                                           _stream(stream))
+        _check(rc, "uzip_decompress_chunked_table")
+    else:
+        rc = uzip_decompress_chunked(buf.data_ptr(), slot_bytes, first, count, dt, n_elems, block_bytes,
+                                     chunk_bytes, out.data_ptr() if n_elems else None, cap, status.data_ptr(),
+                                     _stream(stream))
+        _check(rc, "uzip_decompress_chunked")
+    return out, status
 
 
 _MODE = {"per_block": TABLE_PER_BLOCK, "sampled": TABLE_SAMPLED, "external": TABLE_EXTERNAL}

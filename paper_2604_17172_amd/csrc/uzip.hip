@@ -109,6 +109,17 @@ struct DecodeArgs {
   uint8_t *out;
   uint32_t *dstatus;
   const uint16_t *table;  // the caller's table (streams of table mode 2)
+  // chunk streams of the split-send producer (bpc > 0): chunk c's stream in
+  // the slot at in + c slot_bytes, its elements at out + c chunk_elems E;
+  // the launch decodes chunks [first_chunk, first_chunk + n_chunks), bpc
+  // blocks of block_elems each (the tensor's last chunk: fewer).  bpc == 0:
+  // one stream of n elements at in, its block count from its header.
+  uint64_t slot_bytes;
+  uint64_t chunk_elems;
+  uint64_t first_chunk;
+  uint64_t n_chunks;
+  uint32_t bpc;
+  uint32_t block_elems;
 };
 
 // first error wins
@@ -1574,19 +1585,28 @@ __device__ inline void load_raw_full(const uint8_t *plane, uint64_t first, uint3
   }
 }
 
-template <int DT, bool SHARED = false>
-__global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
+// The header of one stream checked (and, for a stream-wide table, its
+// lookup table built): its place and geometry.
+struct DecStream {
+  const uint8_t *s;
+  uint8_t *out;
+  uint64_t n, total;
+  uint32_t be, nb;
+  Geom g;
+};
+template <int DT, bool SHARED>
+__device__ bool open_stream(const DecodeArgs &a, uint64_t c, DecStream &st, uint32_t *lut, uint16_t *cum_s,
+                            uint16_t *f_s) {
   constexpr int E = (DT == 2) ? 4 : 2;
-  constexpr int NW = 4 * (E / 2);
-  __shared__ uint32_t lut[kM];
-  __shared__ __align__(16) uint8_t ring[kDecRingBytes];
-  // the table-build scratch (cum, f) lives in the ring before the ring fills
-  uint16_t *cum_s = (uint16_t *)ring, *f_s = (uint16_t *)ring + 256;
-  const uint32_t lane = lane_id();
-  const uint8_t *s = a.in;
-  if (a.in_bytes < kHeaderBytes) {
-    if (blockIdx.x == 0 && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
-    return;
+  const bool chunked = a.bpc != 0;
+  st.s = a.in + (chunked ? c * a.slot_bytes : 0);
+  st.out = a.out + (chunked ? c * a.chunk_elems * E : 0);
+  st.n = chunked ? ((a.n - c * a.chunk_elems) < a.chunk_elems ? a.n - c * a.chunk_elems : a.chunk_elems) : a.n;
+  const uint64_t cap = chunked ? a.slot_bytes : a.in_bytes;
+  const uint8_t *s = st.s;
+  if (cap < kHeaderBytes) {
+    st.nb = 0;
+    return false;
   }
   const uint32_t be = ld32(s + 8);
   const uint32_t nb = ld32(s + 12);
@@ -1596,9 +1616,10 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
   const uint32_t mode = s[7];
   bool ok = ld32(s) == kMagic && s[4] == kVersion && s[5] == DT && s[6] == kProbBits &&
             (SHARED ? ((mode == 1) || (mode == 2 && a.table != nullptr)) : mode == 0) &&
-            ld64(s + 16) == a.n && be > 0 && (be & (be - 1)) == 0 && (uint64_t)be * E >= kMinBlockBytes &&
-            (uint64_t)be * E <= kMaxBlockBytes && (uint64_t)nb == (a.n + be - 1) / be && total <= a.in_bytes;
-  Geom g = make_geom(a.n, ok ? be : 1, E);
+            ld64(s + 16) == st.n && be > 0 && (be & (be - 1)) == 0 && (uint64_t)be * E >= kMinBlockBytes &&
+            (uint64_t)be * E <= kMaxBlockBytes && (uint64_t)nb == (st.n + be - 1) / be && total <= cap &&
+            (!chunked || be == a.block_elems);
+  Geom g = make_geom(st.n, ok ? be : 1, E);
   const uint64_t table_off = g.raw_off;
   if (SHARED && mode == 1 && nb > 0) {
     g.raw_off += kTableBytes;
@@ -1610,24 +1631,75 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
     ok = build_lut_shared(mode == 1 ? (const uint16_t *)(s + table_off) : a.table, lut, cum_s, f_s);
     __syncthreads();
   }
-  if (!ok) {
-    if (blockIdx.x == 0 && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
-    return;
+  st.be = be;
+  st.nb = ok ? nb : 0;
+  st.total = total;
+  st.g = g;
+  return ok;
+}
+
+// the stream's sections end where its header says it ends
+__device__ inline bool stream_end_ok(const DecStream &st) {
+  const uint64_t endall = st.nb ? 16ull * (ld32(st.s + kHeaderBytes + 4 * (st.nb - 1)) & ~kStoredBit) : 0;
+  return st.g.coded_off + endall == st.total;
+}
+
+template <int DT, bool SHARED = false>
+__global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
+  constexpr int E = (DT == 2) ? 4 : 2;
+  constexpr int NW = 4 * (E / 2);
+  __shared__ uint32_t lut[kM];
+  __shared__ __align__(16) uint8_t ring[kDecRingBytes];
+  // the table-build scratch (cum, f) lives in the ring before the ring fills
+  uint16_t *cum_s = (uint16_t *)ring, *f_s = (uint16_t *)ring + 256;
+  const uint32_t lane = lane_id();
+  DecStream st;
+  uint64_t cur = 0, n_work = 0;
+  bool ok = true;
+  if (a.bpc == 0) {
+    // one stream
+    ok = open_stream<DT, SHARED>(a, 0, st, lut, cum_s, f_s);
+    if (!ok) {
+      if (blockIdx.x == 0 && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
+      return;
+    }
+    if (blockIdx.x == 0 && lane == 0 && !stream_end_ok(st)) report(a.dstatus, UZIP_ECORRUPT);
+    n_work = st.nb;
+  } else {
+    // chunk streams: a header is opened when the walk reaches its chunk
+    cur = ~0ull;
+    n_work = a.n_chunks * a.bpc;
   }
-  if (blockIdx.x == 0 && lane == 0) {
-    uint64_t endall = nb ? 16ull * (ld32(s + kHeaderBytes + 4 * (nb - 1)) & ~kStoredBit) : 0;
-    if (g.coded_off + endall != total) report(a.dstatus, UZIP_ECORRUPT);
-  }
-  const uint8_t *raw_plane = s + g.raw_off;
 
   // blocks are independent: a grid-stride walk, no ticket (one counter for
   // every wave costs more in queueing than it recovers in balance)
-  for (uint32_t b = blockIdx.x; b < nb; b += gridDim.x) {
+  for (uint64_t gb = blockIdx.x; gb < n_work; gb += gridDim.x) {
+    uint32_t b = (uint32_t)gb;
+    if (a.bpc != 0) {
+      const uint64_t q = gb / a.bpc;
+      const uint64_t c = a.first_chunk + q;
+      b = (uint32_t)(gb - q * a.bpc);
+      if (c != cur) {
+        cur = c;
+        ok = open_stream<DT, SHARED>(a, c, st, lut, cum_s, f_s);
+      }
+      if (!ok) {
+        if (b == 0 && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
+        continue;
+      }
+      if (b >= st.nb) continue;  // the tensor's last chunk has fewer blocks
+      if (b == 0 && lane == 0 && !stream_end_ok(st)) report(a.dstatus, UZIP_ECORRUPT);
+    }
+    const uint8_t *s = st.s;
+    const Geom &g = st.g;
+    const uint32_t be = st.be;
+    const uint64_t total = st.total;
+    const uint8_t *raw_plane = s + g.raw_off;
     const uint32_t d = ld32(s + kHeaderBytes + 4 * b);
     const uint64_t start = b ? 16ull * (ld32(s + kHeaderBytes + 4 * (b - 1)) & ~kStoredBit) : 0;
     const uint64_t end = 16ull * (d & ~kStoredBit);
     const uint64_t blk0 = (uint64_t)b * be;
-    const uint32_t n_b = (uint32_t)((a.n - blk0) < be ? (a.n - blk0) : be);
+    const uint32_t n_b = (uint32_t)((st.n - blk0) < be ? (st.n - blk0) : be);
     const uint32_t rounds = (n_b + kRound - 1) / kRound;
     bool bad = !(end >= start && g.coded_off + end <= total);
     const uint8_t *sec = s + g.coded_off + start;
@@ -1657,7 +1729,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
         load_raw<E>(raw_plane, blk0 + i0, valid, raw);
         uint32_t w[NW];
         merge_group<DT>(sym, raw, w);
-        store_words<E>(a.out, blk0 + i0, valid, w);
+        store_words<E>(st.out, blk0 + i0, valid, w);
       }
       continue;
     }
@@ -1697,7 +1769,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
     __syncthreads();
     uint32_t p = 0, rb = wb & (kDecRingBytes - 1);
     const uint32_t full = n_b / kRound;
-    uint8_t *outp = a.out + blk0 * E;
+    uint8_t *outp = st.out + blk0 * E;
     const uint8_t *rawp = raw_plane + blk0 * (E - 1);
     uint32_t rawA[6] = {0, 0, 0, 0, 0, 0}, rawB[6] = {0, 0, 0, 0, 0, 0};
     // round 0's raw bytes; with no full round a dummy load of the stream
@@ -1787,7 +1859,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
         load_raw<E>(raw_plane, blk0 + i0, valid, raw);
         uint32_t w[NW];
         merge_entries<DT>(e, raw, w);
-        store_words<E>(a.out, blk0 + i0, valid, w);
+        store_words<E>(st.out, blk0 + i0, valid, w);
       }
     }
     asm volatile("" ::"v"(pad_load));
@@ -3000,6 +3072,9 @@ uzip_status uzip_compress_chunked_table(const void *d_in, uint64_t n_elems, uzip
 }  // extern "C"
 
 namespace {
+uzip_status launch_decode_args(DecodeArgs &a, uzip_dtype dtype, uint64_t most, const DeviceInfo &info,
+                               hipStream_t stream, bool shared);
+
 uzip_status launch_decode(const void *d_in, size_t in_bytes, uzip_dtype dtype, uint64_t n_elems, void *d_out,
                           size_t out_cap, uint32_t *d_status, void *d_ws, size_t ws_bytes, hipStream_t stream,
                           bool shared, const uint16_t *d_table) {
@@ -3021,8 +3096,14 @@ uzip_status launch_decode(const void *d_in, size_t in_bytes, uzip_dtype dtype, u
   a.out = (uint8_t *)d_out;
   a.dstatus = d_status;
   a.table = d_table;
-  // an occupancy-sized grid; its waves walk the blocks grid-stride
+  // at most one wave per block of the smallest size
   const uint64_t most = (n_elems + (kMinBlockBytes / elem_bytes(dtype)) - 1) / (kMinBlockBytes / elem_bytes(dtype));
+  return launch_decode_args(a, dtype, most, info, stream, shared);
+}
+
+uzip_status launch_decode_args(DecodeArgs &a, uzip_dtype dtype, uint64_t most, const DeviceInfo &info,
+                               hipStream_t stream, bool shared) {
+  // an occupancy-sized grid; its waves walk the blocks grid-stride
   static const void *const dec_tab[10] = {
       (const void *)decode_kernel<0>,       (const void *)decode_kernel<1>,       (const void *)decode_kernel<2>,
       (const void *)decode_kernel<3>,       (const void *)decode_kernel<4>,       (const void *)decode_kernel<0, true>,
@@ -3037,6 +3118,45 @@ uzip_status launch_decode(const void *d_in, size_t in_bytes, uzip_dtype dtype, u
   void *args[] = {&a};
   if (hipLaunchKernel(fn, dim3((unsigned)grid), dim3(64), args, 0, stream) != hipSuccess) return UZIP_EHIP;
   return UZIP_OK;
+}
+
+uzip_status launch_decode_chunked(const void *d_in, size_t slot_bytes, uint64_t first_chunk, uint64_t n_chunks,
+                                  uzip_dtype dtype, uint64_t n_elems, uint32_t block_bytes, uint64_t chunk_bytes,
+                                  void *d_out, size_t out_cap, uint32_t *d_status, hipStream_t stream, bool shared,
+                                  const uint16_t *d_table) {
+  if (!valid_dtype(dtype) || !valid_block(block_bytes)) return UZIP_EINVAL;
+  if (chunk_bytes == 0 || chunk_bytes % block_bytes) return UZIP_EINVAL;
+  if (d_table != nullptr && !aligned16(d_table)) return UZIP_EINVAL;
+  const uint32_t E = elem_bytes(dtype), be = block_bytes / E;
+  const uint64_t ce = chunk_bytes / E;
+  if (ce / be >= 0x7FFFFFFFull) return UZIP_EINVAL;
+  const uint64_t chunks = (n_elems + ce - 1) / ce;
+  if (first_chunk > chunks || n_chunks > chunks - first_chunk) return UZIP_EINVAL;
+  if (n_chunks == 0) return UZIP_OK;
+  if (d_in == nullptr || !aligned16(d_in) || (slot_bytes & 15u) || slot_bytes < kHeaderBytes) return UZIP_EINVAL;
+  if (d_out == nullptr || !aligned16(d_out)) return UZIP_EINVAL;
+  // the output covers the tensor up to the end of the last chunk decoded
+  const uint64_t end = (first_chunk + n_chunks) * ce < n_elems ? (first_chunk + n_chunks) * ce : n_elems;
+  if (out_cap < end * E) return UZIP_ENOSPC;
+  if (n_chunks * (ce / be) >= 0x7FFFFFFFull) return UZIP_EINVAL;
+  DeviceInfo info;
+  uzip_status st = device_info(info);
+  if (st != UZIP_OK) return st;
+  DecodeArgs a;
+  memset(&a, 0, sizeof(a));
+  a.in = (const uint8_t *)d_in;
+  a.n = n_elems;
+  a.dtype = (uint32_t)dtype;
+  a.out = (uint8_t *)d_out;
+  a.dstatus = d_status;
+  a.table = d_table;
+  a.slot_bytes = slot_bytes;
+  a.chunk_elems = ce;
+  a.first_chunk = first_chunk;
+  a.n_chunks = n_chunks;
+  a.bpc = (uint32_t)(ce / be);
+  a.block_elems = be;
+  return launch_decode_args(a, dtype, n_chunks * a.bpc, info, stream, shared);
 }
 }  // namespace
 
@@ -3053,6 +3173,21 @@ uzip_status uzip_decompress_table(const void *d_in, size_t in_bytes, uzip_dtype 
                                   void *d_ws, size_t ws_bytes, hipStream_t stream) {
   return launch_decode(d_in, in_bytes, dtype, n_elems, d_out, out_cap, d_status, d_ws, ws_bytes, stream, true,
                        d_table);
+}
+
+uzip_status uzip_decompress_chunked(const void *d_in, size_t slot_bytes, uint64_t first_chunk, uint64_t n_chunks,
+                                    uzip_dtype dtype, uint64_t n_elems, uint32_t block_bytes, uint64_t chunk_bytes,
+                                    void *d_out, size_t out_cap, uint32_t *d_status, hipStream_t stream) {
+  return launch_decode_chunked(d_in, slot_bytes, first_chunk, n_chunks, dtype, n_elems, block_bytes, chunk_bytes,
+                               d_out, out_cap, d_status, stream, false, nullptr);
+}
+
+uzip_status uzip_decompress_chunked_table(const void *d_in, size_t slot_bytes, uint64_t first_chunk,
+                                          uint64_t n_chunks, uzip_dtype dtype, uint64_t n_elems,
+                                          uint32_t block_bytes, uint64_t chunk_bytes, const uint16_t *d_table,
+                                          void *d_out, size_t out_cap, uint32_t *d_status, hipStream_t stream) {
+  return launch_decode_chunked(d_in, slot_bytes, first_chunk, n_chunks, dtype, n_elems, block_bytes, chunk_bytes,
+                               d_out, out_cap, d_status, stream, true, d_table);
 }
 
 uzip_status uzip_build_table(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint16_t *d_table,

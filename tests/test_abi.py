@@ -66,6 +66,26 @@ def test_invalid_arguments_rejected_on_host():
         assert uz.uzip_reduce_fused([16, 32], [64, 64], 2, None, dt, 10, 65536, 48, 1 << 20, None, None,
                                     None, 64, 1 << 20, None) == uz.EINVAL
     assert uz.uzip_max_compressed_size(5, 100, 65536) == 0
+    # batched chunk decode: a range past the tensor's chunks, a chunk size
+    # that is not a multiple of the block size, a misaligned slot size, an
+    # output that does not reach the last chosen chunk; an empty range is a
+    # no-op that touches nothing
+    n, bb, cb = 3 * (1 << 19) + 5, 65536, 1 << 20              # 4 chunks
+    args = dict(dtype=0, n_elems=n, block_bytes=bb, chunk_bytes=cb)
+
+    def dc(first, count, slot=1 << 20, cap=2 * n, cbytes=cb, **kw):
+        a = {**args, "chunk_bytes": cbytes, **kw}
+        return uz.uzip_decompress_chunked(16, slot, first, count, a["dtype"], a["n_elems"], a["block_bytes"],
+                                          a["chunk_bytes"], 32, cap, None, None)
+    assert dc(3, 2) == uz.EINVAL and dc(5, 0) == uz.EINVAL
+    assert dc(0, 1, cbytes=cb + 4096) == uz.EINVAL
+    assert dc(0, 1, slot=(1 << 20) + 8) == uz.EINVAL
+    assert dc(0, 2, cap=2 * (1 << 20) - 2) == uz.ENOSPC
+    assert dc(0, 4, cap=2 * n - 2) == uz.ENOSPC
+    assert dc(2, 0) == uz.OK and dc(4, 0) == uz.OK
+    assert dc(0, 1, dtype=9) == uz.EINVAL
+    assert uz.uzip_decompress_chunked_table(16, 1 << 20, 0, 1, 0, n, bb, cb, 24, 32, 2 * n, None,
+                                            None) == uz.EINVAL   # misaligned table
 
 
 def test_workspace_sizes_are_bounded():

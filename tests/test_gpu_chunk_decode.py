@@ -1,0 +1,164 @@
+"""GPU: the receiver side of the split-send pipeline (section 3.2.3) --
+every chunk stream the producer laid out in its slots, or a range of them,
+decoded in one launch (uzip_decompress_chunked), through the C ABI.
+
+The decoded values must equal the input bit for bit, both from the GPU
+producer's chunk streams and from the oracle's (copied into slots of the
+same layout), only the chosen chunks' elements may be written, and a
+corrupt chunk is reported without stopping the others."""
+import struct
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import ref
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+EB = {"bf16": 2, "fp16": 2, "fp32": 4, "e4m3fn": 2, "e5m2": 2}
+NP_BITS = {"bf16": np.int16, "fp16": np.int16, "fp32": np.int32, "e4m3fn": np.int16, "e5m2": np.int16}
+SENTINEL = {2: 0x5A5A, 4: 0x5A5A5A5A}
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def uz():
+    import paper_2604_17172_amd as m
+    return m
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host_bits(t, dtype):
+    return t.cpu().numpy().view(np.uint16 if EB[dtype] == 2 else np.uint32)
+
+
+def data(dtype, n, seed):
+    if dtype in ("e4m3fn", "e5m2"):
+        return W.normal_fp8_pairs(n, dtype, seed=seed)
+    if dtype == "bf16":
+        return W.normal_bf16(n, seed=seed)
+    if dtype == "fp16":
+        return W.grad_fp16(n, seed=seed)
+    return W.grad_fp32(n, seed=seed)
+
+
+def sentinel_out(dtype, n):
+    out = torch.empty(max(n, 1), dtype=torch.int16 if EB[dtype] == 2 else torch.int32, device="cuda")[:n]
+    out.view(torch.uint8).fill_(0x5A)
+    return out
+
+
+def oracle_slots(streams, slot):
+    buf = np.zeros(slot * len(streams), dtype=np.uint8)
+    for c, w in enumerate(streams):
+        assert w.size <= slot
+        buf[c * slot:c * slot + w.size] = w
+    return dev(buf)
+
+
+@pytest.mark.parametrize("dtype,bb,cb,n", [("bf16", 65536, 1 << 20, 3 * (1 << 19) + 77_777),
+                                           ("fp32", 262144, 1 << 20, 2 * (1 << 18) + 1),
+                                           ("fp16", 4096, 16384, 100_000),
+                                           ("e4m3fn", 4096, 16384, 70_001),
+                                           ("bf16", 65536, 65536, 5 * 32768)])
+def test_all_chunks_in_one_launch(uz, dtype, bb, cb, n):
+    say(f"[chunk-decode] dtype={dtype} n={n} block={bb} chunk={cb}")
+    x = data(dtype, n, seed=61)
+    xt = dev(x.view(NP_BITS[dtype]))
+    out, slot, sizes, flags = uz.compress_chunked(xt, bb, cb, dtype=dtype, epoch=2, check=True)
+    y, st = uz.decompress_chunked(out, slot, dtype, n, bb, cb)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    assert np.array_equal(host_bits(y, dtype), x)
+    # the oracle's chunk streams in slots of the same size
+    want = ref.compress_chunked(x, dtype, bb, cb)
+    y2, st2 = uz.decompress_chunked(oracle_slots(want, slot), slot, dtype, n, bb, cb)
+    torch.cuda.synchronize()
+    assert int(st2.item()) == 0
+    assert np.array_equal(host_bits(y2, dtype), x)
+
+
+def test_a_range_of_chunks_writes_only_its_elements(uz):
+    dtype, bb, cb, n = "bf16", 65536, 1 << 20, 7 * (1 << 19) + 12_345   # 8 chunks, the last ragged
+    ce = cb // 2
+    say(f"[chunk-decode] ranges n={n}")
+    x = data(dtype, n, seed=62)
+    out, slot, _, _ = uz.compress_chunked(dev(x.view(np.int16)), bb, cb, dtype=dtype, epoch=3, check=True)
+    for first, count in ((2, 3), (0, 1), (7, 1), (5, 3), (3, 0)):
+        y = sentinel_out(dtype, n)
+        _, st = uz.decompress_chunked(out, slot, dtype, n, bb, cb, first=first, count=count, out=y)
+        torch.cuda.synchronize()
+        assert int(st.item()) == 0
+        h = host_bits(y, dtype)
+        lo, hi = first * ce, min(n, (first + count) * ce)
+        assert np.array_equal(h[lo:hi], x[lo:hi]), (first, count)
+        assert np.all(h[:lo] == SENTINEL[2]) and np.all(h[hi:] == SENTINEL[2]), (first, count)
+
+
+def test_chunks_with_stream_wide_tables(uz):
+    dtype, bb, cb = "bf16", 65536, 1 << 20
+    x = np.ascontiguousarray(W.weight_sync(136_134_656 + 3_000_000)[-6_000_000:])
+    n = x.size
+    xt = dev(x.view(np.int16))
+    say(f"[chunk-decode] sampled tables per chunk n={n}")
+    out, slot, _, _ = uz.compress_chunked_table(xt, bb, cb, "sampled", dtype=dtype, epoch=4)
+    y, st = uz.decompress_chunked(out, slot, dtype, n, bb, cb, shared=True)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0 and np.array_equal(host_bits(y, dtype), x)
+    want = ref.compress_chunked(x, dtype, bb, cb, "sampled")
+    y2, st2 = uz.decompress_chunked(oracle_slots(want, slot), slot, dtype, n, bb, cb, shared=True)
+    torch.cuda.synchronize()
+    assert int(st2.item()) == 0 and np.array_equal(host_bits(y2, dtype), x)
+    # a per-block chunk stream is not a table stream, and the reverse
+    pb, pslot, _, _ = uz.compress_chunked(xt, bb, cb, dtype=dtype, epoch=5)
+    _, st3 = uz.decompress_chunked(pb, pslot, dtype, n, bb, cb, shared=True)
+    _, st4 = uz.decompress_chunked(out, slot, dtype, n, bb, cb)
+    torch.cuda.synchronize()
+    assert int(st3.item()) == uz.ECORRUPT and int(st4.item()) == uz.ECORRUPT
+    # the caller's table
+    say("[chunk-decode] external table")
+    x5 = W.normal_bf16(5 * (1 << 19) + 17, seed=4)
+    t = ref.sampled_table(x5, "bf16")
+    t_dev = dev(t.astype(np.uint16).view(np.int16))
+    out5, slot5, _, _ = uz.compress_chunked_table(dev(x5.view(np.int16)), bb, cb, "external", t_dev, dtype=dtype,
+                                                  epoch=6)
+    y5, st5 = uz.decompress_chunked(out5, slot5, dtype, x5.size, bb, cb, table=t_dev)
+    _, st6 = uz.decompress_chunked(out5, slot5, dtype, x5.size, bb, cb, shared=True)   # no table
+    torch.cuda.synchronize()
+    assert int(st5.item()) == 0 and np.array_equal(host_bits(y5, dtype), x5)
+    assert int(st6.item()) == uz.ECORRUPT
+
+
+def test_a_corrupt_chunk_is_reported_and_the_others_decode(uz):
+    dtype, bb, cb, n = "bf16", 65536, 1 << 20, 4 * (1 << 19)
+    ce = cb // 2
+    x = data(dtype, n, seed=63)
+    out, slot, _, _ = uz.compress_chunked(dev(x.view(np.int16)), bb, cb, dtype=dtype, epoch=7, check=True)
+    say("[chunk-decode] corrupt chunk 2 (magic), chunk 1 (a directory entry)")
+    bad = out.clone()
+    bad[2 * slot] ^= 0xFF                      # chunk 2: magic
+    d1 = 1 * slot + 32 + 4 * 3                 # chunk 1: block 3's directory entry
+    e = struct.unpack_from("<I", bad[d1:d1 + 4].cpu().numpy().tobytes())[0]
+    bad[d1:d1 + 4] = torch.tensor(np.frombuffer(struct.pack("<I", e + 0x100000), dtype=np.uint8).copy()).cuda()
+    y = sentinel_out(dtype, n)
+    _, st = uz.decompress_chunked(bad, slot, dtype, n, bb, cb, out=y)
+    torch.cuda.synchronize()
+    assert int(st.item()) == uz.ECORRUPT
+    h = host_bits(y, dtype)
+    for c in (0, 3):
+        assert np.array_equal(h[c * ce:(c + 1) * ce], x[c * ce:(c + 1) * ce]), c
+    assert np.all(h[2 * ce:3 * ce] == SENTINEL[2])
+    # block size other than the stream's
+    _, st2 = uz.decompress_chunked(out, slot, dtype, n, 4096, cb)
+    torch.cuda.synchronize()
+    assert int(st2.item()) == uz.ECORRUPT

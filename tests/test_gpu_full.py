@@ -77,7 +77,7 @@ def check_chunked(uz, x, dtype, bb, cb, label):
         assert sz[c] == w.size, f"{label}: chunk {c} size {sz[c]} != {w.size}"
         assert np.array_equal(buf[c * slot:c * slot + w.size], w), f"{label}: chunk {c} differs"
     say(f"[full] {label}: {sz.size} chunks equal to the oracle ({time.time() - t0:.1f}s)")
-    # every chunk decodes back to its slice
+    # every chunk decodes back to its slice, one call per chunk
     y = torch.empty_like(xt)
     for c in range(sz.size):
         n_c = min(ce, x.size - c * ce)
@@ -85,6 +85,11 @@ def check_chunked(uz, x, dtype, bb, cb, label):
         assert int(st.item()) == 0
     torch.cuda.synchronize()
     assert torch.equal(y, xt)
+    # and all chunks in one launch
+    y.zero_()
+    _, st = uz.decompress_chunked(out, slot, dtype, x.size, bb, cb, out=y)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0 and torch.equal(y, xt)
 
 
 def test_normal_bf16_4MiB(uz):

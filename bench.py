@@ -123,6 +123,18 @@ def main() -> int:
     def ev():
         return torch.cuda.Event(enable_timing=True)
 
+    open_leg = [False]
+
+    def mark(name):
+        """A roctx range per leg (rocprofv3 --marker-trace attributes the
+        kernels to legs); the GPU is drained at both ends."""
+        torch.cuda.synchronize()
+        if open_leg[0]:
+            torch.cuda.nvtx.range_pop()
+        open_leg[0] = name is not None
+        if name is not None:
+            torch.cuda.nvtx.range_push(name)
+
     def timed(fn, reps, flush=None):
         """ms of each of `reps` calls of fn (HIP events on the launch stream),
         after one untimed call; `flush` runs untimed before each call."""
@@ -154,6 +166,7 @@ def main() -> int:
     dws = torch.empty(uz.uzip_workspace_size(uz.OP_DECOMPRESS, uz.BF16, n, bb), dtype=torch.uint8, device=dev)
 
     size = status = None
+    mark("headline")
     for _ in range(args.warmup):
         _, size = uz.compress(x, bb, dtype="bf16", out=out, ws=ws)
         _, status = uz.decompress(out, "bf16", n, out=y, ws=dws)
@@ -203,6 +216,7 @@ def main() -> int:
                 "compress_frac": frac(alg_comp, c_ms), "decompress_frac": frac(alg_dec, d_ms)}
 
     # ---------------- measured device-copy bandwidth (1 GiB, read + write) ----------------
+    mark("device_copy")
     src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
     dst = torch.empty_like(src)
     cp = timed(lambda: dst.copy_(src), 5)
@@ -227,6 +241,7 @@ def main() -> int:
             flush_buf.fill_(flush_n[0] & 0xFF)
 
         # ------------- split-send producer: 4 MiB chunks, host-mapped flags -------------
+        mark("chunked_weight_sync")
         cb = 4 << 20
         chunks = (nbytes + cb - 1) // cb
         flags = torch.zeros(2 * chunks, dtype=torch.int32).pin_memory()
@@ -283,6 +298,7 @@ def main() -> int:
         del cout, cws
 
         # ------------- 4 MiB bf16 N(0, 0.02), 64 KiB blocks (after a cache flush) -------------
+        mark("normal_bf16_4MiB")
         x1h = W.normal_bf16()
         x1 = torch.from_numpy(x1h.view(np.int16)).to(dev)
         n1 = x1h.size
@@ -311,6 +327,7 @@ def main() -> int:
         # ------------- fp32 / fp16 gradients, 256 KiB blocks -------------
         for name, gen, code, e_bytes in (("grad_fp32_1GiB", W.grad_fp32, uz.FP32, 4),
                                          ("grad_fp16_512MiB", W.grad_fp16, uz.FP16, 2)):
+            mark(name)
             gh = gen()
             ng = gh.size
             gt = torch.from_numpy(gh.view(np.int32 if e_bytes == 4 else np.int16)).to(dev)
@@ -334,6 +351,7 @@ def main() -> int:
             del gt, go, gw, gy
 
         # ------------- 2 GiB bf16 KV cache, 1 MiB chunks -------------
+        mark("kv_chunked")
         kh = W.kv_cache()
         nk = kh.size
         kt = torch.from_numpy(kh.view(np.int16)).to(dev)
@@ -367,15 +385,18 @@ def main() -> int:
                 uz.uzip_decompress(kout.data_ptr() + c * kslot, kslot, uz.BF16, kce, ky.data_ptr() + 2 * c * kce,
                                    2 * kce, kst.data_ptr(), None, 0, s_ptr)
 
+        mark("kv_chunk_decode_calls")
         kd_ms = timed(kdecode, 3)
         assert int(kst.item()) == 0 and torch.equal(kt, ky)
         # the same chunk streams, all decoded in one launch
+        mark("kv_chunk_decode_batched")
         ky.zero_()
         kb_ms = timed(lambda: uz.uzip_decompress_chunked(kout.data_ptr(), kslot, 0, kchunks, uz.BF16, nk, bb, kcb,
                                                          ky.data_ptr(), 2 * nk, kst.data_ptr(), s_ptr), reps)
         assert int(kst.item()) == 0 and torch.equal(kt, ky)
         del kout, kws, ky
         # the same tensor as one stream (one launch each way)
+        mark("kv_whole_stream")
         ko = torch.empty(uz.uzip_max_compressed_size(uz.BF16, nk, bb), dtype=torch.uint8, device=dev)
         kw = torch.empty(uz.uzip_workspace_size(uz.OP_COMPRESS, uz.BF16, nk, bb), dtype=torch.uint8, device=dev)
         ky2 = torch.empty_like(kt)
@@ -399,6 +420,7 @@ def main() -> int:
         del kt, ko, kw, ky2
 
         # ------------- fused reduce: 8 compressed bf16 shares [1024 x 8192] -------------
+        mark("reduce_inputs")
         shares = W.reduce_slices()
         rn = shares[0].size
         streams = []
@@ -416,6 +438,7 @@ def main() -> int:
 
         # the inputs (~90 MB) fit the 256 MB Infinity Cache: warm runs, and
         # cold ones each after a 512 MiB write that evicts them
+        mark("reduce_8x16MiB")
         times = timed(reduce_call, reps)
         cold = timed(reduce_call, reps, flush)
         _, rsz, raw, rst = res["r"]
@@ -436,6 +459,7 @@ def main() -> int:
         if not args.no_reduce_full:
             # the other reading of the activation slices: each input is the
             # whole [8192 x 8192] tensor (128 MiB), 2048 blocks per input
+            mark("reduce_full_inputs")
             fshares = W.reduce_slices(tokens=8192)
             fn_ = fshares[0].size
             fstreams = []
@@ -451,6 +475,7 @@ def main() -> int:
             def freduce():
                 res["f"] = uz.reduce_fused(fstreams, "bf16", fn_, bb, out=fout, ws=fws)
 
+            mark("reduce_full_tensor")
             times = timed(freduce, reps)
             _, fsz, fraw, fst = res["f"]
             assert int(fst.item()) == 0
@@ -469,6 +494,7 @@ def main() -> int:
             res.clear()
 
         # ------------- stream-wide tables: the same buffer, one table per stream -------------
+        mark("tables")
         tws = torch.empty(uz.uzip_workspace_size(uz.OP_COMPRESS_TABLE, uz.BF16, n, bb), dtype=torch.uint8, device=dev)
         tout = torch.empty(cap + uz.TABLE_BYTES, dtype=torch.uint8, device=dev)
         ty = torch.empty_like(x)
@@ -494,6 +520,7 @@ def main() -> int:
             log(f"[bench] table {mode}: ratio {tsize / nbytes:.4f} compress {fc:.3f} ms decompress {fd:.3f} ms")
         del tws, tout, ty
         # split-send producer with a table per 4 MiB chunk (sampled from the chunk's first 256 KiB)
+        mark("chunked_sampled_tables")
         cws2 = torch.empty(uz.uzip_workspace_size(uz.OP_CHUNKED_TABLE, uz.BF16, n, bb, cb), dtype=torch.uint8,
                            device=dev)
         slot2 = (uz.uzip_max_compressed_size(uz.BF16, cb // 2, bb) + uz.TABLE_BYTES + 255) // 256 * 256
@@ -515,6 +542,7 @@ def main() -> int:
 
         # ------------- FP8 pairs: 1 GiB of e4m3fn / e5m2 values N(0, 1) -------------
         for fmt, code in (("e4m3fn", uz.E4M3FN), ("e5m2", uz.E5M2)):
+            mark(f"fp8_{fmt}")
             f8 = torch.from_numpy(W.normal_fp8_pairs(n, fmt).view(np.int16)).to(dev)
             fout = torch.empty(uz.uzip_max_compressed_size(code, n, bb), dtype=torch.uint8, device=dev)
             fws = torch.empty(uz.uzip_workspace_size(uz.OP_COMPRESS, code, n, bb), dtype=torch.uint8, device=dev)
@@ -537,10 +565,12 @@ def main() -> int:
 
     if args.calibrate_copy:
         # a plain device copy of known size, for scaling the HBM counters
+        mark("calibration_copy")
         for _ in range(3):
             dst.copy_(src)
         torch.cuda.synchronize()
 
+    mark(None)
     cpu = None
     if not args.no_cpu_baseline:
         # the oracle as it stands, on independent 4 MiB chunks of the same

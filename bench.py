@@ -24,6 +24,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -41,10 +42,17 @@ def log(msg: str) -> None:
 
 
 def kernel_source_hash() -> str:
+    """sha256 of the kernel sources' code: comments, trailing blanks and
+    empty lines removed, so that editing a comment keeps the measured
+    traffic valid while any change to the code does not."""
     h = hashlib.sha256()
     for name in ("uzip.hip", "uzip_device.h"):
-        with open(os.path.join(os.path.dirname(KERNEL_SRC), name), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(os.path.dirname(KERNEL_SRC), name)) as fh:
+            text = re.sub(r"/\*.*?\*/", "", fh.read(), flags=re.S)
+        for line in text.splitlines():
+            line = re.sub(r"//.*", "", line).rstrip()
+            if line:
+                h.update(line.encode() + b"\n")
     return h.hexdigest()
 
 
@@ -56,7 +64,7 @@ def measured_traffic(kernel: str):
             t = json.load(fh)
     except (OSError, ValueError):
         return None
-    if t.get("kernel_source_sha256") != kernel_source_hash():
+    if t.get("kernel_code_sha256") != kernel_source_hash():
         return None
     k = t.get("kernels", {}).get(kernel)
     if not k:

@@ -26,6 +26,9 @@
 //                   offset is read from the directory, its decode table
 //                   (2048 x u32) is built in LDS, its words are staged
 //                   through an LDS ring and the 64 states decode forwards.
+//                   For the receiver of the split-send producer the walk
+//                   covers the blocks of a range of chunk streams at once,
+//                   opening each chunk's header when it reaches that chunk.
 //   reduce_fused_kernel (fused reduce)  one workgroup per output block
 //                   decodes block b of up to eight inputs in parallel waves,
 //                   round by round; a further wave adds them in binary32 in

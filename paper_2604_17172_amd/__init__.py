@@ -211,12 +211,13 @@ def check_sizes(sizes: torch.Tensor, what: str) -> None:
 
 
 def compress(x: torch.Tensor, block_bytes: int = 65536, dtype=None, out: torch.Tensor | None = None,
-             ws: torch.Tensor | None = None, stream=None, check: bool = False):
+             ws: torch.Tensor | None = None, stream=None, check: bool = False, size: torch.Tensor | None = None):
     """Compress a contiguous CUDA tensor (bf16/fp16/fp32/float8, or an
     int16/int32 bit view with ``dtype`` given; float8 tensors are coded as
-    pairs of values).  Returns (stream buffer, device u64 size).  With
-    ``check`` the call waits for the GPU and raises UzipError(ETIMEOUT) if
-    the stream was marked invalid (size 0)."""
+    pairs of values).  Returns (stream buffer, device u64 size; ``size``, a
+    device int64[1], is reused when given).  With ``check`` the call waits
+    for the GPU and raises UzipError(ETIMEOUT) if the stream was marked
+    invalid (size 0)."""
     assert x.is_cuda and x.is_contiguous()
     dt = dtype_code(dtype if dtype is not None else x.dtype)
     n = _n_elems(x, dt)
@@ -228,7 +229,8 @@ def compress(x: torch.Tensor, block_bytes: int = 65536, dtype=None, out: torch.T
     wsb = uzip_workspace_size(OP_COMPRESS, dt, n, block_bytes)
     if ws is None:
         ws = _dev_empty(wsb, x.device)
-    size = torch.zeros(1, dtype=torch.int64, device=x.device)
+    if size is None:
+        size = torch.zeros(1, dtype=torch.int64, device=x.device)
     _check(uzip_compress(x.data_ptr() if n else None, n, dt, block_bytes, out.data_ptr(), out.numel(),
                          size.data_ptr(), ws.data_ptr(), ws.numel(), _stream(stream)), "uzip_compress")
     if check:
@@ -237,13 +239,17 @@ def compress(x: torch.Tensor, block_bytes: int = 65536, dtype=None, out: torch.T
 
 
 def decompress(s: torch.Tensor, dtype, n_elems: int, out: torch.Tensor | None = None,
-               in_bytes: int | None = None, ws: torch.Tensor | None = None, stream=None):
+               in_bytes: int | None = None, ws: torch.Tensor | None = None, stream=None,
+               status: torch.Tensor | None = None):
     """Decompress a stream of n_elems elements (FP8: pairs).  Returns
-    (bit-pattern tensor, int16 per FP8 pair; device u32 status)."""
+    (bit-pattern tensor, int16 per FP8 pair; device u32 status).  A
+    ``status`` given (device int32[1]) is reused as it is: the decoder only
+    writes it on an error, so the caller zeroes it."""
     dt = dtype_code(dtype)
     if out is None:
         out = torch.empty(max(n_elems, 1), dtype=_BITS[dt], device=s.device)[:n_elems]
-    status = torch.zeros(1, dtype=torch.int32, device=s.device)
+    if status is None:
+        status = torch.zeros(1, dtype=torch.int32, device=s.device)
     nbytes = s.numel() * s.element_size() if in_bytes is None else in_bytes
     wsb = uzip_workspace_size(OP_DECOMPRESS, dt, n_elems, 65536, 0)
     if ws is None:

@@ -743,10 +743,10 @@ template <int E, bool NT = false>
 __device__ __forceinline__ void load_round(const uint8_t *round_base, uint32_t w[4 * (E / 2)]) {
   typedef uint32_t v4u __attribute__((ext_vector_type(4)));
   const v4u *p = (const v4u *)round_base + (E / 2) * lane_id();
-  // NT: the block is read once (its symbols stay in registers), so its
-  // lines need not stay in the caches (compress alone 0.586 -> 0.548 ms,
-  // interleaved A/B on the 1 GiB buffer); a block re-read in the coding
-  // pass keeps ordinary loads
+  // NT for a last read: a block whose symbols stay in registers is read
+  // once, so its lines need not stay in the caches (compress alone 0.586 ->
+  // 0.548 ms, interleaved A/B on the 1 GiB buffer); a block re-read in the
+  // coding pass keeps ordinary loads in pass 1 and takes NT ones there
   const v4u a = NT ? __builtin_nontemporal_load(p) : p[0];
   w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
   if (E == 4) {
@@ -1319,14 +1319,16 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         if (gi > 0) shift_up(S);
       }
     } else if constexpr (!REDUCE) {
-      // larger blocks: the block re-read backwards, four rounds ahead, and
-      // the LDS window sliding into the workgroup's slot as for small ones
+      // larger blocks: the block re-read backwards, four rounds ahead (its
+      // last read: non-temporal; fp16 in 256 KiB blocks 0.503 -> 0.457 ms,
+      // fp32 0.749 -> 0.733 ms, interleaved A/B), and the LDS window sliding
+      // into the workgroup's slot as for small ones
       constexpr int P = 4;
       uint32_t pb[P][NW];
       if (full > 0) {
 #pragma unroll
         for (int u = 0; u < P; ++u)
-          load_round<E>(src_blk + (uint64_t)((int)full - 1 - u >= 0 ? (int)full - 1 - u : 0) * kRound * E, pb[u]);
+          load_round<E, true>(src_blk + (uint64_t)((int)full - 1 - u >= 0 ? (int)full - 1 - u : 0) * kRound * E, pb[u]);
       }
       for (int r0 = (int)full - 1; r0 >= 0 && !stored; r0 -= P) {
 #pragma unroll
@@ -1344,7 +1346,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
             split_group<DT>(pb[u], gr);
             // round r - P into the buffer just used (round 0 again once below it)
             const int rn = r - P;
-            load_round<E>(src_blk + (uint64_t)(rn >= 0 ? rn : 0) * kRound * E, pb[u]);
+            load_round<E, true>(src_blk + (uint64_t)(rn >= 0 ? rn : 0) * kRound * E, pb[u]);
             uint4 e[8];
 #pragma unroll
             for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];

@@ -111,6 +111,9 @@ def main() -> int:
     ap.add_argument("--no-extras", action="store_true", help="only the headline step")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run a 1 GiB device copy (counter calibration under rocprofv3)")
+    ap.add_argument("--fixed-preheat", action="store_true",
+                    help="untimed calls by count instead of by time (a dispatch sequence that repeats "
+                         "exactly from run to run, for attributing counter runs)")
     ap.add_argument("--no-reduce-full", action="store_true",
                     help="skip the fused reduce on the full-tensor reading (8 slices [8192 x 8192] bf16)")
     args = ap.parse_args()
@@ -145,20 +148,32 @@ def main() -> int:
             torch.cuda.nvtx.range_push(name)
 
     def timed(fn, reps, flush=None):
-        """ms of each of `reps` calls of fn (HIP events on the launch stream),
-        after one untimed call; `flush` runs untimed before each call."""
-        fn()
-        out = []
-        for _ in range(reps):
+        """ms of each of `reps` calls of fn (HIP events on the launch stream
+        around each call), after untimed calls for at least 30 ms (the clocks
+        ramp up after the leg's host-side set-up); `flush` runs untimed
+        before each call."""
+        t0 = time.perf_counter()
+        k = 0
+        while True:
+            fn()
+            torch.cuda.synchronize()
+            k += 1
+            if (k >= 2) if args.fixed_preheat else (time.perf_counter() - t0 >= 0.03):
+                break
+        # the calls go out back to back, so the host's set-up of a call
+        # overlaps the GPU work before it; the first, which starts on an idle
+        # GPU and would count its own host set-up, is not kept
+        pairs = []
+        for _ in range(reps + 1):
             if flush is not None:
                 flush()
             a, b = ev(), ev()
             a.record(stream)
             fn()
             b.record(stream)
-            torch.cuda.synchronize()
-            out.append(a.elapsed_time(b))
-        return out
+            pairs.append((a, b))
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) for a, b in pairs[1:]]
 
     # ---------------- workload: 1 GiB bf16 weight-sync buffer ----------------
     bb = 65536
@@ -197,7 +212,7 @@ def main() -> int:
     # results are checked after the timed loop).
     t_pre = time.perf_counter()
     pre_steps = 0
-    while time.perf_counter() - t_pre < PREHEAT_MS * 1e-3:
+    while (pre_steps < 16) if args.fixed_preheat else (time.perf_counter() - t_pre < PREHEAT_MS * 1e-3):
         for _ in range(8):
             step()
         pre_steps += 8

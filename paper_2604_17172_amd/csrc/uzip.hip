@@ -725,17 +725,6 @@ __device__ __forceinline__ uint4 keep_bytes(uint4 o, uint32_t keep) {
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-template <int E>
-__device__ __forceinline__ void load_full(const uint8_t *base, uint64_t first, uint32_t w[4 * (E / 2)]) {
-  const uint4 *p = (const uint4 *)(base + first * E);
-  uint4 a = p[0];
-  w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
-  if (E == 4) {
-    uint4 b = p[1];
-    w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
-  }
-}
-
 // Full groups addressed as a wave-uniform round base (kept in scalar
 // registers) plus a 32-bit lane offset: round r of a block starts at
 // elements blk0 + 512 r; lane j owns 16 (E = 2) or 32 (E = 4) bytes of it.
@@ -762,16 +751,6 @@ __device__ __forceinline__ void store_raw_round(uint8_t *raw_round_base, const G
   if (E == 4) {
     out64<SYS>(q + 8, g.raw[2], g.raw[3]);
     out64<SYS>(q + 16, g.raw[4], g.raw[5]);
-  }
-}
-
-template <int E>
-__device__ __forceinline__ void store_raw_full(uint8_t *plane, uint64_t first, const Group &g) {
-  uint2 *q = (uint2 *)(plane + (uint64_t)(E - 1) * first);
-  q[0] = make_uint2(g.raw[0], g.raw[1]);
-  if (E == 4) {
-    q[1] = make_uint2(g.raw[2], g.raw[3]);
-    q[2] = make_uint2(g.raw[4], g.raw[5]);
   }
 }
 

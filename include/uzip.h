@@ -20,7 +20,8 @@
  * Stream layout (little-endian; pad16(x) rounds x up to a multiple of 16,
  * padding bytes are zero):
  *     0  u32 magic 0x31505A55   4 u8 version = 1   5 u8 dtype
- *     6  u8 prob_bits = 11      7 u8 flags = 0
+ *     6  u8 prob_bits = 11      7 u8 flags = the table mode (0 for a table
+ *                                 per block; 1, 2: see uzip_table_mode)
  *     8  u32 block_elems       12 u32 n_blocks
  *    16  u64 n_elems           24 u64 total_bytes
  *    32  u32 dir[n_blocks]: bit 31 = STORED, bits 30..0 = end offset of

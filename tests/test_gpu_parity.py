@@ -159,6 +159,16 @@ def test_single_symbol_blocks(uz):
     check_roundtrip(uz, x, "bf16", 65536, "constant blocks")
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "fp16", "fp32"])
+def test_stored_coded_boundary(uz, dtype):
+    """A one-symbol block codes to 290 bytes: STORED at 289 and 290
+    elements, CODED at 291 (the strict inequality of the STORED rule)."""
+    one = {"bf16": 0x3F80, "fp16": 0x3C00, "fp32": 0x3F800000}[dtype]
+    for n in (289, 290, 291):
+        x = np.full(n, one, np.uint32 if dtype == "fp32" else np.uint16)
+        check_roundtrip(uz, x, dtype, 65536, f"boundary n={n}")
+
+
 def test_uniform_bf16(uz):
     x = W.uniform_bf16(1 << 21, seed=11)
     check_roundtrip(uz, x, "bf16", 65536, "uniform bf16")

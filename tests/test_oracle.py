@@ -266,6 +266,30 @@ def test_single_symbol_block_closed_form():
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp16", "fp32"])
+def test_stored_coded_boundary_closed_form(dtype):
+    """One symbol, no words: the coded section would be 288 + 2 = 290 bytes,
+    so a block of 290 elements is STORED (290 symbol bytes are not more)
+    and one of 291 is CODED (pad16(290) = 304 bytes) -- the strict
+    inequality of the STORED rule, at its edge."""
+    one = {"bf16": 0x3F80, "fp16": 0x3C00, "fp32": 0x3F800000}[dtype]
+    for n, stored, sec_len in ((290, True, 304), (291, False, 304), (289, True, 304), (300, False, 304)):
+        x = np.full(n, one, np.uint32 if dtype == "fp32" else np.uint16)
+        s = ref.compress(x, dtype, 65536)
+        h = header(s)
+        d = struct.unpack_from("<I", s.tobytes(), 32)[0]
+        assert bool(d >> 31) == stored, (dtype, n)
+        assert 16 * (d & 0x7FFFFFFF) == sec_len
+        assert h["total"] == s.size
+        raw_off = 32 + pad16(4)
+        coded_off = raw_off + pad16((EB[dtype] - 1) * n)
+        assert s.size == coded_off + sec_len
+        if not stored:
+            states = np.frombuffer(s[coded_off:coded_off + 256].tobytes(), np.uint32)
+            assert np.all(states == L_STATE)
+        assert np.array_equal(ref.decompress(s, dtype, n), x)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16", "fp32"])
 def test_uniform_random_words_all_stored(dtype):
     """Uniformly random words carry 8 bits per symbol plus the table, so
     every block is STORED and the size has a closed form."""

@@ -98,3 +98,30 @@ def test_sweep_matches_oracle(uz, seed):
     yt, stt = uz.decompress_table(tout, dtype, n)
     torch.cuda.synchronize()
     assert int(stt.item()) == 0 and np.array_equal(host_bits(yt, dtype), x)
+
+
+def reduce_case(seed):
+    rng = np.random.default_rng(5000 + seed)
+    dtype = ("bf16", "fp16", "fp32")[seed % 3]
+    n_in = int(rng.integers(1, 17))
+    bb = int(2 ** rng.integers(12, 19))
+    n = int(np.exp(rng.uniform(0, np.log(400_000))))
+    gen = {"bf16": lambda k: W.normal_bf16(n, sigma=float(rng.choice([0.02, 1.0])), seed=k),
+           "fp16": lambda k: W.grad_fp16(n, seed=k), "fp32": lambda k: W.grad_fp32(n, seed=k)}[dtype]
+    xs = [np.ascontiguousarray(gen(100 * seed + i)[:n]) for i in range(n_in)]
+    local = np.ascontiguousarray(gen(100 * seed + 99)[:n]) if rng.integers(0, 2) else None
+    return dtype, n_in, n, bb, xs, local
+
+
+@pytest.mark.parametrize("seed", range(15))
+def test_reduce_sweep_matches_oracle(uz, seed):
+    dtype, n_in, n, bb, xs, local = reduce_case(seed)
+    say(f"[sweep] reduce seed={seed} dtype={dtype} n_in={n_in} n={n} block={bb} local={local is not None}")
+    streams = [ref.compress(v, dtype, bb) for v in xs]
+    want_s, want_y = ref.reduce(streams, dtype, n, bb, local=local)
+    out, size, raw, status = uz.reduce_fused([dev(s) for s in streams], dtype, n, bb,
+                                             local=dev(local.view(NP_BITS[dtype])) if local is not None else None,
+                                             check=True)
+    got = out[:int(size.item())].cpu().numpy()
+    assert got.size == want_s.size and np.array_equal(got, want_s), f"seed {seed}: output stream differs"
+    assert np.array_equal(host_bits(raw, dtype), np.asarray(want_y).view(host_bits(raw, dtype).dtype)[:n])

@@ -303,8 +303,10 @@ const char *uzip_status_str(uzip_status status);
  * wait at spin_limit polls (0 restores the default, 2^22), and the block
  * with the global index held_block (counted over all chunks of a call;
  * UINT32_MAX: none) never publishes its size, so every later block of its
- * stream waits until its bound runs out and the stream is marked invalid;
- * every kernel still ends normally.  Process-wide; not for production use.
+ * stream waits until its bound runs out and the stream is marked invalid
+ * (and so is a stream whose block was taken by a workgroup held up in such
+ * a wait, when its own later blocks run out of polls in turn); every kernel
+ * still ends normally.  Process-wide; not for production use.
  * Errors: none (returns UZIP_OK). */
 uzip_status uzip_inject_scan_stall(uint32_t spin_limit, uint32_t held_block);
 

@@ -90,6 +90,12 @@ struct EncodeArgs {
   uint32_t table_stride;  // u16 entries between the tables of consecutive streams (0: one table for all)
   uint32_t table_mode;
   uint32_t table_bytes;
+  // split-send producer, XCD-local (n_xcd > 0): chunk c is coded only by
+  // waves of XCD c mod n_xcd, which take its blocks from their XCD's own
+  // ticket counter; the stream bytes then go out with ordinary stores and
+  // the block that completes a chunk's count writes the XCD's L2 back
+  // before raising the flag
+  uint32_t n_xcd;
 };
 
 // The first workspace words of an encoder launch (u32 index), written by the
@@ -101,6 +107,9 @@ struct EncodeArgs {
 // reduce; may be null).  Read from memory where used, they take no
 // registers in the encoder's loop.
 enum : uint32_t { kWsTicket = 0, kWsError = 1, kWsExit = 2, kWsSpin = 32, kWsHold = 33, kWsStatusPtr = 34 };
+// the XCD-local producer's ticket counters, one 64-byte line per XCD
+constexpr uint32_t kWsXcd = 64, kWsXcdStride = 16, kMaxXcd = 8;
+constexpr uint64_t kWsHeaderBytes = 4 * (kWsXcd + kWsXcdStride * kMaxXcd);
 
 constexpr size_t kDecodeWsBytes = 256;   // reserved: the decoder keeps no state there
 
@@ -588,12 +597,47 @@ __device__ uint64_t resolve_prefix(uint64_t *status, uint32_t b, uint32_t first,
 // A block whose look-back failed first sets the counter's top bit (block
 // counts stay below 2^31), so no later count can equal `need` and the flag
 // is left to finish_launch, which raises it over a zero size.
+// A system-scope release: this XCD's L2 written back to memory, then a wait
+// for the write-back.  The wait is explicit because the compiler leaves out
+// its own after the write-back when an explicit wait precedes the fence.
+__device__ __forceinline__ void writeback_l2() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
+  __builtin_amdgcn_s_waitcnt(0);
+}
+
+// XCD-local producer (wb): the bytes went out with ordinary stores into the
+// L2 of the XCD that codes the whole chunk, so the block that completes the
+// count first writes that L2 back and then stores the flag.
 constexpr uint32_t kChunkFailed = 0x80000000u;
-__device__ void publish_chunk(uint32_t *cnt, uint32_t need, uint32_t *flag, uint32_t epoch, bool failed = false) {
+__device__ void publish_chunk(uint32_t *cnt, uint32_t need, uint32_t *flag, uint32_t epoch, bool failed = false,
+                              bool wb = false) {
   if (failed && lane_id() == 0) __hip_atomic_fetch_or(cnt, kChunkFailed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   __builtin_amdgcn_s_waitcnt(0);
-  if (lane_id() == 0 && __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) + 1 == need)
+  if (lane_id() == 0 && __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) + 1 == need) {
+    if (wb) writeback_l2();
     __hip_atomic_store(flag, epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  }
+}
+
+// The next block of a persistent encoder wave (lane 0 only).  Tickets are
+// block indices in order, or, for the XCD-local producer, indices into the
+// blocks of this XCD's chunks (c = xcd, xcd + n_xcd, ...) in order; past the
+// last block: n_blocks.
+__device__ uint32_t take_block(const EncodeArgs &a) {
+  if (a.n_xcd == 0) return __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // HW_REG_XCC_ID (hardware register 20), bits 3..0: the XCD this wave runs on
+  const uint32_t xcd = (__builtin_amdgcn_s_getreg(20u | (0u << 6) | ((4u - 1u) << 11)) & 15u) % a.n_xcd;
+  uint32_t *ctr = a.ticket + kWsXcd + kWsXcdStride * xcd;
+  const uint64_t chunks = ((uint64_t)a.n_blocks + a.blocks_per_chunk - 1) / a.blocks_per_chunk;
+  while (true) {
+    const uint32_t t = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t q = t / a.blocks_per_chunk;
+    const uint64_t c = xcd + (uint64_t)a.n_xcd * q;
+    if (c >= chunks) return a.n_blocks;
+    const uint64_t b = c * a.blocks_per_chunk + (t - q * a.blocks_per_chunk);
+    if (b < a.n_blocks) return (uint32_t)b;
+    // past the end of the tensor's last, shorter chunk: take another ticket
+  }
 }
 
 template <int DT>
@@ -958,7 +1002,7 @@ __device__ __forceinline__ void finish_block(const EncodeArgs &a, const Fin &f, 
     if (lane < 16 && db < f.dir_end) out8<SYS>(f.sout + db, 0);
   }
   if (a.flags != nullptr)
-    publish_chunk(&a.chunk_cnt[2 * f.chunk + 1], f.n_blocks, &a.flags[2 * f.chunk + 1], a.epoch, failed);
+    publish_chunk(&a.chunk_cnt[2 * f.chunk + 1], f.n_blocks, &a.flags[2 * f.chunk + 1], a.epoch, failed, !SYS);
 }
 
 // End of a persistent encoder workgroup.  The last one out (its stores and
@@ -966,7 +1010,9 @@ __device__ __forceinline__ void finish_block(const EncodeArgs &a, const Fin &f, 
 // itself) marks every stream that had a failed look-back invalid: magic and
 // size 0 -- a stream is never shorter than its 32-byte header, so a zero
 // size is the error -- the split-send producer's DONE flag raised over it,
-// and the fused reduce's status set.
+// and the fused reduce's status set.  The XCD-local producer also marks a
+// chunk that no wave finished (an XCD that received no workgroup) so, rather
+// than leave its flag down.
 template <bool SYS, bool REDUCE>
 __device__ void finish_launch(const EncodeArgs &a) {
   const uint32_t lane = lane_id();
@@ -975,16 +1021,22 @@ __device__ void finish_launch(const EncodeArgs &a) {
   if (lane == 0)
     last = __hip_atomic_fetch_add(a.ticket + kWsExit, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1 == gridDim.x;
   if (!uniform(last)) return;
-  if (__hip_atomic_load(a.ticket + kWsError, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) return;
+  const bool err = __hip_atomic_load(a.ticket + kWsError, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+  if (!err && a.n_xcd == 0) return;
   const uint32_t streams = (a.n_blocks + a.blocks_per_chunk - 1) / a.blocks_per_chunk;
   for (uint32_t c = lane; c < streams; c += 64) {
-    const bool bad = a.flags == nullptr ||
-                     (__hip_atomic_load(&a.chunk_cnt[2 * c + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) & kChunkFailed);
+    bool bad = a.flags == nullptr;
+    if (!bad) {
+      const uint32_t cnt = __hip_atomic_load(&a.chunk_cnt[2 * c + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      const uint32_t left = a.n_blocks - c * a.blocks_per_chunk;
+      bad = (cnt & kChunkFailed) || (cnt & ~kChunkFailed) != (left < a.blocks_per_chunk ? left : a.blocks_per_chunk);
+    }
     if (!bad) continue;
     coh64<SYS>((uint64_t *)(a.out + (uint64_t)c * a.slot_bytes), 0);
     if (a.sizes != nullptr) coh64<SYS>(&a.sizes[c], 0);
     if (a.flags != nullptr) {
       __builtin_amdgcn_s_waitcnt(0);
+      if (!SYS) writeback_l2();
       __hip_atomic_store(&a.flags[2 * c + 1], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     }
   }
@@ -1040,13 +1092,13 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   // the coding pass, which hide the atomic's latency (lane 0 holds it)
   uint32_t next_ticket = 0;
   if constexpr (DEFER) {
-    if (lane == 0) next_ticket = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (lane == 0) next_ticket = take_block(a);
   }
 
   while (true) {
     uint32_t b = 0;
     if constexpr (DEFER) b = next_ticket;
-    else if (lane == 0) b = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else if (lane == 0) b = take_block(a);
     b = uniform(b);
     if (b >= a.n_blocks) break;
 
@@ -1217,7 +1269,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     }
     __syncthreads();
     if (a.flags != nullptr) {
-      publish_chunk(&a.chunk_cnt[2 * chunk], g.n_blocks, &a.flags[2 * chunk], a.epoch);
+      publish_chunk(&a.chunk_cnt[2 * chunk], g.n_blocks, &a.flags[2 * chunk], a.epoch, false, !SYS);
     }
 
     __builtin_amdgcn_s_setprio(0);
@@ -1225,7 +1277,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
       // the previous block's section leaves the staging area
       if (have_pend) finish_block<DT, SYS>(a, pend, stage, ovf);
       have_pend = false;
-      if (lane == 0) next_ticket = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (lane == 0) next_ticket = take_block(a);
       __syncthreads();
     }
     // ---- table ----
@@ -2760,7 +2812,7 @@ struct EncodeWs {
 EncodeWs encode_ws(uint64_t n_blocks, uint64_t n_chunks, uint32_t block_elems, uint64_t ybytes, bool reduce = false,
                    uint64_t slots = 0) {
   EncodeWs w;
-  w.status_off = 256;
+  w.status_off = kWsHeaderBytes;
   w.cnt_off = pad256(w.status_off + 8 * n_blocks);
   w.slot_off = pad256(w.cnt_off + 8 * n_chunks);
   w.slots = slots ? slots : n_slots(n_blocks, block_elems);
@@ -2862,9 +2914,20 @@ uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws
   a.pass2_off = kEncTableBytes;
   const uint32_t lds = encode_lds(a.block_elems, !reduce);
   if (lds > 160 * 1024) return UZIP_EINVAL;
-  const void *fn = reduce ? reduce_kernel_ptr((int)dt)
-                   : shared ? shared_kernel_ptr((int)dt * 4 + (a.flags != nullptr ? 2 : 0) + (small ? 1 : 0))
-                            : encode_kernel_ptr((int)dt * 4 + (a.flags != nullptr ? 2 : 0) + (small ? 1 : 0));
+  // The split-send producer keeps each chunk on one XCD when the chip runs
+  // as one device of 8 XCDs and the grid gives every XCD 32 workgroups
+  // (workgroups go to the XCDs in turn): its stream bytes then need no
+  // write-through stores, one write-back of the XCD's L2 per chunk does.
+  const uint64_t chunks = ((uint64_t)a.n_blocks + a.blocks_per_chunk - 1) / a.blocks_per_chunk;
+  const uint64_t most = a.n_blocks < w.slots ? a.n_blocks : w.slots;
+  a.n_xcd = (!reduce && a.flags != nullptr && info.cus == 32 * (int)kMaxXcd && chunks >= 8 * kMaxXcd &&
+             most >= (uint64_t)info.cus)
+                ? kMaxXcd
+                : 0;
+  const int kind = (a.flags != nullptr && a.n_xcd == 0 ? 2 : 0) + (small ? 1 : 0);
+  const void *fn = reduce   ? reduce_kernel_ptr((int)dt)
+                   : shared ? shared_kernel_ptr((int)dt * 4 + kind)
+                            : encode_kernel_ptr((int)dt * 4 + kind);
   int occ = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, 64, lds) != hipSuccess || occ < 1) occ = 1;
   uint64_t grid = (uint64_t)info.cus * (uint64_t)occ;

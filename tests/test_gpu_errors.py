@@ -73,9 +73,12 @@ def test_compress_marks_a_stalled_stream_invalid(uz, stall):
     assert np.array_equal(out[: int(size.item())].cpu().numpy(), want)
 
 
-def test_chunked_producer_marks_only_the_stalled_chunk(uz, stall):
+# 7 chunks: every workgroup takes any chunk's blocks; 81 chunks and 321
+# blocks: on a chip of 8 XCDs each chunk is coded on one XCD
+@pytest.mark.parametrize("full_chunks", [6, 80])
+def test_chunked_producer_marks_only_the_stalled_chunk(uz, stall, full_chunks):
     bb, cb = 16384, 65536               # four blocks per chunk
-    x = W.normal_bf16(6 * 32768 + 5000, seed=51)
+    x = W.normal_bf16(full_chunks * 32768 + 5000, seed=51)
     xt = dev(x.view(np.int16))
     chunks = -(-x.size // (cb // 2))
     flags = torch.zeros(2 * chunks, dtype=torch.int32).pin_memory()

@@ -250,6 +250,87 @@ def test_split_send_ordering_seen_from_the_host(uz):
     assert lead >= 1
 
 
+def test_split_send_chunks_read_by_the_copy_engine_at_done(uz):
+    """Split-send into device memory (section 3.2.3): a consumer outside the
+    GPU's caches -- a NIC, here the copy engine -- may read a chunk's stream
+    as soon as its DONE flag is up.  The producer writes the streams to
+    device memory and the sizes and flags to pinned host memory; this thread
+    polls the flags and, at the first sight of DONE[c], copies the chunk's
+    slot to the host on a second stream.  One block of chunk 700 is held
+    from the host (uzip_inject_scan_stall, a wait of 100000 polls, about
+    0.1 s), so the producer is still running while the other chunks are
+    copied; that chunk ends marked invalid, and so may a chunk whose block
+    was taken by a wave held up in that wait.  Every copy of a chunk not
+    marked invalid is compared with the oracle's stream.  1 GiB of the
+    weight-sync buffer, 1 MiB chunks (1024 chunks), 64 KiB blocks."""
+    from concurrent.futures import ThreadPoolExecutor
+    bb, cb = 65536, 1 << 20
+    x = W.weight_sync()
+    n = x.size
+    ce = cb // 2
+    chunks = -(-n // ce)
+    held_chunk = 700
+    held = held_chunk * (cb // bb) + 3
+    t0 = time.time()
+    with ThreadPoolExecutor(16) as ex:
+        want = list(ex.map(lambda c: ref.compress(x[c * ce:(c + 1) * ce], "bf16", bb), range(chunks)))
+    say(f"[full] copy at DONE: {chunks} chunks, oracle {time.time() - t0:.1f}s, block {held} held")
+    slot = (uz.uzip_max_compressed_size(uz.BF16, ce, bb) + 255) // 256 * 256
+    out = torch.zeros(slot * chunks, dtype=torch.uint8, device="cuda")
+    host = torch.zeros(slot * chunks, dtype=torch.uint8).pin_memory()
+    sizes = torch.zeros(chunks, dtype=torch.int64).pin_memory()
+    flags = torch.zeros(2 * chunks, dtype=torch.int32).pin_memory()
+    ws = torch.empty(uz.uzip_workspace_size(uz.OP_CHUNKED, uz.BF16, n, bb, cb), dtype=torch.uint8, device="cuda")
+    xt = to_dev(x, "bf16")
+    fl = flags.numpy()
+    side = torch.cuda.Stream()
+    epoch = 9
+    torch.cuda.synchronize()
+    assert uz.uzip_inject_scan_stall(100000, held) == uz.OK
+    try:
+        rc = uz.uzip_compress_chunked(xt.data_ptr(), n, uz.BF16, bb, cb, out.data_ptr(), slot, sizes.data_ptr(),
+                                      flags.data_ptr(), epoch, ws.data_ptr(), ws.numel(),
+                                      torch.cuda.current_stream().cuda_stream)
+        assert rc == uz.OK
+        copied = np.zeros(chunks, bool)
+        pending = []
+        lead = 0       # copies seen complete while some DONE flag was still down
+        deadline = time.time() + 60
+        with torch.cuda.stream(side):
+            while not copied.all():
+                assert time.time() < deadline, "flags never all raised"
+                finished = 0
+                while pending and pending[0].query():
+                    pending.pop(0)
+                    finished += 1
+                done = fl[1::2].copy() == epoch     # read after the queries
+                if not done.all():
+                    lead += finished
+                for c in np.flatnonzero(done & ~copied):
+                    copied[c] = True
+                    host[c * slot:(c + 1) * slot].copy_(out[c * slot:(c + 1) * slot], non_blocking=True)
+                    ev = torch.cuda.Event()
+                    ev.record(side)
+                    pending.append(ev)
+        torch.cuda.synchronize()
+    finally:
+        uz.uzip_inject_scan_stall(0, 0xFFFFFFFF)
+    hb, sb = host.numpy(), sizes.numpy()
+    assert int(sb[held_chunk]) == 0
+    invalid = []
+    for c in range(chunks):
+        if int(sb[c]) == 0:
+            # marked invalid: size 0 and magic 0, in the copy taken at DONE
+            assert not hb[c * slot:c * slot + 4].any(), f"chunk {c}: size 0 but magic set"
+            invalid.append(c)
+            continue
+        assert int(sb[c]) == want[c].size, f"chunk {c} size {int(sb[c])} != {want[c].size}"
+        assert np.array_equal(hb[c * slot:c * slot + want[c].size], want[c]), f"chunk {c} not in memory at DONE"
+    say(f"[full] copy at DONE: {lead} of {chunks} copies complete while the producer ran; "
+        f"chunks marked invalid: {invalid}")
+    assert len(invalid) <= 64 and lead >= chunks // 2
+
+
 def test_reduce_full_tensor_reading(uz):
     """The other reading of the activation slices (section 3.4, the fused
     reduce of one rank): each of the 8 inputs is the whole [8192 x 8192]

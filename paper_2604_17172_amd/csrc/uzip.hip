@@ -1641,9 +1641,18 @@ struct DecStream {
   uint32_t be, nb;
   Geom g;
 };
+// A stream header's eight words (loaded by the caller, ahead of their use).
+struct Hdr {
+  uint4 lo, hi;
+};
+__device__ inline Hdr load_hdr(const uint8_t *s) { return Hdr{((const uint4 *)s)[0], ((const uint4 *)s)[1]}; }
+
+// Checks stream c's header h (words: magic | version, dtype, probability
+// bits, flags | block elements | blocks | elements (2) | total bytes (2))
+// and sets up its geometry; builds the stream-wide lookup table.
 template <int DT, bool SHARED>
-__device__ bool open_stream(const DecodeArgs &a, uint64_t c, DecStream &st, uint32_t *lut, uint16_t *cum_s,
-                            uint16_t *f_s) {
+__device__ bool open_stream(const DecodeArgs &a, uint64_t c, const Hdr &h, DecStream &st, uint32_t *lut,
+                            uint16_t *cum_s, uint16_t *f_s) {
   constexpr int E = (DT == 2) ? 4 : 2;
   const bool chunked = a.bpc != 0;
   st.s = a.in + (chunked ? c * a.slot_bytes : 0);
@@ -1655,15 +1664,17 @@ __device__ bool open_stream(const DecodeArgs &a, uint64_t c, DecStream &st, uint
     st.nb = 0;
     return false;
   }
-  const uint32_t be = ld32(s + 8);
-  const uint32_t nb = ld32(s + 12);
-  const uint64_t total = ld64(s + 24);
+  const uint32_t be = h.lo.z;
+  const uint32_t nb = h.lo.w;
+  const uint64_t total = (uint64_t)h.hi.z | (uint64_t)h.hi.w << 32;
   // flags byte: the table mode (0: a table per block; 1: a stream-wide
   // table after the directory; 2: the caller's stream-wide table)
-  const uint32_t mode = s[7];
-  bool ok = ld32(s) == kMagic && s[4] == kVersion && s[5] == DT && s[6] == kProbBits &&
+  const uint32_t mode = h.lo.y >> 24;
+  bool ok = h.lo.x == kMagic && (h.lo.y & 0xFFu) == kVersion && ((h.lo.y >> 8) & 0xFFu) == DT &&
+            ((h.lo.y >> 16) & 0xFFu) == kProbBits &&
             (SHARED ? ((mode == 1) || (mode == 2 && a.table != nullptr)) : mode == 0) &&
-            ld64(s + 16) == st.n && be > 0 && (be & (be - 1)) == 0 && (uint64_t)be * E >= kMinBlockBytes &&
+            ((uint64_t)h.hi.x | (uint64_t)h.hi.y << 32) == st.n && be > 0 && (be & (be - 1)) == 0 &&
+            (uint64_t)be * E >= kMinBlockBytes &&
             (uint64_t)be * E <= kMaxBlockBytes && (uint64_t)nb == (st.n + be - 1) / be && total <= cap &&
             (!chunked || be == a.block_elems);
   Geom g = make_geom(st.n, ok ? be : 1, E);
@@ -1705,7 +1716,9 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
   bool ok = true;
   if (a.bpc == 0) {
     // one stream
-    ok = open_stream<DT, SHARED>(a, 0, st, lut, cum_s, f_s);
+    Hdr h = {};
+    if (a.in_bytes >= kHeaderBytes) h = load_hdr(a.in);
+    ok = open_stream<DT, SHARED>(a, 0, h, st, lut, cum_s, f_s);
     if (!ok) {
       if (blockIdx.x == 0 && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
       return;
@@ -1718,9 +1731,37 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
     n_work = a.n_chunks * a.bpc;
   }
 
+  // The next block's directory entries, and over chunk streams its chunk's
+  // header, are loaded a block ahead: a block then starts from its section
+  // instead of a chain of dependent loads.  Directory words are only read
+  // inside the stream's bytes (a valid header puts the directory there).
+  struct Ahead {
+    Hdr h;
+    uint32_t d, dp;
+  };
+  auto fetch = [&](uint64_t g2, Ahead &nx) {
+    const uint8_t *s2 = a.in;
+    uint64_t cap = a.in_bytes;
+    uint32_t b2 = (uint32_t)g2;
+    if (a.bpc != 0) {
+      const uint64_t q = g2 / a.bpc;
+      b2 = (uint32_t)(g2 - q * a.bpc);
+      s2 = a.in + (a.first_chunk + q) * a.slot_bytes;
+      cap = a.slot_bytes;
+      nx.h = load_hdr(s2);
+    }
+    const uint64_t de = kHeaderBytes + 4ull * (b2 + 1);
+    nx.d = de <= cap ? ld32(s2 + de - 4) : 0u;
+    nx.dp = (b2 > 0 && de <= cap) ? ld32(s2 + de - 8) : 0u;
+  };
+
   // blocks are independent: a grid-stride walk, no ticket (one counter for
   // every wave costs more in queueing than it recovers in balance)
+  Ahead nx = {};
+  if (blockIdx.x < n_work) fetch(blockIdx.x, nx);
   for (uint64_t gb = blockIdx.x; gb < n_work; gb += gridDim.x) {
+    const Ahead here = nx;
+    if (gb + gridDim.x < n_work) fetch(gb + gridDim.x, nx);
     uint32_t b = (uint32_t)gb;
     if (a.bpc != 0) {
       const uint64_t q = gb / a.bpc;
@@ -1728,7 +1769,7 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
       b = (uint32_t)(gb - q * a.bpc);
       if (c != cur) {
         cur = c;
-        ok = open_stream<DT, SHARED>(a, c, st, lut, cum_s, f_s);
+        ok = open_stream<DT, SHARED>(a, c, here.h, st, lut, cum_s, f_s);
       }
       if (!ok) {
         if (b == 0 && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
@@ -1742,8 +1783,8 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
     const uint32_t be = st.be;
     const uint64_t total = st.total;
     const uint8_t *raw_plane = s + g.raw_off;
-    const uint32_t d = ld32(s + kHeaderBytes + 4 * b);
-    const uint64_t start = b ? 16ull * (ld32(s + kHeaderBytes + 4 * (b - 1)) & ~kStoredBit) : 0;
+    const uint32_t d = here.d;
+    const uint64_t start = b ? 16ull * (here.dp & ~kStoredBit) : 0;
     const uint64_t end = 16ull * (d & ~kStoredBit);
     const uint64_t blk0 = (uint64_t)b * be;
     const uint32_t n_b = (uint32_t)((st.n - blk0) < be ? (st.n - blk0) : be);

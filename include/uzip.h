@@ -57,8 +57,9 @@
  *     its compute units for longer), the stream is marked invalid: its
  *     magic and its size (*d_out_size, chunk_sizes[c]) read 0 -- a valid
  *     stream is never shorter than its 32-byte header -- the split-send
- *     producer still raises the chunk's DONE flag, and the fused reduce
- *     also sets *d_status to UZIP_ETIMEOUT.  The call may be repeated.
+ *     producer still raises the chunk's DONE flag (and its RAW_READY flag,
+ *     had it not risen), and the fused reduce also sets *d_status to
+ *     UZIP_ETIMEOUT.  The call may be repeated.
  */
 #ifndef UZIP_H
 #define UZIP_H
@@ -190,8 +191,9 @@ uzip_status uzip_compress_table(const void *d_in, uint64_t n_elems, uzip_dtype d
  * it; with EXTERNAL every chunk is coded with d_table.  slot_bytes >=
  * uzip_max_compressed_size(one chunk) + UZIP_TABLE_BYTES; workspace:
  * uzip_workspace_size(UZIP_OP_CHUNKED_TABLE, ..., chunk_bytes).  An
- * EXTERNAL table that is not an all-symbol table codes nothing: the chunk
- * sizes read 0 and no flag is raised.  Otherwise as uzip_compress_chunked
+ * EXTERNAL table that is not an all-symbol table codes nothing: every
+ * chunk is marked invalid as after an encoder failure (magic and size 0,
+ * both flags raised).  Otherwise as uzip_compress_chunked
  * (PER_BLOCK is that call).  Each chunk decodes with
  * uzip_decompress_table, or a batch of chunks with
  * uzip_decompress_chunked_table. */

@@ -1010,9 +1010,10 @@ __device__ __forceinline__ void finish_block(const EncodeArgs &a, const Fin &f, 
 // itself) marks every stream that had a failed look-back invalid: magic and
 // size 0 -- a stream is never shorter than its 32-byte header, so a zero
 // size is the error -- the split-send producer's DONE flag raised over it,
-// and the fused reduce's status set.  The XCD-local producer also marks a
-// chunk that no wave finished (an XCD that received no workgroup) so, rather
-// than leave its flag down.
+// and the fused reduce's status set.  The split-send producer also marks a
+// chunk that no wave finished so (under the XCD-local producer, an XCD that
+// received no workgroup; a stream-wide table found invalid), rather than
+// leave its flags down.
 template <bool SYS, bool REDUCE>
 __device__ void finish_launch(const EncodeArgs &a) {
   const uint32_t lane = lane_id();
@@ -1022,14 +1023,16 @@ __device__ void finish_launch(const EncodeArgs &a) {
     last = __hip_atomic_fetch_add(a.ticket + kWsExit, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1 == gridDim.x;
   if (!uniform(last)) return;
   const bool err = __hip_atomic_load(a.ticket + kWsError, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
-  if (!err && a.n_xcd == 0) return;
+  if (!err && a.flags == nullptr) return;
   const uint32_t streams = (a.n_blocks + a.blocks_per_chunk - 1) / a.blocks_per_chunk;
   for (uint32_t c = lane; c < streams; c += 64) {
-    bool bad = a.flags == nullptr;
+    bool bad = a.flags == nullptr, raw_short = false;
     if (!bad) {
-      const uint32_t cnt = __hip_atomic_load(&a.chunk_cnt[2 * c + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
       const uint32_t left = a.n_blocks - c * a.blocks_per_chunk;
-      bad = (cnt & kChunkFailed) || (cnt & ~kChunkFailed) != (left < a.blocks_per_chunk ? left : a.blocks_per_chunk);
+      const uint32_t need = left < a.blocks_per_chunk ? left : a.blocks_per_chunk;
+      const uint32_t cnt = __hip_atomic_load(&a.chunk_cnt[2 * c + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      raw_short = __hip_atomic_load(&a.chunk_cnt[2 * c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != need;
+      bad = (cnt & kChunkFailed) || (cnt & ~kChunkFailed) != need;
     }
     if (!bad) continue;
     coh64<SYS>((uint64_t *)(a.out + (uint64_t)c * a.slot_bytes), 0);
@@ -1037,6 +1040,8 @@ __device__ void finish_launch(const EncodeArgs &a) {
     if (a.flags != nullptr) {
       __builtin_amdgcn_s_waitcnt(0);
       if (!SYS) writeback_l2();
+      // a chunk that no wave coded has not raised RAW_READY either
+      if (raw_short) __hip_atomic_store(&a.flags[2 * c], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
       __hip_atomic_store(&a.flags[2 * c + 1], a.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     }
   }
@@ -1114,15 +1119,21 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         ts.f[2] = v.y & 0xFFFFu;
         ts.f[3] = v.y >> 16;
         // a table that is not an all-symbol table (some f = 0, or a sum
-        // other than M) codes nothing: the stream sizes read 0
+        // other than M) codes nothing: the block is skipped (every block of
+        // the stream is, the table being the stream's) and the stream size
+        // reads 0; the wave goes on with its next ticket, so that every
+        // stream of the call has its size set
         const bool bad = ts.f[0] == 0 || ts.f[1] == 0 || ts.f[2] == 0 || ts.f[3] == 0;
         if (__any(bad) || wave_sum(ts.f[0] + ts.f[1] + ts.f[2] + ts.f[3]) != kM) {
           if (lane == 0 && a.sizes != nullptr) a.sizes[chunk] = 0;
-          // a pending block belongs to an earlier stream with a valid table
           if constexpr (DEFER) {
+            // a pending block belongs to an earlier stream with a valid table
             if (have_pend) finish_block<DT, SYS>(a, pend, stage, ovf);
+            have_pend = false;
+            if (lane == 0) next_ticket = take_block(a);
           }
-          return;
+          __syncthreads();
+          continue;
         }
         __syncthreads();  // the previous block's coding pass is done with the entries
         enc_entries(ts, enc);

@@ -190,12 +190,30 @@ def test_chunked_external_table(uz):
     check_chunked(uz, x, "bf16", 65536, 1 << 20, "external", "external", ref.sampled_table(x, "bf16"))
 
 
-def test_chunked_invalid_external_table(uz):
-    say("[tables] chunked invalid table")
-    x = W.normal_bf16(3 * (1 << 19), seed=5)
+@pytest.mark.parametrize("n_chunks,chunk_bytes", [(3, 1 << 20), (600, 1 << 18)])
+def test_chunked_invalid_external_table(uz, n_chunks, chunk_bytes):
+    """An EXTERNAL table whose frequencies do not sum to M codes nothing:
+    every chunk is marked invalid (magic and size 0) and both its flags are
+    raised, also when the call has more blocks (2400) than the encoder has
+    workgroups.  Sizes and slots start as 0xFF bytes, so a chunk left
+    untouched would show."""
+    ce = chunk_bytes // 2
+    say(f"[tables] chunked invalid table: {n_chunks} chunks of {chunk_bytes} bytes")
+    x = W.normal_bf16(n_chunks * ce, seed=5)
     bad = ref.sampled_table(x, "bf16").astype(np.uint16)
     bad[0] += 1
-    out, slot, sizes, flags = uz.compress_chunked_table(dev(x.view(np.int16)), 65536, 1 << 20, "external",
-                                                        dev(bad.view(np.int16)), dtype="bf16", epoch=4)
+    slot = (uz.uzip_max_compressed_size(uz.BF16, ce, 65536) + uz.TABLE_BYTES + 255) // 256 * 256
+    out = torch.full((slot * n_chunks,), 0xFF, dtype=torch.uint8, device="cuda")
+    sizes = torch.full((n_chunks,), -1, dtype=torch.int64, device="cuda")
+    flags = torch.zeros(2 * n_chunks, dtype=torch.int32, device="cuda")
+    ws = torch.empty(uz.uzip_workspace_size(uz.OP_CHUNKED_TABLE, uz.BF16, x.size, 65536, chunk_bytes),
+                     dtype=torch.uint8, device="cuda")
+    xt, t = dev(x.view(np.int16)), dev(bad.view(np.int16))
+    rc = uz.uzip_compress_chunked_table(xt.data_ptr(), x.size, uz.BF16, 65536, chunk_bytes, uz.TABLE_EXTERNAL,
+                                        t.data_ptr(), out.data_ptr(), slot, sizes.data_ptr(), flags.data_ptr(), 4,
+                                        ws.data_ptr(), ws.numel(), torch.cuda.current_stream().cuda_stream)
+    assert rc == uz.OK
     torch.cuda.synchronize()
-    assert int(sizes.sum().item()) == 0 and not bool((flags == 4).any())
+    assert bool((sizes == 0).all()) and bool((flags == 4).all())
+    magic = out.view(n_chunks, slot)[:, :8].cpu().numpy()
+    assert not magic.any()

@@ -364,6 +364,41 @@ __device__ bool build_lut(const uint8_t *sec, uint64_t sec_len, uint32_t *lut, u
   return true;
 }
 
+// build_lut from words the caller loaded with the rest of the section's
+// start: `byte`, byte 256 + lane / 2 of the section (the presence bits),
+// and `fa`, its bytes 288 + 8 lane .. + 7 (the u16 frequencies of ranks
+// 4 lane .. 4 lane + 3; zero past the section's end).
+__device__ bool build_lut_pre(uint32_t byte, uint2 fa, uint64_t sec_len, uint32_t *lut, uint16_t *cum_s,
+                              uint16_t *f_s, uint32_t &k_out) {
+  const uint32_t lane = lane_id();
+  if (sec_len < kSectionFixed) return false;
+  const uint32_t nib = (byte >> (4 * (lane & 1))) & 0xFu;
+  const uint32_t pres = __popc(nib);
+  const uint32_t k = wave_sum(pres);
+  const uint32_t rank0 = wave_excl_scan(pres);
+  const bool ok0 = k >= 1 && (uint64_t)kSectionFixed + 2ull * k <= sec_len;
+  // the frequencies of ranks 0 .. 255, staged where the table will go
+  ((uint2 *)lut)[lane] = fa;
+  wave_lds_fence();
+  const uint16_t *fr = (const uint16_t *)lut;
+  uint32_t f[4] = {0, 0, 0, 0};
+  uint32_t r = rank0, total = 0;
+  if (ok0) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (nib & (1u << q)) f[q] = fr[r++];
+      total += f[q];
+    }
+  }
+  wave_lds_fence();  // read before the table overwrites them
+  const uint32_t bad = (nib & 1 && f[0] == 0) | (nib & 2 && f[1] == 0) | (nib & 4 && f[2] == 0) |
+                       (nib & 8 && f[3] == 0);
+  if (!(ok0 && !__any(bad) && wave_sum(total) == kM)) return false;
+  fill_lut(f, lut, cum_s, f_s);
+  k_out = k;
+  return true;
+}
+
 // The lookup table from this lane's frequencies f[4] of symbols 4 lane ..
 // 4 lane + 3 (summing to M over the wave).
 __device__ void fill_lut(const uint32_t f[4], uint32_t *lut, uint16_t *cum_s, uint16_t *f_s) {
@@ -1805,6 +1840,26 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
     const uint32_t len = bad ? 0 : (uint32_t)(end - start);
     const bool stored = d >> 31;
     if (!bad && stored && len < n_b) bad = true;
+    // The start of a coded section in one round of loads: the states, the
+    // presence bits and frequencies, and the 2048 bytes that follow the
+    // fixed part (the first three ring chunks start within its first 512:
+    // the words begin at most 2 x 256 bytes of frequencies in).  Sections
+    // are 16-byte units, so a 16-byte load is either whole inside it or
+    // skipped.
+    constexpr uint32_t P0 = SHARED ? kSharedSectionFixed : kSectionFixed;
+    uint32_t x = 0, pbyte = 0;
+    uint2 pfa = make_uint2(0u, 0u);
+    uint4 pre0 = make_uint4(0u, 0u, 0u, 0u), pre1 = pre0;
+    if (!bad && !stored && len >= P0) {
+      x = ((const uint32_t *)sec)[lane];
+      if constexpr (!SHARED) {
+        pbyte = sec[256 + (lane >> 1)];
+        if (kSectionFixed + 8 * lane + 8 <= len) pfa = *(const uint2 *)(sec + kSectionFixed + 8 * lane);
+      }
+      const uint32_t o0 = P0 + 32 * lane;
+      if (o0 + 16 <= len) pre0 = *(const uint4 *)(sec + o0);
+      if (o0 + 32 <= len) pre1 = *(const uint4 *)(sec + o0 + 16);
+    }
     if (bad) {
       if (lane == 0) report(a.dstatus, UZIP_ECORRUPT);
       continue;
@@ -1839,31 +1894,30 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
         continue;
       }
     } else {
-      if (!build_lut(sec, len, lut, cum_s, f_s, k)) {
+      if (!build_lut_pre(pbyte, pfa, len, lut, cum_s, f_s, k)) {
         if (lane == 0) report(a.dstatus, UZIP_ECORRUPT);
         continue;
       }
       k = uniform(k);
     }
-    uint32_t x = ((const uint32_t *)sec)[lane];
     const uint32_t x0 = x;  // checked at the end of the block: no wait for it here
     const uint32_t wb = SHARED ? kSharedSectionFixed : kSectionFixed + 2 * k;  // section offset of word 0
     const uint32_t w_avail = (len - wb) / 2;
     RingD rg;
     rg.len = len;
     {
+      // section bytes [P0, P0 + 2048) fill the ring (which held the table
+      // build's scratch until now), so it holds the three chunks from the
+      // word start's 16-byte unit on; the third chunk is also the first
+      // pending refill
       const uint32_t base = wb & ~15u;
-      uint2 v[3];
-#pragma unroll
-      for (int c = 0; c < 3; ++c) {
-        const uint32_t o = base + c * kDecChunk + 8 * lane;
-        v[c] = *(const uint2 *)(sec + (o + 8 <= len ? o : len - 8));
-      }
-#pragma unroll
-      for (int c = 0; c < 3; ++c) *(uint2 *)(ring + ((base + c * kDecChunk + 8 * lane) & (kDecRingBytes - 1))) = v[c];
+      const uint32_t o0 = P0 + 32 * lane;
+      *(uint4 *)(ring + (o0 & (kDecRingBytes - 1))) = pre0;
+      *(uint4 *)(ring + ((o0 + 16) & (kDecRingBytes - 1))) = pre1;
+      wave_lds_fence();
       rg.front = base + 3 * kDecChunk;
       rg.pos[0] = rg.pos[1] = base + 2 * kDecChunk;
-      rg.pv[0] = rg.pv[1] = v[2];
+      rg.pv[0] = rg.pv[1] = *(const uint2 *)(ring + ((base + 2 * kDecChunk + 8 * lane) & (kDecRingBytes - 1)));
     }
     __syncthreads();
     uint32_t p = 0, rb = wb & (kDecRingBytes - 1);

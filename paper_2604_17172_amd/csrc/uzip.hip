@@ -1619,6 +1619,92 @@ __device__ __forceinline__ uint4 ring_fetch(const uint8_t *sec, uint32_t o, uint
   return *(const uint4 *)(sec + (o + 16 <= len ? o : len - 16));
 }
 
+// A stream header's eight words (loaded by the caller, ahead of their use).
+struct Hdr {
+  uint4 lo, hi;
+};
+__device__ inline Hdr load_hdr(const uint8_t *s) { return Hdr{((const uint4 *)s)[0], ((const uint4 *)s)[1]}; }
+
+// Modes of a decoding wave's input block in the fused reduce.
+enum : uint32_t { kBad = 0, kStored = 1, kCoded = 2 };
+
+// Opens block b of one input stream s (in_bytes long) of the fused reduce:
+// checks the header against the call (n elements, blocks of be) and the
+// block's directory entries, and for a coded block builds the lookup table
+// and fills the ring.  The loads come in two rounds: the header with the
+// directory entries, then the start of the section -- states, presence
+// bits, frequencies and the 4096 bytes from the end of the fixed part,
+// which hold the first two ring chunks and the first pending one (the
+// words begin at most 512 bytes in) -- instead of five dependent ones.
+// Returns kBad, kStored or kCoded; sets sec, raw_plane, the states x, the
+// word start wb, the words available and the ring.
+template <int DT>
+__device__ uint32_t open_input_block(const uint8_t *s, uint64_t in_bytes, uint64_t n, uint32_t be, uint32_t b,
+                                     uint32_t n_b, uint32_t *lut, uint8_t *ring, const uint8_t *&sec,
+                                     const uint8_t *&raw_plane, uint32_t &x, uint32_t &wb, uint32_t &w_avail,
+                                     Ring &rg) {
+  constexpr int E = (DT == 2) ? 4 : 2;
+  const uint32_t lane = lane_id();
+  const Geom g = make_geom(n, be, E);
+  if (in_bytes < kHeaderBytes) return kBad;
+  // round 1: header and directory entries (inside the stream's bytes)
+  const Hdr h = load_hdr(s);
+  const uint64_t de = kHeaderBytes + 4ull * (b + 1);
+  const uint32_t d = de <= in_bytes ? ld32(s + de - 4) : 0u;
+  const uint32_t dp = (b > 0 && de <= in_bytes) ? ld32(s + de - 8) : 0u;
+  const uint64_t start = b ? 16ull * (dp & ~kStoredBit) : 0;
+  const uint64_t end = 16ull * (d & ~kStoredBit);
+  const bool stored = d >> 31;
+  const uint32_t len = end >= start ? (uint32_t)(end - start) : 0u;
+  // round 2: the section's start, read inside the stream's bytes (16-byte
+  // loads of a section of 16-byte units are whole inside it or skipped)
+  uint32_t pbyte = 0;
+  uint2 pfa = make_uint2(0u, 0u);
+  uint4 pre[4] = {make_uint4(0u, 0u, 0u, 0u), make_uint4(0u, 0u, 0u, 0u), make_uint4(0u, 0u, 0u, 0u),
+                  make_uint4(0u, 0u, 0u, 0u)};
+  const uint8_t *sc = s + g.coded_off + start;
+  uint32_t xs = kStateLo;
+  x = kStateLo;
+  if (end >= start && g.coded_off + end <= in_bytes && !stored && len >= kSectionFixed) {
+    xs = ((const uint32_t *)sc)[lane];
+    pbyte = sc[256 + (lane >> 1)];
+    if (kSectionFixed + 8 * lane + 8 <= len) pfa = *(const uint2 *)(sc + kSectionFixed + 8 * lane);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t o = kSectionFixed + 1024 * j + 16 * lane;
+      if (o + 16 <= len) pre[j] = *(const uint4 *)(sc + o);
+    }
+  }
+  const uint64_t total = (uint64_t)h.hi.z | (uint64_t)h.hi.w << 32;
+  const bool ok = h.lo.x == kMagic && h.lo.y == (kVersion | ((uint32_t)DT << 8) | (kProbBits << 16)) &&
+                  h.lo.z == be && h.lo.w == g.n_blocks && ((uint64_t)h.hi.x | (uint64_t)h.hi.y << 32) == n &&
+                  total <= in_bytes && total >= g.coded_off && de <= in_bytes && end >= start &&
+                  g.coded_off + end <= total;
+  if (!ok) return kBad;
+  sec = sc;
+  raw_plane = s + g.raw_off;
+  if (stored) return len >= n_b ? kStored : kBad;
+  uint32_t k = 0;
+  if (!build_lut_pre(pbyte, pfa, len, lut, (uint16_t *)ring, (uint16_t *)ring + 256, k)) return kBad;
+  k = uniform(k);
+  x = xs;
+  wb = kSectionFixed + 2 * k;
+  w_avail = (len - wb) / 2;
+  rg.len = len;
+  // section bytes [288, 288 + 4096) fill the ring (the table build's
+  // scratch until now): it then holds the two chunks from the word start's
+  // 16-byte unit on, and the third is the first pending one
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t o = kSectionFixed + 1024 * j + 16 * lane;
+    ring_put(ring, o & (kRingBytes - 1), pre[j]);
+  }
+  wave_lds_fence();
+  rg.written = (wb & ~15u) + 2 * kChunkBytes;
+  rg.pv = *(const uint4 *)(ring + ((rg.written + 16 * lane) & (kRingBytes - 1)));
+  return kCoded;
+}
+
 // Before a round: make sure the next 1 KB of words (from section offset cur)
 // is in LDS, then load the following chunk for the next round.  Every round
 // stores the loaded chunk at its ring position and loads the chunk at
@@ -1687,12 +1773,6 @@ struct DecStream {
   uint32_t be, nb;
   Geom g;
 };
-// A stream header's eight words (loaded by the caller, ahead of their use).
-struct Hdr {
-  uint4 lo, hi;
-};
-__device__ inline Hdr load_hdr(const uint8_t *s) { return Hdr{((const uint4 *)s)[0], ((const uint4 *)s)[1]}; }
-
 // Checks stream c's header h (words: magic | version, dtype, probability
 // bits, flags | block elements | blocks | elements (2) | total bytes (2))
 // and sets up its geometry; builds the stream-wide lookup table.
@@ -2083,7 +2163,6 @@ __global__ void __launch_bounds__(64 * (kReduceGroup + 1)) reduce_decode_kernel(
   // ---- decoding waves: block b of input `wave` ----
   uint32_t *lut = (uint32_t *)(smem_base + wave * kDecLds);
   uint8_t *ring = smem_base + wave * kDecLds + kLutBytes;
-  enum : uint32_t { kBad = 0, kStored = 1, kCoded = 2 };
   uint32_t mode = kBad;
   const uint8_t *sec = nullptr, *raw_plane = nullptr;
   uint32_t x = kStateLo, x0 = kStateLo, p = 0, rb = 0, wb = 0, w_avail = 0;
@@ -2092,57 +2171,11 @@ __global__ void __launch_bounds__(64 * (kReduceGroup + 1)) reduce_decode_kernel(
   rg.len = 16;
   rg.pv = make_uint4(0, 0, 0, 0);
   if (decoder) {
-    const uint8_t *s = a.ins[wave];
-    bool ok = a.in_bytes[wave] >= kHeaderBytes;
-    uint64_t total = 0;
-    Geom g = make_geom(a.n, be, E);
-    if (ok) {
-      total = ld64(s + 24);
-      ok = ld32(s) == kMagic && s[4] == kVersion && s[5] == DT && s[6] == kProbBits && s[7] == 0 &&
-           ld32(s + 8) == be && ld32(s + 12) == g.n_blocks && ld64(s + 16) == a.n && total <= a.in_bytes[wave] &&
-           total >= g.coded_off;
-    }
-    uint64_t start = 0, end = 0;
-    uint32_t d = 0;
-    if (ok) {
-      d = ld32(s + kHeaderBytes + 4 * b);
-      start = b ? 16ull * (ld32(s + kHeaderBytes + 4 * (b - 1)) & ~kStoredBit) : 0;
-      end = 16ull * (d & ~kStoredBit);
-      ok = end >= start && g.coded_off + end <= total;
-    }
-    if (ok) {
-      sec = s + g.coded_off + start;
-      raw_plane = s + g.raw_off;
-      const uint32_t len = (uint32_t)(end - start);
-      if (d >> 31) {
-        ok = len >= n_b;
-        mode = kStored;
-      } else {
-        uint32_t k = 0;
-        ok = build_lut(sec, len, lut, (uint16_t *)ring, (uint16_t *)ring + 256, k);
-        if (ok) {
-          mode = kCoded;
-          k = uniform(k);
-          x = x0 = ((const uint32_t *)sec)[lane];
-          wb = kSectionFixed + 2 * k;
-          w_avail = (len - wb) / 2;
-          rb = wb & (kRingBytes - 1);
-          rg.len = len;
-          rg.written = wb & ~15u;
-#pragma unroll
-          for (int c = 0; c < 2; ++c) {
-            const uint32_t o = rg.written + 16 * lane;
-            ring_put(ring, o & (kRingBytes - 1), ring_fetch(sec, o, len));
-            rg.written += kChunkBytes;
-          }
-          rg.pv = ring_fetch(sec, rg.written + 16 * lane, len);
-        }
-      }
-    }
-    if (!ok) {
-      mode = kBad;
-      if (lane == 0) report(a.dstatus, UZIP_ECORRUPT);
-    }
+    mode = open_input_block<DT>(a.ins[wave], a.in_bytes[wave], a.n, be, b, n_b, lut, ring, sec, raw_plane, x, wb,
+                                w_avail, rg);
+    x0 = x;
+    rb = wb & (kRingBytes - 1);
+    if (mode == kBad && lane == 0) report(a.dstatus, UZIP_ECORRUPT);
   } else {
     for (uint32_t i = lane; i < kHistReplicas * kHistStride; i += 64) hist[i] = 0;
   }
@@ -2306,7 +2339,6 @@ __global__ void __launch_bounds__(64 * (kReduceGroup + 1)) reduce_fused_kernel(R
   // ---- decoding waves: block b of input `wave` ----
   uint32_t *lut = (uint32_t *)(smem_base + wave * kDecLds);
   uint8_t *ring = smem_base + wave * kDecLds + kLutBytes;
-  enum : uint32_t { kBad = 0, kStored = 1, kCoded = 2 };
   uint32_t mode = kBad;
   const uint8_t *sec = nullptr, *raw_plane = nullptr;
   uint32_t x = kStateLo, x0 = kStateLo, p = 0, rb = 0, wb = 0, w_avail = 0;
@@ -2315,56 +2347,11 @@ __global__ void __launch_bounds__(64 * (kReduceGroup + 1)) reduce_fused_kernel(R
   rg.len = 16;
   rg.pv = make_uint4(0, 0, 0, 0);
   if (decoder) {
-    const uint8_t *s = r.ins[wave];
-    bool ok = r.in_bytes[wave] >= kHeaderBytes;
-    uint64_t total = 0;
-    if (ok) {
-      total = ld64(s + 24);
-      ok = ld32(s) == kMagic && s[4] == kVersion && s[5] == DT && s[6] == kProbBits && s[7] == 0 &&
-           ld32(s + 8) == be && ld32(s + 12) == g.n_blocks && ld64(s + 16) == r.n && total <= r.in_bytes[wave] &&
-           total >= g.coded_off;
-    }
-    uint64_t start = 0, end = 0;
-    uint32_t d = 0;
-    if (ok) {
-      d = ld32(s + kHeaderBytes + 4 * b);
-      start = b ? 16ull * (ld32(s + kHeaderBytes + 4 * (b - 1)) & ~kStoredBit) : 0;
-      end = 16ull * (d & ~kStoredBit);
-      ok = end >= start && g.coded_off + end <= total;
-    }
-    if (ok) {
-      sec = s + g.coded_off + start;
-      raw_plane = s + g.raw_off;
-      const uint32_t len = (uint32_t)(end - start);
-      if (d >> 31) {
-        ok = len >= n_b;
-        mode = kStored;
-      } else {
-        uint32_t k = 0;
-        ok = build_lut(sec, len, lut, (uint16_t *)ring, (uint16_t *)ring + 256, k);
-        if (ok) {
-          mode = kCoded;
-          k = uniform(k);
-          x = x0 = ((const uint32_t *)sec)[lane];
-          wb = kSectionFixed + 2 * k;
-          w_avail = (len - wb) / 2;
-          rb = wb & (kRingBytes - 1);
-          rg.len = len;
-          rg.written = wb & ~15u;
-#pragma unroll
-          for (int c = 0; c < 2; ++c) {
-            const uint32_t o = rg.written + 16 * lane;
-            ring_put(ring, o & (kRingBytes - 1), ring_fetch(sec, o, len));
-            rg.written += kChunkBytes;
-          }
-          rg.pv = ring_fetch(sec, rg.written + 16 * lane, len);
-        }
-      }
-    }
-    if (!ok) {
-      mode = kBad;
-      if (lane == 0) report(r.dstatus, UZIP_ECORRUPT);
-    }
+    mode = open_input_block<DT>(r.ins[wave], r.in_bytes[wave], r.n, be, b, n_b, lut, ring, sec, raw_plane, x, wb,
+                                w_avail, rg);
+    x0 = x;
+    rb = wb & (kRingBytes - 1);
+    if (mode == kBad && lane == 0) report(r.dstatus, UZIP_ECORRUPT);
   }
   uint32_t *h = hist + (lane & (kHistReplicas - 1)) * kHistStride;
   // raw bytes of this lane's group of round q (the output's for a partial

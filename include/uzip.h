@@ -44,6 +44,7 @@
  *     *d_status) are valid once the stream reaches that point.
  *   - Device pointers must be 16-byte aligned.
  *   - block_bytes is a power of two in [4096, 262144].
+ *   - n_elems <= 2^48 (else EINVAL; the size queries return 0).
  *   - Calls that overlap in time need separate workspaces.
  *   - Host-side errors are returned immediately and nothing is enqueued.
  *     Device-side errors (corrupt streams) are written to *d_status (the

@@ -2852,6 +2852,10 @@ bool valid_dtype(uzip_dtype dt) { return dt >= UZIP_BF16 && dt <= UZIP_E5M2; }
 // the fused reduction adds values, which FP8 pairs are not given for
 bool valid_reduce_dtype(uzip_dtype dt) { return dt >= UZIP_BF16 && dt <= UZIP_FP32; }
 bool valid_block(uint32_t bb) { return bb >= kMinBlockBytes && bb <= kMaxBlockBytes && (bb & (bb - 1)) == 0; }
+// element counts up to 2^48: every size computed from one stays far from
+// 64-bit overflow
+constexpr uint64_t kMaxElems = 1ull << 48;
+bool valid_n(uint64_t n) { return n <= kMaxElems; }
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 uint64_t pad256(uint64_t x) { return (x + 255u) & ~uint64_t(255); }
 
@@ -3043,12 +3047,12 @@ uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws
 extern "C" {
 
 size_t uzip_max_compressed_size(uzip_dtype dtype, uint64_t n_elems, uint32_t block_bytes) {
-  if (!valid_dtype(dtype) || !valid_block(block_bytes)) return 0;
+  if (!valid_dtype(dtype) || !valid_block(block_bytes) || !valid_n(n_elems)) return 0;
   return (size_t)max_size(elem_bytes(dtype), n_elems, block_bytes / elem_bytes(dtype));
 }
 
 size_t uzip_workspace_size(int op, uzip_dtype dtype, uint64_t n_elems, uint32_t block_bytes, uint64_t aux) {
-  if (!valid_dtype(dtype) || !valid_block(block_bytes)) return 0;
+  if (!valid_dtype(dtype) || !valid_block(block_bytes) || !valid_n(n_elems)) return 0;
   const uint32_t E = elem_bytes(dtype), be = block_bytes / E;
   const uint64_t nb = (n_elems + be - 1) / be;
   switch (op) {
@@ -3084,7 +3088,7 @@ size_t uzip_workspace_size(int op, uzip_dtype dtype, uint64_t n_elems, uint32_t 
 uzip_status uzip_compress(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint32_t block_bytes,
                           void *d_out, size_t out_cap, uint64_t *d_out_size, void *d_ws, size_t ws_bytes,
                           hipStream_t stream) {
-  if (!valid_dtype(dtype) || !valid_block(block_bytes)) return UZIP_EINVAL;
+  if (!valid_dtype(dtype) || !valid_block(block_bytes) || !valid_n(n_elems)) return UZIP_EINVAL;
   if (d_out == nullptr || !aligned16(d_out) || (n_elems > 0 && (d_in == nullptr || !aligned16(d_in))))
     return UZIP_EINVAL;
   const uint32_t E = elem_bytes(dtype), be = block_bytes / E;
@@ -3117,7 +3121,7 @@ uzip_status uzip_compress(const void *d_in, uint64_t n_elems, uzip_dtype dtype, 
 
 uzip_status uzip_compress_noalloc(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint32_t block_bytes,
                                   void *d_out, size_t out_cap, uint64_t *d_out_size, hipStream_t stream) {
-  if (!valid_dtype(dtype) || !valid_block(block_bytes)) return UZIP_EINVAL;
+  if (!valid_dtype(dtype) || !valid_block(block_bytes) || !valid_n(n_elems)) return UZIP_EINVAL;
   if (d_out == nullptr || !aligned16(d_out) || (n_elems > 0 && (d_in == nullptr || !aligned16(d_in))))
     return UZIP_EINVAL;
   const uint32_t E = elem_bytes(dtype), be = block_bytes / E;
@@ -3168,7 +3172,7 @@ uzip_status uzip_compress_chunked_table(const void *d_in, uint64_t n_elems, uzip
                                         uint64_t chunk_bytes, uzip_table_mode mode, const uint16_t *d_table,
                                         void *d_out, size_t slot_bytes, uint64_t *chunk_sizes, uint32_t *flags,
                                         uint32_t epoch, void *d_ws, size_t ws_bytes, hipStream_t stream) {
-  if (!valid_dtype(dtype) || !valid_block(block_bytes)) return UZIP_EINVAL;
+  if (!valid_dtype(dtype) || !valid_block(block_bytes) || !valid_n(n_elems)) return UZIP_EINVAL;
   if (mode != UZIP_TABLE_PER_BLOCK && mode != UZIP_TABLE_SAMPLED && mode != UZIP_TABLE_EXTERNAL) return UZIP_EINVAL;
   if (mode == UZIP_TABLE_EXTERNAL && (d_table == nullptr || !aligned16(d_table))) return UZIP_EINVAL;
   if (chunk_bytes == 0 || chunk_bytes % block_bytes) return UZIP_EINVAL;
@@ -3229,7 +3233,7 @@ uzip_status launch_decode_args(DecodeArgs &a, uzip_dtype dtype, uint64_t most, c
 uzip_status launch_decode(const void *d_in, size_t in_bytes, uzip_dtype dtype, uint64_t n_elems, void *d_out,
                           size_t out_cap, uint32_t *d_status, void *d_ws, size_t ws_bytes, hipStream_t stream,
                           bool shared, const uint16_t *d_table) {
-  if (!valid_dtype(dtype) || d_in == nullptr || !aligned16(d_in)) return UZIP_EINVAL;
+  if (!valid_dtype(dtype) || !valid_n(n_elems) || d_in == nullptr || !aligned16(d_in)) return UZIP_EINVAL;
   if (d_table != nullptr && !aligned16(d_table)) return UZIP_EINVAL;
   if (n_elems > 0 && (d_out == nullptr || !aligned16(d_out))) return UZIP_EINVAL;
   if (out_cap < n_elems * elem_bytes(dtype)) return UZIP_ENOSPC;
@@ -3275,7 +3279,7 @@ uzip_status launch_decode_chunked(const void *d_in, size_t slot_bytes, uint64_t 
                                   uzip_dtype dtype, uint64_t n_elems, uint32_t block_bytes, uint64_t chunk_bytes,
                                   void *d_out, size_t out_cap, uint32_t *d_status, hipStream_t stream, bool shared,
                                   const uint16_t *d_table) {
-  if (!valid_dtype(dtype) || !valid_block(block_bytes)) return UZIP_EINVAL;
+  if (!valid_dtype(dtype) || !valid_block(block_bytes) || !valid_n(n_elems)) return UZIP_EINVAL;
   if (chunk_bytes == 0 || chunk_bytes % block_bytes) return UZIP_EINVAL;
   if (d_table != nullptr && !aligned16(d_table)) return UZIP_EINVAL;
   const uint32_t E = elem_bytes(dtype), be = block_bytes / E;
@@ -3343,7 +3347,7 @@ uzip_status uzip_decompress_chunked_table(const void *d_in, size_t slot_bytes, u
 
 uzip_status uzip_build_table(const void *d_in, uint64_t n_elems, uzip_dtype dtype, uint16_t *d_table,
                              hipStream_t stream) {
-  if (!valid_dtype(dtype) || d_table == nullptr || !aligned16(d_table)) return UZIP_EINVAL;
+  if (!valid_dtype(dtype) || !valid_n(n_elems) || d_table == nullptr || !aligned16(d_table)) return UZIP_EINVAL;
   if (n_elems > 0 && (d_in == nullptr || !aligned16(d_in))) return UZIP_EINVAL;
   DeviceInfo info;
   uzip_status st = device_info(info);
@@ -3358,7 +3362,7 @@ uzip_status uzip_compress_table(const void *d_in, uint64_t n_elems, uzip_dtype d
   if (mode == UZIP_TABLE_PER_BLOCK)
     return uzip_compress(d_in, n_elems, dtype, block_bytes, d_out, out_cap, d_out_size, d_ws, ws_bytes, stream);
   if (mode != UZIP_TABLE_SAMPLED && mode != UZIP_TABLE_EXTERNAL) return UZIP_EINVAL;
-  if (!valid_dtype(dtype) || !valid_block(block_bytes)) return UZIP_EINVAL;
+  if (!valid_dtype(dtype) || !valid_block(block_bytes) || !valid_n(n_elems)) return UZIP_EINVAL;
   if (d_out == nullptr || !aligned16(d_out) || (n_elems > 0 && (d_in == nullptr || !aligned16(d_in))))
     return UZIP_EINVAL;
   if (mode == UZIP_TABLE_EXTERNAL && (d_table == nullptr || !aligned16(d_table))) return UZIP_EINVAL;
@@ -3410,7 +3414,7 @@ uzip_status uzip_reduce_fused(const void *const *d_in, const size_t *in_bytes, i
                               uzip_dtype dtype, uint64_t n_elems, uint32_t block_bytes, void *d_out, size_t out_cap,
                               uint64_t *d_out_size, void *d_out_raw, uint32_t *d_status, void *d_ws,
                               size_t ws_bytes, hipStream_t stream) {
-  if (!valid_reduce_dtype(dtype) || !valid_block(block_bytes)) return UZIP_EINVAL;
+  if (!valid_reduce_dtype(dtype) || !valid_block(block_bytes) || !valid_n(n_elems)) return UZIP_EINVAL;
   if (n_in < 1 || n_in > kMaxInputs || d_in == nullptr || in_bytes == nullptr) return UZIP_EINVAL;
   for (int i = 0; i < n_in; ++i)
     if (d_in[i] == nullptr || !aligned16(d_in[i]) || in_bytes[i] < kHeaderBytes) return UZIP_EINVAL;

@@ -88,6 +88,30 @@ def test_invalid_arguments_rejected_on_host():
                                             None) == uz.EINVAL   # misaligned table
 
 
+def test_element_count_bound():
+    """Element counts above 2^48 are refused before anything is enqueued
+    (sizes computed from them would come near 64-bit overflow)."""
+    import paper_2604_17172_amd as uz
+    big = (1 << 48) + 1
+    assert uz.uzip_max_compressed_size(0, 1 << 48, 65536) > 0
+    assert uz.uzip_max_compressed_size(0, big, 65536) == 0
+    assert uz.uzip_max_compressed_size(0, (1 << 64) - 1, 65536) == 0
+    assert uz.uzip_workspace_size(uz.OP_COMPRESS, 0, big, 65536, 0) == 0
+    assert uz.uzip_workspace_size(uz.OP_DECOMPRESS, 0, big, 65536, 0) == 0
+    assert uz.uzip_compress(16, big, 0, 65536, 32, 1 << 62, 48, 64, 1 << 20, None) == uz.EINVAL
+    assert uz.uzip_compress_noalloc(16, big, 0, 65536, 32, 1 << 62, 48, None) == uz.EINVAL
+    assert uz.uzip_compress_chunked(16, big, 0, 65536, 1 << 20, 32, 1 << 22, 48, 64, 1, 80, 1 << 20,
+                                    None) == uz.EINVAL
+    assert uz.uzip_compress_table(16, big, 0, 65536, uz.TABLE_SAMPLED, None, 32, 1 << 62, 48, 64, 1 << 20,
+                                  None) == uz.EINVAL
+    assert uz.uzip_build_table(16, big, 0, 32, None) == uz.EINVAL
+    assert uz.uzip_decompress(16, 1 << 40, 0, big, 32, 1 << 62, None, None, 0, None) == uz.EINVAL
+    assert uz.uzip_decompress_chunked(16, 1 << 22, 0, 1, 0, big, 65536, 1 << 20, 32, 1 << 62, None,
+                                      None) == uz.EINVAL
+    assert uz.uzip_reduce_fused([16], [1 << 40], 1, None, 0, big, 65536, 32, 1 << 62, None, None, None, 48,
+                                1 << 20, None) == uz.EINVAL
+
+
 def test_workspace_sizes_are_bounded():
     """The workspace is a status word per block, plus a fixed pool of
     per-workgroup overflow slots for the words of a block that can leave the

@@ -1121,6 +1121,12 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   // counts in the trash slots and encoder table instead, which are free
   // until the coding pass (the table is built from the counts in place).
   constexpr bool DEFER = SMALL && !REDUCE;
+  // larger fp32 blocks keep their last 64 rounds' symbols in registers, so
+  // the coding pass reads half of a 256 KiB block again instead of all of it
+  // (1 GiB fp32 gradient: 0.748 -> 0.680 ms, interleaved A/B); 16-bit types
+  // keep only a quarter of such a block and lost by it (fp16 0.486 -> 0.495
+  // ms)
+  constexpr bool KEEP = !SMALL && !REDUCE && DT == 2;
   static_assert(kHistReplicas * kPackedHistStride * 4 <= kTrashBytes + kEncTableBytes, "packed histogram");
   uint32_t *phist = (uint32_t *)smem_base;
   Fin pend;
@@ -1274,15 +1280,19 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         }
         if (full < rounds) partial_round();  // its symbols stay in psym0/psym1
       } else {
-        if (full > 0) {
+        // rounds below kb stream through (the coding pass reads them
+        // again); for fp32 the last 64 then keep their symbols in registers
+        // as a small block's do, and the coding pass starts with them
+        const uint32_t kb = KEEP ? (full > kRegRounds ? full - kRegRounds : 0) : full;
+        if (kb > 0) {
           uint32_t r = 0;
-          for (; r + D <= full; r += D) {
+          for (; r + D <= kb; r += D) {
 #pragma unroll
             for (int u = 0; u < D; ++u) {
               uint32_t w[NW];
 #pragma unroll
               for (int q = 0; q < NW; ++q) w[q] = buf[u][q];
-              const uint32_t rn = (r + u + D < full) ? r + u + D : full - 1;
+              const uint32_t rn = (r + u + D < kb) ? r + u + D : kb - 1;
               load_round<E>(src_blk + (uint64_t)rn * kRound * E, buf[u]);
               Group gr;
               split_group<DT>(w, gr);
@@ -1292,11 +1302,42 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
           }
 #pragma unroll
           for (int u = 0; u < D - 1; ++u) {
-            if (r + u < full) {
+            if (r + u < kb) {
               Group gr;
               split_group<DT>(buf[u], gr);
               store_raw_round<E, SYS>(raw_blk + (uint64_t)(r + u) * kRound * (E - 1), gr);
               if constexpr (!SHARED) hist_add8(h, gr, 8);
+            }
+          }
+        }
+        if constexpr (KEEP) {
+          if (full > 0) {
+            // the small-block loop above, from round kb (the block is not
+            // read again after these rounds: non-temporal loads)
+#pragma unroll
+            for (int u = 0; u < D; ++u)
+              load_round<E, true>(src_blk + (uint64_t)(kb + u < full ? kb + u : full - 1) * kRound * E, buf[u]);
+#pragma unroll
+            for (uint32_t gi = 0; gi < 4; ++gi) {
+#pragma unroll
+              for (int rr = 0; rr < 16; ++rr) {
+                const uint32_t r = kb + 16 * gi + rr;
+                uint32_t w[NW];
+#pragma unroll
+                for (int q = 0; q < NW; ++q) w[q] = buf[rr % D][q];
+                const uint32_t rn = (r + D < full) ? r + D : full - 1;
+                load_round<E, true>(src_blk + (uint64_t)rn * kRound * E, buf[rr % D]);
+                Group gr;
+                split_group<DT>(w, gr);
+                asm volatile("" : "+v"(gr.sym[0]), "+v"(gr.sym[1]));
+                S.v3[2 * rr] = gr.sym[0];
+                S.v3[2 * rr + 1] = gr.sym[1];
+                if (r < full) {
+                  store_raw_round<E, SYS>(raw_blk + (uint64_t)r * kRound * (E - 1), gr);
+                  if constexpr (!SHARED) hist_add8(h, gr, 8);
+                }
+              }
+              if (gi < 3) shift_down(S);
             }
           }
         }
@@ -1396,18 +1437,47 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         if (gi > 0) shift_up(S);
       }
     } else if constexpr (!REDUCE) {
-      // larger blocks: the block re-read backwards, four rounds ahead (its
-      // last read: non-temporal; fp16 in 256 KiB blocks 0.503 -> 0.457 ms,
-      // fp32 0.749 -> 0.733 ms, interleaved A/B), and the LDS window sliding
-      // into the workgroup's slot as for small ones
+      // larger blocks: for fp32 the last 64 rounds from the register store
+      // (as for a small block, from round kb), then the rest of the block
+      // re-read backwards, four rounds ahead (its last read: non-temporal;
+      // fp16 in 256 KiB blocks 0.503 -> 0.457 ms, fp32 0.749 -> 0.733 ms,
+      // interleaved A/B), and the LDS window sliding into the workgroup's
+      // slot as for small ones
+      const uint32_t kb = KEEP ? (full > kRegRounds ? full - kRegRounds : 0) : full;
+      if constexpr (KEEP) {
+        for (int gi = 3; gi >= 0; --gi) {
+#pragma unroll
+          for (int rr = 15; rr >= 0; --rr) {
+            const int r = (int)kb + 16 * gi + rr;
+            if (r < (int)full && !stored) {
+              if (pos < lo + kRound && lo > 0) {  // the LDS window is full: slide it down
+                const uint32_t x = lo < kSlideWords ? lo : kSlideWords;
+                slide_window((lds16_t *)stage16, ovf + lo, a.lds_words, x, pos - lo);
+                lo -= x;
+                spilled = lo + a.lds_words;
+                lds_rel = (lds16_t *)stage16 - lo;
+              }
+              const uint32_t s0 = S.v3[2 * rr], s1 = S.v3[2 * rr + 1];
+              uint4 e[8];
+#pragma unroll
+              for (int tt = 0; tt < 4; ++tt) e[tt] = enc[(s0 >> (8 * tt)) & 0xFFu];
+#pragma unroll
+              for (int tt = 0; tt < 4; ++tt) e[4 + tt] = enc[(s1 >> (8 * tt)) & 0xFFu];
+              enc_round<true>(x, e, 8, pos, lds_rel, trash);
+              if (a.wcap - pos >= limit_words) stored = true;
+            }
+          }
+          if (gi > 0) shift_up(S);
+        }
+      }
       constexpr int P = 4;
       uint32_t pb[P][NW];
-      if (full > 0) {
+      if (kb > 0) {
 #pragma unroll
         for (int u = 0; u < P; ++u)
-          load_round<E, true>(src_blk + (uint64_t)((int)full - 1 - u >= 0 ? (int)full - 1 - u : 0) * kRound * E, pb[u]);
+          load_round<E, true>(src_blk + (uint64_t)((int)kb - 1 - u >= 0 ? (int)kb - 1 - u : 0) * kRound * E, pb[u]);
       }
-      for (int r0 = (int)full - 1; r0 >= 0 && !stored; r0 -= P) {
+      for (int r0 = (int)kb - 1; r0 >= 0 && !stored; r0 -= P) {
 #pragma unroll
         for (int u = 0; u < P; ++u) {
           const int r = r0 - u;

@@ -1121,12 +1121,12 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   // counts in the trash slots and encoder table instead, which are free
   // until the coding pass (the table is built from the counts in place).
   constexpr bool DEFER = SMALL && !REDUCE;
-  // larger fp32 blocks keep their last 64 rounds' symbols in registers, so
-  // the coding pass reads half of a 256 KiB block again instead of all of it
-  // (1 GiB fp32 gradient: 0.748 -> 0.680 ms, interleaved A/B); 16-bit types
-  // keep only a quarter of such a block and lost by it (fp16 0.486 -> 0.495
-  // ms)
-  constexpr bool KEEP = !SMALL && !REDUCE && DT == 2;
+  // larger blocks keep their last 64 rounds' symbols in registers, so the
+  // coding pass reads the rest of the block again instead of all of it
+  // (interleaved A/B, 256 KiB blocks: 1 GiB fp32 gradient 0.748 -> 0.680 ms,
+  // 1 GiB bf16 buffer 0.816 -> 0.775 ms, 512 MiB fp16 gradient 0.484 ->
+  // 0.480 ms)
+  constexpr bool KEEP = !SMALL && !REDUCE;
   static_assert(kHistReplicas * kPackedHistStride * 4 <= kTrashBytes + kEncTableBytes, "packed histogram");
   uint32_t *phist = (uint32_t *)smem_base;
   Fin pend;
@@ -1281,8 +1281,8 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         if (full < rounds) partial_round();  // its symbols stay in psym0/psym1
       } else {
         // rounds below kb stream through (the coding pass reads them
-        // again); for fp32 the last 64 then keep their symbols in registers
-        // as a small block's do, and the coding pass starts with them
+        // again); the last 64 then keep their symbols in registers as a
+        // small block's do, and the coding pass starts with them
         const uint32_t kb = KEEP ? (full > kRegRounds ? full - kRegRounds : 0) : full;
         if (kb > 0) {
           uint32_t r = 0;
@@ -1437,8 +1437,8 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         if (gi > 0) shift_up(S);
       }
     } else if constexpr (!REDUCE) {
-      // larger blocks: for fp32 the last 64 rounds from the register store
-      // (as for a small block, from round kb), then the rest of the block
+      // larger blocks: the last 64 rounds from the register store (as for a
+      // small block, from round kb), then the rest of the block
       // re-read backwards, four rounds ahead (its last read: non-temporal;
       // fp16 in 256 KiB blocks 0.503 -> 0.457 ms, fp32 0.749 -> 0.733 ms,
       // interleaved A/B), and the LDS window sliding into the workgroup's

@@ -162,3 +162,26 @@ def test_a_corrupt_chunk_is_reported_and_the_others_decode(uz):
     _, st2 = uz.decompress_chunked(out, slot, dtype, n, 4096, cb)
     torch.cuda.synchronize()
     assert int(st2.item()) == uz.ECORRUPT
+
+
+def test_corrupt_chunk_header_words_are_reported(uz):
+    """Header words that would place a chunk's directory or sections outside
+    its slot (a huge block count, a total size past the slot, an element
+    count other than the chunk's) are caught before anything is read from
+    there; the other chunks still decode."""
+    dtype, bb, cb, n = "bf16", 65536, 1 << 20, 4 * (1 << 19)
+    ce = cb // 2
+    x = data(dtype, n, seed=64)
+    out, slot, _, _ = uz.compress_chunked(dev(x.view(np.int16)), bb, cb, dtype=dtype, epoch=7, check=True)
+    for off, val in ((12, 0xFFFFFFF0), (24, slot + 16), (16, ce + 1)):
+        say(f"[chunk-decode] chunk 1 header word at byte {off} set to {val:#x}")
+        bad = out.clone()
+        bad[slot + off:slot + off + 4] = torch.tensor(np.frombuffer(struct.pack("<I", val), dtype=np.uint8).copy()).cuda()
+        y = sentinel_out(dtype, n)
+        _, st = uz.decompress_chunked(bad, slot, dtype, n, bb, cb, out=y)
+        torch.cuda.synchronize()
+        assert int(st.item()) == uz.ECORRUPT
+        h = host_bits(y, dtype)
+        for c in (0, 2, 3):
+            assert np.array_equal(h[c * ce:(c + 1) * ce], x[c * ce:(c + 1) * ce]), (off, c)
+        assert np.all(h[ce:2 * ce] == SENTINEL[2]), off

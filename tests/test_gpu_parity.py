@@ -223,10 +223,11 @@ def test_fp8_tensor_input_counts_pairs(uz, dtype):
         uz.compress(f8[:-1].clone(), 65536)
 
 
+# (4096, 16384): 66 chunks and 264 blocks, the XCD-local producer
+@pytest.mark.parametrize("bb,cb,n", [(65536, 1 << 20, 3 * (1 << 19) + 999), (4096, 16384, 66 * 8192 - 7)])
 @pytest.mark.parametrize("dtype", ["e4m3fn", "e5m2"])
-def test_fp8_chunked_producer(uz, dtype):
-    n, bb, cb = 3 * (1 << 19) + 999, 65536, 1 << 20
-    say(f"[parity] fp8 chunked dtype={dtype} n={n}")
+def test_fp8_chunked_producer(uz, dtype, bb, cb, n):
+    say(f"[parity] fp8 chunked dtype={dtype} n={n} block={bb} chunk={cb}")
     x = special_words(dtype, n, seed=41)
     out, slot, sizes, flags = uz.compress_chunked(to_dev_bits(x, dtype), bb, cb, dtype=dtype, epoch=5)
     torch.cuda.synchronize()

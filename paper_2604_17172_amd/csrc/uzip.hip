@@ -2091,6 +2091,21 @@ __global__ void __launch_bounds__(64) decode_kernel(DecodeArgs a) {
     uint32_t rawC[6] = {0, 0, 0, 0, 0, 0}, rawD[6] = {0, 0, 0, 0, 0, 0};
     auto clampr = [&](uint32_t q) { return q < full ? q : full - 1; };
     for (; r + 4 <= full; r += 4) {
+      if ((r & 15u) == 0) {
+        // a wave's priority steps down with every 16 rounds of a block it
+        // decodes and wraps after four steps: a SIMD issues for its oldest
+        // wave first, and with equal shares the waves that arrived last on a
+        // SIMD would finish last (the fourth ~10% after the first); a wave
+        // that lags gets the issue slots until it has caught up (1 GiB
+        // buffer 0.413 -> 0.407 ms, its chunk streams 0.425 -> 0.421 ms,
+        // interleaved A/B)
+        switch ((r >> 4) & 3u) {
+          case 0: __builtin_amdgcn_s_setprio(3); break;
+          case 1: __builtin_amdgcn_s_setprio(2); break;
+          case 2: __builtin_amdgcn_s_setprio(1); break;
+          default: __builtin_amdgcn_s_setprio(0); break;
+        }
+      }
       uint32_t e[kPerLane], w[NW];
 #define UZIP_DEC_ROUND(RAWUSE, RAWLOAD, DR, AHEAD)                                              \
   ringd_half<0>(rg, ring, sec, wb + 2 * p);                                                     \

@@ -1602,13 +1602,15 @@ __global__ void __launch_bounds__(64) reduce_kernel(EncodeArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// decode_kernel
+// Table decoding: the decode sub-step shared by decode_kernel and the fused
+// reduce's decoding waves, and the fused reduce's word ring.
 //
-// Words of a coded block are staged through a 4 KB LDS ring in 1 KB chunks
-// read with one 16-byte load per lane: a chunk is loaded as soon as the ring
-// has room and written to LDS only when the decoder is about to need it, so
-// the serial decode chain only ever waits on LDS.  The raw plane of the next
-// round is loaded one round ahead.
+// In the fused reduce the words of a coded block are staged through a 4 KB
+// LDS ring in 1 KB chunks read with one 16-byte load per lane: a chunk is
+// loaded as soon as the ring has room and written to LDS only when the
+// decoder is about to need it, so the serial decode chain only ever waits on
+// LDS.  The raw plane of the next round is loaded one round ahead.
+// decode_kernel's own ring (2 KB, more waves per CU) is described with it.
 // ---------------------------------------------------------------------------
 constexpr uint32_t kRingBytes = 4096;
 constexpr uint32_t kRingMirror = 128;  // ring[0, 128) repeated past the end: one step's reads never wrap

@@ -3102,10 +3102,11 @@ uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws
   // as one device of 8 XCDs and the grid gives every XCD 32 workgroups
   // (workgroups go to the XCDs in turn): its stream bytes then need no
   // write-through stores, one write-back of the XCD's L2 per chunk does.
+  // The XCDs get equal numbers of chunks, or numbers at most 1/8 apart.
   const uint64_t chunks = ((uint64_t)a.n_blocks + a.blocks_per_chunk - 1) / a.blocks_per_chunk;
   const uint64_t most = a.n_blocks < w.slots ? a.n_blocks : w.slots;
-  a.n_xcd = (!reduce && a.flags != nullptr && info.cus == 32 * (int)kMaxXcd && chunks >= 8 * kMaxXcd &&
-             most >= (uint64_t)info.cus)
+  const bool even = chunks >= 8 * kMaxXcd || (chunks >= kMaxXcd && chunks % kMaxXcd == 0);
+  a.n_xcd = (!reduce && a.flags != nullptr && info.cus == 32 * (int)kMaxXcd && even && most >= (uint64_t)info.cus)
                 ? kMaxXcd
                 : 0;
   const int kind = (a.flags != nullptr && a.n_xcd == 0 ? 2 : 0) + (small ? 1 : 0);

@@ -250,15 +250,17 @@ def test_fp8_stream_dtype_must_match(uz):
 
 
 # ---------------------------------------------------------- split-send producer
-# The last three run the XCD-local producer on a chip of 8 XCDs (at least 64
-# chunks and 256 blocks): each chunk coded on one XCD, flags raised after a
-# write-back of that XCD's L2.
+# The last five run the XCD-local producer on a chip of 8 XCDs (at least 64
+# chunks, or a multiple of 8, and 256 blocks): each chunk coded on one XCD,
+# flags raised after a write-back of that XCD's L2.
 @pytest.mark.parametrize("dtype,bb,cb,n", [("bf16", 65536, 1 << 20, 3 * (1 << 19) + 77_777),
                                            ("fp32", 262144, 1 << 20, 2 * (1 << 18) + 1),
                                            ("fp16", 4096, 16384, 100_000),
                                            ("bf16", 4096, 16384, 64 * 8192 + 777),
                                            ("fp16", 4096, 16384, 70 * 8192 + 1234),
-                                           ("fp32", 16384, 65536, 66 * 16384 + 5)])
+                                           ("fp32", 16384, 65536, 66 * 16384 + 5),
+                                           ("bf16", 4096, 131072, 8 * 65536),
+                                           ("fp16", 4096, 65536, 24 * 32768 - 100)])
 def test_chunked_producer_matches_per_chunk_oracle(uz, dtype, bb, cb, n):
     say(f"[parity] chunked dtype={dtype} n={n} block={bb} chunk={cb}")
     x = special_words(dtype, n, seed=31)

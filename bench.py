@@ -118,8 +118,8 @@ def main() -> int:
                     help="skip the fused reduce on the full-tensor reading (8 slices [8192 x 8192] bf16)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              "(the codec shards per GPU with no exchange; see the design notes)", file=sys.stderr)
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
+              "(each GPU codes its own shard and nothing is exchanged between GPUs)", file=sys.stderr)
         return 2
 
     import numpy as np

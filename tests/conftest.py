@@ -10,7 +10,7 @@ if ROOT not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs a real MI355X (gfx950) GPU")
-    config.addinivalue_line("markers", "slow: full-size configuration (GPU box only)")
+    config.addinivalue_line("markers", "slow: full-size configuration (needs a GPU)")
 
 
 def pytest_collection_modifyitems(config, items):

@@ -80,7 +80,7 @@ struct EncodeArgs {
   // fused reduce only
   const uint8_t *ybuf;      // the reduced tensor: source of both passes
   const uint32_t *hist_in;  // [n_blocks][256] symbol histograms of the reduced tensor
-  // small-block path: per-workgroup overflow slots for the staged words
+  // per-workgroup overflow slots for the staged words past the LDS window
   uint16_t *slots;
   uint32_t slot_words;
   uint32_t lds_words;       // staging words held in LDS
@@ -1109,7 +1109,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   // the workgroup's overflow slot holds the staging indices that can leave
   // the LDS window, [lds_words, wcap), after kSlotLead words of margin:
   // ovf[v] is index v
-  uint16_t *ovf = !REDUCE ? a.slots + (uint64_t)blockIdx.x * a.slot_words + kSlotLead - a.lds_words : nullptr;
+  uint16_t *ovf = a.slots + (uint64_t)blockIdx.x * a.slot_words + kSlotLead - a.lds_words;
   typedef __attribute__((address_space(3))) uint16_t lds16_t;
   // one private 2-byte slot per lane for words that are not emitted (64
   // slots in 32 consecutive words: every bank once)
@@ -1504,11 +1504,19 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
       }
     } else {
       // the fused reduce's coding pass: the reduced block re-read backwards,
-      // one round ahead; its staging area holds the whole block's words
+      // one round ahead, and the LDS window sliding into the workgroup's
+      // slot as for compress
       uint32_t wa[NW], wbuf[NW];
       if (full > 0) load_round<E>(src_blk + (uint64_t)(full - 1) * kRound * E, wa);
       int r = (int)full - 1;
       for (; r >= 1 && !stored; r -= 2) {
+        if (pos < lo + kRound && lo > 0) {  // the LDS window is full: slide it down
+          const uint32_t x = lo < kSlideWords ? lo : kSlideWords;
+          slide_window((lds16_t *)stage16, ovf + lo, a.lds_words, x, pos - lo);
+          lo -= x;
+          spilled = lo + a.lds_words;
+          lds_rel = (lds16_t *)stage16 - lo;
+        }
         load_round<E>(src_blk + (uint64_t)(r - 1) * kRound * E, wbuf);
         Group gr;
         split_group<DT>(wa, gr);
@@ -1518,6 +1526,13 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         enc_round<true>(x, e, 8, pos, lds_rel, trash);
         if (a.wcap - pos >= limit_words) stored = true;
         if (stored) break;
+        if (pos < lo + kRound && lo > 0) {  // the LDS window is full: slide it down
+          const uint32_t x = lo < kSlideWords ? lo : kSlideWords;
+          slide_window((lds16_t *)stage16, ovf + lo, a.lds_words, x, pos - lo);
+          lo -= x;
+          spilled = lo + a.lds_words;
+          lds_rel = (lds16_t *)stage16 - lo;
+        }
         const uint32_t rn = r >= 2 ? (uint32_t)(r - 2) : 0u;
         load_round<E>(src_blk + (uint64_t)rn * kRound * E, wa);
         split_group<DT>(wbuf, gr);
@@ -1527,6 +1542,13 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         if (a.wcap - pos >= limit_words) stored = true;
       }
       if (r == 0 && !stored) {  // wa holds round 0
+        if (pos < lo + kRound && lo > 0) {  // the LDS window is full: slide it down
+          const uint32_t x = lo < kSlideWords ? lo : kSlideWords;
+          slide_window((lds16_t *)stage16, ovf + lo, a.lds_words, x, pos - lo);
+          lo -= x;
+          spilled = lo + a.lds_words;
+          lds_rel = (lds16_t *)stage16 - lo;
+        }
         Group gr;
         split_group<DT>(wa, gr);
         uint4 e[8];
@@ -1562,7 +1584,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     f.lds_bytes = hdr + 2 * (spilled - pos);
     f.slot_delta = 2 * spilled - f.lds_bytes;
     f.stored = stored;
-    f.spilled = !REDUCE && spilled != a.wcap;
+    f.spilled = spilled != a.wcap;
     f.last = last_in_chunk;
     f.sym_lds = nullptr;
     if (!stored) {
@@ -2968,18 +2990,18 @@ uint32_t slot_words(uint32_t block_elems) {
   const uint32_t w = word_cap(block_elems), l = stage_words(block_elems);
   return w > l ? (kSlotLead + (w - l) + kSlotTail + 127u) & ~127u : 0u;
 }
-// overflow slots of a compress (the fused reduce's coding pass has none):
-// one per persistent workgroup
+// overflow slots of a coding pass (compress, the split-send producer, the
+// fused reduce's separate coding pass): one per persistent workgroup
 uint64_t n_slots(uint64_t n_blocks, uint32_t block_elems) {
   (void)block_elems;
   return n_blocks < kMaxSlots ? n_blocks : kMaxSlots;
 }
 
-// LDS bytes of encode_kernel (windowed: compress; otherwise the fused
-// reduce's coding pass, which stages a whole block)
-uint32_t encode_lds(uint32_t block_elems, bool windowed) {
+// LDS bytes of encode_kernel and reduce_kernel: the pass-1 histogram or the
+// coding pass's staging window
+uint32_t encode_lds(uint32_t block_elems) {
   const uint32_t pass1 = kHistBytes;
-  const uint32_t pass2 = kStageHead + 2 * (windowed ? stage_words(block_elems) : word_cap(block_elems)) + kStageTail;
+  const uint32_t pass2 = kStageHead + 2 * stage_words(block_elems) + kStageTail;
   return kTrashBytes + kEncTableBytes + (pass1 > pass2 ? pass1 : pass2);
 }
 
@@ -2989,18 +3011,17 @@ struct EncodeWs {
 };
 
 // workspace: ticket, error word, exit counter | look-back status per block |
-// chunk counters | overflow slots (compress, blocks whose words can exceed
-// the LDS window) | reduced tensor (fused reduce without a caller buffer).
+// chunk counters | overflow slots (blocks whose words can exceed the LDS
+// window) | reduced tensor (fused reduce without a caller buffer).
 // [0, slot_off) is cleared per call.
 // `slots`: how many overflow slots to lay out (0: n_slots of the call)
-EncodeWs encode_ws(uint64_t n_blocks, uint64_t n_chunks, uint32_t block_elems, uint64_t ybytes, bool reduce = false,
-                   uint64_t slots = 0) {
+EncodeWs encode_ws(uint64_t n_blocks, uint64_t n_chunks, uint32_t block_elems, uint64_t ybytes, uint64_t slots = 0) {
   EncodeWs w;
   w.status_off = kWsHeaderBytes;
   w.cnt_off = pad256(w.status_off + 8 * n_blocks);
   w.slot_off = pad256(w.cnt_off + 8 * n_chunks);
   w.slots = slots ? slots : n_slots(n_blocks, block_elems);
-  w.y_off = pad256(w.slot_off + (reduce ? 0 : 2ull * w.slots * slot_words(block_elems)));
+  w.y_off = pad256(w.slot_off + 2ull * w.slots * slot_words(block_elems));
   w.total = pad256(w.y_off + ybytes);
   return w;
 }
@@ -3014,7 +3035,7 @@ struct ReduceWs {
 };
 ReduceWs reduce_ws(uint64_t n_blocks, uint32_t block_elems, uint64_t n, uint32_t E, int n_in, bool need_y) {
   ReduceWs w;
-  w.enc = encode_ws(n_blocks, 1, block_elems, need_y ? n * E : 0, true);
+  w.enc = encode_ws(n_blocks, 1, block_elems, need_y ? n * E : 0);
   w.hist_off = w.enc.total;
   w.acc_off = pad256(w.hist_off + 1024 * n_blocks);
   w.total = pad256(w.acc_off + (n_in > kReduceGroup ? 4 * n : 0));
@@ -3094,9 +3115,9 @@ uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws
   a.slots = (uint16_t *)(ws + w.slot_off);
   a.slot_words = slot_words(a.block_elems);
   a.wcap = word_cap(a.block_elems);
-  a.lds_words = reduce ? a.wcap : stage_words(a.block_elems);
+  a.lds_words = stage_words(a.block_elems);
   a.pass2_off = kEncTableBytes;
-  const uint32_t lds = encode_lds(a.block_elems, !reduce);
+  const uint32_t lds = encode_lds(a.block_elems);
   if (lds > 160 * 1024) return UZIP_EINVAL;
   // The split-send producer keeps each chunk on one XCD when the chip runs
   // as one device of 8 XCDs and the grid gives every XCD 32 workgroups
@@ -3117,7 +3138,7 @@ uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, 64, lds) != hipSuccess || occ < 1) occ = 1;
   uint64_t grid = (uint64_t)info.cus * (uint64_t)occ;
   if (grid > a.n_blocks) grid = a.n_blocks;
-  if (!reduce && grid > w.slots) grid = w.slots;
+  if (grid > w.slots) grid = w.slots;
   if (grid == 0) grid = 1;
   const uint64_t clear_words = w.slot_off / 4;
   const uint64_t cgrid = (clear_words + 255) / 256 < 4096 ? (clear_words + 255) / 256 : 4096;
@@ -3232,7 +3253,7 @@ uzip_status uzip_compress_noalloc(const void *d_in, uint64_t n_elems, uzip_dtype
   const uint64_t sw = 2ull * slot_words(be);
   if (sw > 0 && full.slot_off + slots * sw > kScratchBytes) slots = (kScratchBytes - full.slot_off) / sw;
   if (slots == 0) return UZIP_ENOSPC;
-  const EncodeWs w = encode_ws(nb, 1, be, 0, false, slots);
+  const EncodeWs w = encode_ws(nb, 1, be, 0, slots);
   if (w.total > kScratchBytes) return UZIP_ENOSPC;
   EncodeArgs a;
   memset(&a, 0, sizeof(a));

@@ -144,9 +144,6 @@ __device__ inline void report(uint32_t *dstatus, int code) {
 }
 
 __device__ inline uint32_t ld32(const uint8_t *p) { return *(const uint32_t *)p; }
-__device__ inline uint64_t ld64(const uint8_t *p) {
-  return (uint64_t)ld32(p) | ((uint64_t)ld32(p + 4) << 32);
-}
 
 // ---------------------------------------------------------------------------
 // Element groups: lane j of round r owns elements 512 r + 8 j .. +7 of a block
@@ -331,43 +328,10 @@ __device__ __forceinline__ void wave_lds_fence() {
 // Returns false (uniformly) if the stored table is not a valid ANS table.
 // ---------------------------------------------------------------------------
 __device__ void fill_lut(const uint32_t f[4], uint32_t *lut, uint16_t *cum_s, uint16_t *f_s);
-__device__ bool build_lut(const uint8_t *sec, uint64_t sec_len, uint32_t *lut, uint16_t *cum_s,
-                          uint16_t *f_s, uint32_t &k_out) {
-  const uint32_t lane = lane_id();
-  if (sec_len < kSectionFixed) return false;
-  // presence bits of symbols 4 lane .. 4 lane + 3
-  uint32_t byte = sec[256 + (lane >> 1)];
-  uint32_t nib = (byte >> (4 * (lane & 1))) & 0xFu;
-  uint32_t pres = __popc(nib);
-  uint32_t k = wave_sum(pres);
-  uint32_t rank0 = wave_excl_scan(pres);
-  bool ok = k >= 1 && (uint64_t)kSectionFixed + 2ull * k <= sec_len;
-  uint32_t f[4] = {0, 0, 0, 0};
-  uint32_t r = rank0, total = 0;
-  if (ok) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (nib & (1u << q)) {
-        const uint8_t *p = sec + kSectionFixed + 2 * r;
-        f[q] = (uint32_t)p[0] | ((uint32_t)p[1] << 8);
-        ++r;
-      }
-      total += f[q];
-    }
-  }
-  uint32_t bad = (nib & 1 && f[0] == 0) | (nib & 2 && f[1] == 0) | (nib & 4 && f[2] == 0) |
-                 (nib & 8 && f[3] == 0);
-  ok = ok && !__any(bad) && wave_sum(total) == kM;
-  if (!ok) return false;
-  fill_lut(f, lut, cum_s, f_s);
-  k_out = k;
-  return true;
-}
-
-// build_lut from words the caller loaded with the rest of the section's
-// start: `byte`, byte 256 + lane / 2 of the section (the presence bits),
-// and `fa`, its bytes 288 + 8 lane .. + 7 (the u16 frequencies of ranks
-// 4 lane .. 4 lane + 3; zero past the section's end).
+// The caller loaded the section's start: `byte` is byte 256 + lane / 2 of
+// the section (the presence bits), `fa` its bytes 288 + 8 lane .. + 7 (the
+// u16 frequencies of ranks 4 lane .. 4 lane + 3; zero past the section's
+// end).
 __device__ bool build_lut_pre(uint32_t byte, uint2 fa, uint64_t sec_len, uint32_t *lut, uint16_t *cum_s,
                               uint16_t *f_s, uint32_t &k_out) {
   const uint32_t lane = lane_id();
@@ -715,6 +679,58 @@ __device__ __forceinline__ void shift_up(SymRegs &S) {
   S.v1 = S.v0;
 }
 
+// Byte K of w shifted left by SH: one SDWA shift (the compiler would emit an
+// extract and a shift).
+template <int K, int SH>
+__device__ __forceinline__ uint32_t byte_shl(uint32_t w) {
+  static_assert(K >= 0 && K < 4, "byte index");
+  uint32_t r;
+  if constexpr (K == 0)
+    asm("v_lshlrev_b32_sdwa %0, %2, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0"
+        : "=v"(r) : "v"(w), "i"(SH));
+  else if constexpr (K == 1)
+    asm("v_lshlrev_b32_sdwa %0, %2, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1"
+        : "=v"(r) : "v"(w), "i"(SH));
+  else if constexpr (K == 2)
+    asm("v_lshlrev_b32_sdwa %0, %2, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2"
+        : "=v"(r) : "v"(w), "i"(SH));
+  else
+    asm("v_lshlrev_b32_sdwa %0, %2, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3"
+        : "=v"(r) : "v"(w), "i"(SH));
+  return r;
+}
+
+// The encoder table entries of a lane's 8 symbols (s0: symbols 0-3, s1: 4-7)
+__device__ __forceinline__ void enc_lookup8(const uint4 *enc, uint32_t s0, uint32_t s1, uint4 (&e)[8]) {
+#pragma unroll
+  for (int tt = 0; tt < 4; ++tt) e[tt] = enc[(s0 >> (8 * tt)) & 0xFFu];
+#pragma unroll
+  for (int tt = 0; tt < 4; ++tt) e[4 + tt] = enc[(s1 >> (8 * tt)) & 0xFFu];
+}
+
+// 16 bytes at LDS byte address p
+__device__ __forceinline__ uint4 lds_load16(uint32_t p) {
+  typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+  const v4u v = *(const __attribute__((address_space(3))) v4u *)(uintptr_t)p;
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// The same for a table at the fixed LDS byte address TB: the shifted symbol
+// is the address, TB goes into the instruction's offset field (the pointer
+// form adds the LDS base in one more instruction).  Read in the order the
+// backwards coding round uses them.
+template <uint32_t TB>
+__device__ __forceinline__ void enc_lookup8_at(uint32_t s0, uint32_t s1, uint4 (&e)[8]) {
+  e[7] = lds_load16(TB + byte_shl<3, 4>(s1));
+  e[6] = lds_load16(TB + byte_shl<2, 4>(s1));
+  e[5] = lds_load16(TB + byte_shl<1, 4>(s1));
+  e[4] = lds_load16(TB + byte_shl<0, 4>(s1));
+  e[3] = lds_load16(TB + byte_shl<3, 4>(s0));
+  e[2] = lds_load16(TB + byte_shl<2, 4>(s0));
+  e[1] = lds_load16(TB + byte_shl<1, 4>(s0));
+  e[0] = lds_load16(TB + byte_shl<0, 4>(s0));
+}
+
 // One encoder sub-step of every lane (rANS coding function with 16-bit
 // renormalisation).  Emitted words go to virtual staging index
 // pos - cnt + rank, compacted across the wave with ballot + mbcnt.
@@ -722,15 +738,25 @@ __device__ __forceinline__ void shift_up(SymRegs &S) {
 // enc_step_lds: the whole step lands in the LDS staging area (index v lives
 // at lds[v - lo]); branch-free: every lane stores, lanes that emit nothing
 // store into their own trash slot.
-template <bool FULL>
+template <bool FULL, bool RANK0>
 __device__ __forceinline__ void enc_step_lds(uint32_t &x, const uint4 e, bool valid, uint32_t &pos,
                                              __attribute__((address_space(3))) uint16_t *lds_rel,
                                              __attribute__((address_space(3))) uint16_t *trash) {
   const bool emit = (FULL || valid) && x >= e.y;
   const uint64_t m = __ballot(emit);
   const uint32_t base = pos - (uint32_t)__popcll(m);
-  const uint32_t v = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, base));
-  __attribute__((address_space(3))) uint16_t *dst = emit ? lds_rel + v : trash;
+  __attribute__((address_space(3))) uint16_t *dst;
+  if constexpr (RANK0) {
+    // the lane's rank among the emitting lanes, and the wave-uniform row
+    // address formed on the scalar unit (one vector move fewer; the large
+    // blocks' coding loops spill more with it)
+    const uint32_t rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+    __attribute__((address_space(3))) uint16_t *row = lds_rel + base;
+    dst = emit ? row + rank : trash;
+  } else {
+    const uint32_t v = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, base));
+    dst = emit ? lds_rel + v : trash;
+  }
   *dst = (uint16_t)x;
   x = emit ? x >> 16 : x;
   pos = base;
@@ -741,12 +767,13 @@ __device__ __forceinline__ void enc_step_lds(uint32_t &x, const uint4 e, bool va
 }
 
 // One round of 8 sub-steps, backwards.
-template <bool FULL>
+template <bool FULL, bool RANK0 = false>
 __device__ __forceinline__ void enc_round(uint32_t &x, const uint4 (&e)[8], uint32_t valid, uint32_t &pos,
                                           __attribute__((address_space(3))) uint16_t *lds_rel,
                                           __attribute__((address_space(3))) uint16_t *trash) {
 #pragma unroll
-  for (int tt = kPerLane - 1; tt >= 0; --tt) enc_step_lds<FULL>(x, e[tt], (uint32_t)tt < valid, pos, lds_rel, trash);
+  for (int tt = kPerLane - 1; tt >= 0; --tt)
+    enc_step_lds<FULL, RANK0>(x, e[tt], (uint32_t)tt < valid, pos, lds_rel, trash);
 }
 
 // The LDS staging window holds virtual indices [lo, lo + cap) at win[v - lo]
@@ -840,24 +867,40 @@ __device__ __forceinline__ void hist_add8(uint32_t *h, const Group &g, uint32_t 
 }
 
 // Packed 16-bit counts (a block holds at most 32768 symbols): symbols s and
-// s + 128 share word s & 127, low and high half.  The bit-field extracts are
-// written out: the compiler turns them into shift-and-mask pairs.
+// s + 128 share word s & 127, low and high half.  The bit-field extract is
+// written out: the compiler turns it into a shift-and-mask pair.  hs holds,
+// per symbol byte, 16 if the symbol's top bit is set and 0 otherwise: the
+// increment 1 << that is one SDWA shift of a register holding 1.
 template <int O>
-__device__ __forceinline__ void hist_add_packed(uint32_t *h, uint32_t w, bool on) {
-  uint32_t word, high;
-  asm("v_bfe_u32 %0, %1, %2, 7" : "=v"(word) : "v"(w), "i"(O));       // symbol & 127
-  asm("v_bfe_u32 %0, %1, %2, 1" : "=v"(high) : "v"(w), "i"(O + 7));   // symbol >> 7
-  if (on) atomicAdd(&h[word], __umul24(high, 0xFFFFu) + 1u);         // 1 or 1 << 16
+__device__ __forceinline__ void hist_add_packed(uint32_t *h, uint32_t w, uint32_t hs, uint32_t one, bool on) {
+  uint32_t word, inc;
+  asm("v_bfe_u32 %0, %1, %2, 7" : "=v"(word) : "v"(w), "i"(O));  // symbol & 127
+  if constexpr (O == 0)
+    asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_0 src1_sel:DWORD"
+        : "=v"(inc) : "v"(hs), "v"(one));
+  else if constexpr (O == 8)
+    asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_1 src1_sel:DWORD"
+        : "=v"(inc) : "v"(hs), "v"(one));
+  else if constexpr (O == 16)
+    asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_2 src1_sel:DWORD"
+        : "=v"(inc) : "v"(hs), "v"(one));
+  else
+    asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3 src1_sel:DWORD"
+        : "=v"(inc) : "v"(hs), "v"(one));
+  if (on) atomicAdd(&h[word], inc);  // 1 or 1 << 16
 }
 __device__ __forceinline__ void hist_add8_packed(uint32_t *h, const Group &g, uint32_t valid) {
-  hist_add_packed<0>(h, g.sym[0], 0 < valid);
-  hist_add_packed<8>(h, g.sym[0], 1 < valid);
-  hist_add_packed<16>(h, g.sym[0], 2 < valid);
-  hist_add_packed<24>(h, g.sym[0], 3 < valid);
-  hist_add_packed<0>(h, g.sym[1], 4 < valid);
-  hist_add_packed<8>(h, g.sym[1], 5 < valid);
-  hist_add_packed<16>(h, g.sym[1], 6 < valid);
-  hist_add_packed<24>(h, g.sym[1], 7 < valid);
+  const uint32_t hs0 = (g.sym[0] >> 3) & 0x10101010u, hs1 = (g.sym[1] >> 3) & 0x10101010u;
+  uint32_t one = 1;
+  asm volatile("" : "+v"(one));
+  hist_add_packed<0>(h, g.sym[0], hs0, one, 0 < valid);
+  hist_add_packed<8>(h, g.sym[0], hs0, one, 1 < valid);
+  hist_add_packed<16>(h, g.sym[0], hs0, one, 2 < valid);
+  hist_add_packed<24>(h, g.sym[0], hs0, one, 3 < valid);
+  hist_add_packed<0>(h, g.sym[1], hs1, one, 4 < valid);
+  hist_add_packed<8>(h, g.sym[1], hs1, one, 5 < valid);
+  hist_add_packed<16>(h, g.sym[1], hs1, one, 6 < valid);
+  hist_add_packed<24>(h, g.sym[1], hs1, one, 7 < valid);
 }
 
 // 16 image bytes from LDS: unit u of the image at byte offset sh of s32
@@ -1101,7 +1144,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
   constexpr int D = (E == 2) ? (SHARED ? 8 : 16) : 4;
   extern __shared__ __align__(16) uint8_t smem_base[];
   uint8_t *smem = smem_base + kTrashBytes;  // [trash | encoder table | histogram / staging]
-  uint4 *enc = (uint4 *)smem;
+  uint4 *enc = (uint4 *)smem;  // at LDS byte kTrashBytes: the kernel has no static LDS (the host checks)
   uint32_t *hist = (uint32_t *)(smem + kEncTableBytes);
   uint8_t *stage = smem + a.pass2_off;
   uint16_t *stage16 = (uint16_t *)(stage + kStageHead);
@@ -1406,9 +1449,13 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
       }
       const uint32_t sy[2] = {s0, s1};
       uint4 e[8];
+      if constexpr (SMALL) {  // (the large blocks' loops spill more with the fixed-address form)
+        enc_lookup8_at<kTrashBytes>(sy[0], sy[1], e);
+      } else {
 #pragma unroll
-      for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(sy, tt)];
-      enc_round<false>(x, e, valid, pos, lds_rel, trash);
+        for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(sy, tt)];
+      }
+      enc_round<false, SMALL>(x, e, valid, pos, lds_rel, trash);
       if (a.wcap - pos >= limit_words) stored = true;
     }
     if constexpr (SMALL) {
@@ -1426,11 +1473,8 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
             }
             const uint32_t s0 = S.v3[2 * rr], s1 = S.v3[2 * rr + 1];
             uint4 e[8];
-#pragma unroll
-            for (int tt = 0; tt < 4; ++tt) e[tt] = enc[(s0 >> (8 * tt)) & 0xFFu];
-#pragma unroll
-            for (int tt = 0; tt < 4; ++tt) e[4 + tt] = enc[(s1 >> (8 * tt)) & 0xFFu];
-            enc_round<true>(x, e, 8, pos, lds_rel, trash);
+            enc_lookup8_at<kTrashBytes>(s0, s1, e);
+            enc_round<true, true>(x, e, 8, pos, lds_rel, trash);
             if (a.wcap - pos >= limit_words) stored = true;
           }
         }
@@ -1459,10 +1503,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
               }
               const uint32_t s0 = S.v3[2 * rr], s1 = S.v3[2 * rr + 1];
               uint4 e[8];
-#pragma unroll
-              for (int tt = 0; tt < 4; ++tt) e[tt] = enc[(s0 >> (8 * tt)) & 0xFFu];
-#pragma unroll
-              for (int tt = 0; tt < 4; ++tt) e[4 + tt] = enc[(s1 >> (8 * tt)) & 0xFFu];
+              enc_lookup8(enc, s0, s1, e);
               enc_round<true>(x, e, 8, pos, lds_rel, trash);
               if (a.wcap - pos >= limit_words) stored = true;
             }
@@ -1495,8 +1536,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
             const int rn = r - P;
             load_round<E, true>(src_blk + (uint64_t)(rn >= 0 ? rn : 0) * kRound * E, pb[u]);
             uint4 e[8];
-#pragma unroll
-            for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
+            enc_lookup8(enc, gr.sym[0], gr.sym[1], e);
             enc_round<true>(x, e, 8, pos, lds_rel, trash);
             if (a.wcap - pos >= limit_words) stored = true;
           }
@@ -1521,8 +1561,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         Group gr;
         split_group<DT>(wa, gr);
         uint4 e[8];
-#pragma unroll
-        for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
+        enc_lookup8(enc, gr.sym[0], gr.sym[1], e);
         enc_round<true>(x, e, 8, pos, lds_rel, trash);
         if (a.wcap - pos >= limit_words) stored = true;
         if (stored) break;
@@ -1536,8 +1575,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         const uint32_t rn = r >= 2 ? (uint32_t)(r - 2) : 0u;
         load_round<E>(src_blk + (uint64_t)rn * kRound * E, wa);
         split_group<DT>(wbuf, gr);
-#pragma unroll
-        for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
+        enc_lookup8(enc, gr.sym[0], gr.sym[1], e);
         enc_round<true>(x, e, 8, pos, lds_rel, trash);
         if (a.wcap - pos >= limit_words) stored = true;
       }
@@ -1552,8 +1590,7 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
         Group gr;
         split_group<DT>(wa, gr);
         uint4 e[8];
-#pragma unroll
-        for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(gr.sym, tt)];
+        enc_lookup8(enc, gr.sym[0], gr.sym[1], e);
         enc_round<true>(x, e, 8, pos, lds_rel, trash);
         if (a.wcap - pos >= limit_words) stored = true;
       }
@@ -2603,18 +2640,14 @@ __global__ void __launch_bounds__(64 * (kReduceGroup + 1)) reduce_fused_kernel(R
     const uint2 sv = *(const uint2 *)(syms + full * kRound + kPerLane * lane);
     const uint32_t sy[2] = {sv.x, sv.y};
     uint4 e[8];
-#pragma unroll
-    for (int tt = 0; tt < 8; ++tt) e[tt] = enc[sym_at(sy, tt)];
+    enc_lookup8(enc, sy[0], sy[1], e);
     enc_round<false>(xs, e, valid, pos, lds_rel, trash);
     if (a.wcap - pos >= limit_words) stored = true;
   }
   for (int q2 = (int)full - 1; q2 >= 0 && !stored; --q2) {
     const uint2 sv = *(const uint2 *)(syms + (uint32_t)q2 * kRound + kPerLane * lane);
     uint4 e[8];
-#pragma unroll
-    for (int tt = 0; tt < 4; ++tt) e[tt] = enc[(sv.x >> (8 * tt)) & 0xFFu];
-#pragma unroll
-    for (int tt = 0; tt < 4; ++tt) e[4 + tt] = enc[(sv.y >> (8 * tt)) & 0xFFu];
+    enc_lookup8(enc, sv.x, sv.y, e);
     enc_round<true>(xs, e, 8, pos, lds_rel, trash);
     if (a.wcap - pos >= limit_words) stored = true;
   }
@@ -2902,6 +2935,9 @@ struct DeviceInfo {
   int cus = 0;
   bool gfx950 = false;
   uint8_t *scratch = nullptr;  // this device's copy of `scratch` (uzip_compress_noalloc)
+  // the encoder kernels have no static LDS, so their dynamic LDS (and the
+  // encoder table they read at a fixed LDS address) starts at address 0
+  bool enc_lds_at0 = false;
 };
 
 // fault injection (uzip_inject_scan_stall)
@@ -2934,6 +2970,15 @@ uzip_status device_info(DeviceInfo &out) {
       (void)hipFuncSetAttribute(shared_kernel_ptr(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
     for (int k = 0; k < 3; ++k)
       (void)hipFuncSetAttribute(reduce_kernel_ptr(k), hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
+    bool at0 = true;
+    auto no_static_lds = [](const void *f) {
+      hipFuncAttributes fa;
+      return hipFuncGetAttributes(&fa, f) == hipSuccess && fa.sharedSizeBytes == 0;
+    };
+    for (int k = 0; k < kEncodeKernels; ++k) at0 = at0 && no_static_lds(encode_kernel_ptr(k));
+    for (int k = 0; k < kSharedKernels; ++k) at0 = at0 && no_static_lds(shared_kernel_ptr(k));
+    for (int k = 0; k < 3; ++k) at0 = at0 && no_static_lds(reduce_kernel_ptr(k));
+    g_info[dev].enc_lds_at0 = at0;
     (void)hipFuncSetAttribute((const void *)reduce_decode_kernel<0>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
     (void)hipFuncSetAttribute((const void *)reduce_decode_kernel<1>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
     (void)hipFuncSetAttribute((const void *)reduce_decode_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize, lds_max);
@@ -3108,6 +3153,7 @@ uzip_status launch_table_split(const void *d_in, uint64_t n, uzip_dtype dt, uint
 uzip_status launch_encode(EncodeArgs &a, uzip_dtype dt, bool reduce, uint8_t *ws, const EncodeWs &w,
                           const DeviceInfo &info, hipStream_t stream, bool shared = false,
                           uint32_t *dstatus = nullptr) {
+  if (!info.enc_lds_at0) return UZIP_EHIP;
   const bool small = !reduce && small_path(a.block_elems);
   a.ticket = (uint32_t *)ws;  // the kWs* words, then the look-back status
   a.status = (uint64_t *)(ws + w.status_off);

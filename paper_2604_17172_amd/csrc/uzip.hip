@@ -1235,7 +1235,11 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
     const uint64_t blk0 = (uint64_t)lb * a.block_elems;  // chunk-relative
     const uint32_t n_b = (uint32_t)((chunk_n - blk0) < a.block_elems ? (chunk_n - blk0) : a.block_elems);
     const uint32_t rounds = (n_b + kRound - 1) / kRound;
-    const uint32_t full = n_b / kRound;
+    uint32_t full = n_b / kRound;
+    // small blocks: an opaque scalar, or the compiler folds the prefetch
+    // clamps (r + D < full) back into 64-bit vector compares on n (the
+    // large blocks' loops come out slower with it)
+    if constexpr (SMALL) asm volatile("" : "+s"(full));
     const bool last_in_chunk = (lb + 1 == g.n_blocks);
     const uint8_t *src = REDUCE ? a.ybuf : a.in + chunk_first * E;  // pass-2 source (large blocks)
     uint8_t *raw_plane = sout + g.raw_off;
@@ -1302,7 +1306,14 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
 #pragma unroll
               for (int q = 0; q < NW; ++q) w[q] = buf[rr % D][q];
               const uint32_t rn = (r + D < full) ? r + D : full - 1;
-              load_round<E, SMALL>(src_blk + (uint64_t)rn * kRound * E, buf[rr % D]);
+              // the round's address as a scalar base plus the lane's offset
+              // (scalar-base loads and stores; the compiler would otherwise
+              // keep a per-lane 64-bit pointer and add each round's offset
+              // to it with vector adds)
+              const __attribute__((address_space(1))) uint8_t *rsrc =
+                  (const __attribute__((address_space(1))) uint8_t *)(src_blk + (uint64_t)rn * kRound * E);
+              asm("" : "+s"(rsrc));
+              load_round<E, SMALL>((const uint8_t *)rsrc, buf[rr % D]);
               Group gr;
               split_group<DT>(w, gr);
               // the compiler would otherwise carry the split words (four;
@@ -1314,7 +1325,10 @@ __device__ __forceinline__ void encode_body(const EncodeArgs &a) {
               S.v3[2 * rr] = gr.sym[0];
               S.v3[2 * rr + 1] = gr.sym[1];
               if (r < full) {
-                store_raw_round<E, SYS>(raw_blk + (uint64_t)r * kRound * (E - 1), gr);
+                __attribute__((address_space(1))) uint8_t *rdst =
+                    (__attribute__((address_space(1))) uint8_t *)(raw_blk + (uint64_t)r * kRound * (E - 1));
+                asm("" : "+s"(rdst));
+                store_raw_round<E, SYS>((uint8_t *)rdst, gr);
                 if constexpr (!SHARED) hist_upd(gr, 8);
               }
             }

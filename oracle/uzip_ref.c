@@ -281,7 +281,7 @@ int64_t ref_rans_decode(const uint32_t *state_in, const uint16_t *words,
 /* Stream layout helpers                                               */
 /* ------------------------------------------------------------------ */
 static int valid_block_bytes(uint32_t block_bytes) {
-  if (block_bytes < 4096u || block_bytes > 262144u) return 0;
+  if (block_bytes < 4096u || block_bytes > 4194304u) return 0;
   return (block_bytes & (block_bytes - 1u)) == 0;
 }
 

@@ -265,6 +265,29 @@ def test_single_symbol_block_closed_form():
     assert np.all(sec[290:] == 0)
 
 
+def test_largest_block_closed_forms():
+    """A 4 MiB block holds 2^21 16-bit symbols, the most of any block.  One
+    symbol throughout: f = M, no words, a 304-byte section.  With one
+    outlier the counts are 2^21 - 1 and 1: f = 1 + floor((2^21 - 1)(M - 2)
+    / 2^21) = 2046 and 1 + floor((M - 2) / 2^21) = 1, and the remainder 1
+    goes to the most frequent symbol: (2047, 1) -- c (M - k) at its
+    largest, just under 2^32."""
+    n = 1 << 21
+    x = np.full(n, 0x3F80, np.uint16)          # bf16 1.0: symbol (exponent) 127
+    sec, stored = ref.block_section(x, "bf16", 1 << 22, 0)
+    assert not stored and len(sec) == 304
+    assert np.all(np.frombuffer(sec[:256].tobytes(), np.uint32) == L_STATE)
+    assert np.frombuffer(sec[288:290].tobytes(), np.uint16)[0] == M
+    x[12345] = 0x4000                          # bf16 2.0: symbol 128
+    sec, stored = ref.block_section(x, "bf16", 1 << 22, 0)
+    assert not stored
+    present = np.unpackbits(sec[256:288], bitorder="little")
+    assert list(np.flatnonzero(present)) == [127, 128]
+    assert list(np.frombuffer(sec[288:292].tobytes(), np.uint16)) == [2047, 1]
+    s = ref.compress(x, "bf16", 1 << 22)
+    assert np.array_equal(ref.decompress(s, "bf16", n), x)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "fp16", "fp32"])
 def test_stored_coded_boundary_closed_form(dtype):
     """One symbol, no words: the coded section would be 288 + 2 = 290 bytes,
@@ -340,7 +363,9 @@ def test_ratio_bf16_uniform_matches_paper():
 def test_ratio_bounded_by_exponent_entropy():
     for x, dtype, bb in [(W.normal_bf16(1 << 20, seed=2), "bf16", 65536),
                          (W.grad_fp32(1 << 19, seed=3), "fp32", 262144),
-                         (W.grad_fp16(1 << 19, seed=3), "fp16", 262144)]:
+                         (W.grad_fp16(1 << 19, seed=3), "fp16", 262144),
+                         (W.normal_bf16(5 << 20, seed=4), "bf16", 1 << 22),
+                         (W.grad_fp32((1 << 20) + 4321, seed=5), "fp32", 1 << 20)]:
         e = EB[dtype]
         n = x.size
         be = bb // e
@@ -461,6 +486,18 @@ def test_roundtrip_lossless(dtype, n):
     x = _special_words(dtype, n, seed=n)
     for bb in (4096, 65536):
         s = ref.compress(x, dtype, bb)
+        y = ref.decompress(s, dtype, n)
+        assert y is not None and np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16", "fp32", "e4m3fn"])
+def test_roundtrip_lossless_large_blocks(dtype):
+    """1 MiB and 4 MiB blocks with a partial last block."""
+    n = (1 << 21) + 3 * (1 << 18) + 777
+    x = _special_words(dtype, n, seed=5)
+    for bb in (1 << 20, 1 << 22):
+        s = ref.compress(x, dtype, bb)
+        assert len(s) <= ref.max_compressed_size(dtype, n, bb)
         y = ref.decompress(s, dtype, n)
         assert y is not None and np.array_equal(x, y)
 
@@ -611,6 +648,10 @@ def test_c_oracle_matches_python_model():
         b = model.compress([int(v) for v in x], dtype, 4096)
         assert a == b, (trial, n, dtype)
         assert model.decompress(b, dtype, n) == [int(v) for v in x]
+    # one 1 MiB block and part of a second: the model's arithmetic at a
+    # block size past the register path's
+    x = W.grad_fp32((1 << 18) + 777, seed=8)
+    assert ref.compress(x, "fp32", 1 << 20).tobytes() == model.compress([int(v) for v in x], "fp32", 1 << 20)
 
 
 # ------------------------------------------------------ golden fixtures

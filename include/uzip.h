@@ -43,7 +43,7 @@
  *     the given stream; it returns before the GPU has run.  Results (and
  *     *d_status) are valid once the stream reaches that point.
  *   - Device pointers must be 16-byte aligned.
- *   - block_bytes is a power of two in [4096, 262144].
+ *   - block_bytes is a power of two in [4096, 4194304] (4 KiB to 4 MiB).
  *   - n_elems <= 2^48 (else EINVAL; the size queries return 0).
  *   - Calls that overlap in time need separate workspaces.
  *   - Host-side errors are returned immediately and nothing is enqueued.
@@ -134,7 +134,10 @@ size_t uzip_max_compressed_size(uzip_dtype dtype, uint64_t n_elems, uint32_t blo
  * chunk size in `aux`; for UZIP_OP_REDUCE pass n_in in `aux` and add the
  * flag UZIP_WS_NO_OUT_RAW (1 << 16) when d_out_raw will be NULL.  Returns
  * 0 for invalid arguments (a zero-byte workspace is never valid for
- * COMPRESS, CHUNKED or REDUCE). */
+ * COMPRESS, CHUNKED or REDUCE).  Blocks of more than 7424 words' worth of
+ * coded output need an overflow slot of about block_bytes / E bytes for each
+ * of up to 2048 workgroups (min(blocks, 2048) slots): e.g. 1 GiB of bf16 in
+ * 4 MiB blocks, 256 slots of 2 MiB. */
 #define UZIP_WS_NO_OUT_RAW (1u << 16)
 size_t uzip_workspace_size(int op, uzip_dtype dtype, uint64_t n_elems, uint32_t block_bytes,
                            uint64_t aux);

@@ -58,7 +58,7 @@ namespace {
 
 constexpr int kMaxInputs = 16;
 constexpr uint32_t kTrashBytes = 256;  // encoder: slots for non-emitted words (2 bytes per lane), free outside coding
-constexpr uint32_t kMinBlockBytes = 4096, kMaxBlockBytes = 262144;
+constexpr uint32_t kMinBlockBytes = 4096, kMaxBlockBytes = 4194304;
 
 struct EncodeArgs {
   const uint8_t *in;        // elements to compress (compress modes)
@@ -445,8 +445,9 @@ __device__ void build_enc_table(const uint32_t *hist, uint32_t n_b, uint4 *enc, 
   uint32_t pres = (c[0] > 0) + (c[1] > 0) + (c[2] > 0) + (c[3] > 0);
   uint32_t k = wave_sum(pres);
   uint32_t lt = 0;
-  // c (M - k) < 2^17 * 2^11: the quotient is exact in 32 bits; every block
-  // but a stream's last has a power-of-two size, a shift
+  // c (M - k) <= 2^21 (2^11 - 1) < 2^32 (a block holds at most 2^21
+  // symbols): exact in 32 bits; every block but a stream's last has a
+  // power-of-two size, a shift
   const bool pow2 = (n_b & (n_b - 1)) == 0;
   const uint32_t lg = 31 - __clz(n_b);
 #pragma unroll

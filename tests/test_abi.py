@@ -26,7 +26,7 @@ def test_library_exports_every_declared_symbol():
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp16", "fp32", "e4m3fn", "e5m2"])
-@pytest.mark.parametrize("bb", [4096, 65536, 262144])
+@pytest.mark.parametrize("bb", [4096, 65536, 262144, 1 << 20, 1 << 22])
 def test_max_size_matches_oracle(dtype, bb):
     import paper_2604_17172_amd as uz
     for n in (0, 1, 511, 4097, 1 << 20, (1 << 20) + 7, 1 << 29):
@@ -38,7 +38,9 @@ def test_invalid_arguments_rejected_on_host():
     assert uz.uzip_max_compressed_size(7, 100, 65536) == 0
     assert uz.uzip_max_compressed_size(0, 100, 65535) == 0
     assert uz.uzip_max_compressed_size(0, 100, 2048) == 0
-    assert uz.uzip_max_compressed_size(0, 100, 524288) == 0
+    assert uz.uzip_max_compressed_size(0, 100, 1 << 23) == 0      # above 4 MiB
+    assert uz.uzip_max_compressed_size(0, 100, 3 << 20) == 0      # not a power of two
+    assert uz.uzip_max_compressed_size(0, 100, 1 << 22) > 0
     assert uz.uzip_compress(None, 10, 7, 65536, None, 0, None, None, 0, None) == uz.EINVAL
     assert uz.uzip_compress(None, 10, 0, 65535, None, 0, None, None, 0, None) == uz.EINVAL
     # misaligned pointers

@@ -70,7 +70,8 @@ def oracle_slots(streams, slot):
                                            ("fp32", 262144, 1 << 20, 2 * (1 << 18) + 1),
                                            ("fp16", 4096, 16384, 100_000),
                                            ("e4m3fn", 4096, 16384, 70_001),
-                                           ("bf16", 65536, 65536, 5 * 32768)])
+                                           ("bf16", 65536, 65536, 5 * 32768),
+                                           ("bf16", 1 << 22, 1 << 22, 3 * (1 << 21) + 99)])
 def test_all_chunks_in_one_launch(uz, dtype, bb, cb, n):
     say(f"[chunk-decode] dtype={dtype} n={n} block={bb} chunk={cb}")
     x = data(dtype, n, seed=61)

@@ -117,6 +117,26 @@ def test_grad_and_large_blocks(uz, dtype, bb):
     check_roundtrip(uz, x, dtype, bb, f"grad {dtype}")
 
 
+# 1 MiB and 4 MiB blocks (up to 2^21 symbols a block): the large-block
+# encoder's window slides into much bigger overflow slots
+@pytest.mark.parametrize("dtype,bb", [("bf16", 1 << 22), ("fp16", 1 << 22), ("fp32", 1 << 22),
+                                      ("bf16", 1 << 20), ("fp32", 1 << 20), ("e4m3fn", 1 << 22)])
+def test_largest_blocks(uz, dtype, bb):
+    n = 3 * (bb // EB[dtype]) + 12345
+    x = {"fp32": lambda: W.grad_fp32(n, seed=4), "fp16": lambda: W.grad_fp16(n, seed=4),
+         "bf16": lambda: W.normal_bf16(n, seed=4),
+         "e4m3fn": lambda: W.normal_fp8_pairs(n, "e4m3fn", sigma=1.0, seed=4)}[dtype]()
+    check_roundtrip(uz, x, dtype, bb, f"{bb >> 20} MiB blocks {dtype}")
+
+
+def test_largest_block_closed_form(uz):
+    """A 4 MiB bf16 block of one symbol with one outlier: counts 2^21 - 1
+    and 1, table (2047, 1) -- c (M - k) at its largest."""
+    x = np.full(1 << 21, 0x3F80, np.uint16)
+    x[12345] = 0x4000
+    check_roundtrip(uz, x, "bf16", 1 << 22, "4 MiB block, one outlier")
+
+
 def test_weight_sync_prefix(uz):
     x = W.weight_sync(1 << 23)   # embedding + first layers: N(0,1), N(0,0.02), N(1,0.05) regions
     check_roundtrip(uz, x, "bf16", 65536, "weight_sync prefix")
@@ -260,7 +280,9 @@ def test_fp8_stream_dtype_must_match(uz):
                                            ("fp16", 4096, 16384, 70 * 8192 + 1234),
                                            ("fp32", 16384, 65536, 66 * 16384 + 5),
                                            ("bf16", 4096, 131072, 8 * 65536),
-                                           ("fp16", 4096, 65536, 24 * 32768 - 100)])
+                                           ("fp16", 4096, 65536, 24 * 32768 - 100),
+                                           ("bf16", 1 << 22, 1 << 22, 3 * (1 << 21) + 99),
+                                           ("fp32", 1 << 20, 1 << 22, 2 * (1 << 20) + 5)])
 def test_chunked_producer_matches_per_chunk_oracle(uz, dtype, bb, cb, n):
     say(f"[parity] chunked dtype={dtype} n={n} block={bb} chunk={cb}")
     x = special_words(dtype, n, seed=31)
@@ -321,6 +343,22 @@ def test_reduce_matches_oracle(uz, dtype, n_in):
             assert np.array_equal(got, want_s), (use_local, want_raw)
             if want_raw:
                 assert np.array_equal(host_bits(raw, dtype), want_y)
+
+
+@pytest.mark.parametrize("dtype,bb", [("bf16", 1 << 20), ("fp32", 1 << 22)])
+def test_reduce_largest_blocks(uz, dtype, bb):
+    """Blocks of 1 MiB and 4 MiB: the decode-reduce kernel and the separate
+    coding pass (such a block's words do not fit the fused kernel's LDS)."""
+    n = 2 * (bb // EB[dtype]) + 999
+    say(f"[parity] reduce dtype={dtype} n={n} block={bb}")
+    xs = [special_words(dtype, n, seed=300 + i) for i in range(3)]
+    streams = [ref.compress(v, dtype, bb) for v in xs]
+    out, size, raw, status = uz.reduce_fused([dev(v) for v in streams], dtype, n, bb, want_raw=True)
+    torch.cuda.synchronize()
+    want_s, want_y = ref.reduce(streams, dtype, n, bb)
+    assert int(status.item()) == 0
+    assert np.array_equal(out[:int(size.item())].cpu().numpy(), want_s)
+    assert np.array_equal(host_bits(raw, dtype), want_y)
 
 
 @pytest.mark.parametrize("dtype,bb", [("bf16", 16384), ("bf16", 4096), ("fp16", 8192), ("fp32", 16384)])

@@ -84,7 +84,7 @@ def test_edge_sizes(uz, dtype, n):
 
 
 @pytest.mark.parametrize("dtype,bb", [("bf16", 65536), ("bf16", 262144), ("fp32", 262144), ("fp16", 262144),
-                                      ("e4m3fn", 65536), ("fp32", 65536)])
+                                      ("e4m3fn", 65536), ("fp32", 65536), ("bf16", 1 << 22)])
 def test_multi_block_streams(uz, dtype, bb):
     n = 5 * (bb // EB[dtype]) + 4321
     check(uz, data(dtype, n, seed=7), dtype, bb, "sampled", "multi-block")

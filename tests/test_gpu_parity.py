@@ -137,6 +137,44 @@ def test_largest_block_closed_form(uz):
     check_roundtrip(uz, x, "bf16", 1 << 22, "4 MiB block, one outlier")
 
 
+def test_concurrent_calls_on_two_streams(uz):
+    """Two compress calls in flight at once on two streams, each with its
+    own workspace (calls are re-entrant; a wave only waits on blocks of its
+    own call, whose tickets running waves hold), then two decompress calls
+    the same way: both equal the oracle's streams and decode back."""
+    say("[parity] two streams at once")
+    cases = [(W.normal_bf16(1 << 22, seed=61), "bf16", 65536), (W.grad_fp32(1 << 21, seed=62), "fp32", 262144)]
+    xts, outs, wss, sizes = [], [], [], []
+    for x, d, bb in cases:
+        dt = uz.dtype_code(d)
+        xts.append(to_dev_bits(x, d))
+        outs.append(torch.empty(uz.uzip_max_compressed_size(dt, x.size, bb), dtype=torch.uint8, device="cuda"))
+        wss.append(torch.empty(uz.uzip_workspace_size(uz.OP_COMPRESS, dt, x.size, bb), dtype=torch.uint8,
+                               device="cuda"))
+        sizes.append(torch.zeros(1, dtype=torch.int64, device="cuda"))
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for k, (x, d, bb) in enumerate(cases):
+        uz.compress(xts[k], bb, dtype=d, out=outs[k], ws=wss[k], size=sizes[k], stream=streams[k])
+    torch.cuda.synchronize()
+    ys, sts = [], []
+    for k, (x, d, bb) in enumerate(cases):
+        want = ref.compress(x, d, bb)
+        got = outs[k][:int(sizes[k].item())].cpu().numpy()
+        assert np.array_equal(got, want), d
+        ys.append(torch.empty_like(xts[k]))
+        sts.append(torch.zeros(1, dtype=torch.int32, device="cuda"))
+    dws = [torch.empty(uz.uzip_workspace_size(uz.OP_DECOMPRESS, uz.dtype_code(d), x.size, bb), dtype=torch.uint8,
+                       device="cuda") for x, d, bb in cases]
+    torch.cuda.synchronize()
+    for k, (x, d, bb) in enumerate(cases):
+        uz.decompress(outs[k], d, x.size, out=ys[k], ws=dws[k], status=sts[k], stream=streams[k])
+    torch.cuda.synchronize()
+    for k, (x, d, bb) in enumerate(cases):
+        assert int(sts[k].item()) == 0
+        assert np.array_equal(host_bits(ys[k], d), x), d
+
+
 def test_weight_sync_prefix(uz):
     x = W.weight_sync(1 << 23)   # embedding + first layers: N(0,1), N(0,0.02), N(1,0.05) regions
     check_roundtrip(uz, x, "bf16", 65536, "weight_sync prefix")

@@ -44,7 +44,8 @@ def case(seed):
     """(dtype, n, block_bytes, chunk_bytes, kind, data) of sweep case `seed`."""
     rng = np.random.default_rng(1000 + seed)
     dtype = DTYPES[seed % len(DTYPES)]
-    bb = int(2 ** rng.integers(12, 19))                 # 4 KiB .. 256 KiB
+    # 4 KiB .. 256 KiB; seeds from 30 on: 512 KiB .. 4 MiB
+    bb = int(2 ** (rng.integers(12, 19) if seed < 30 else rng.integers(19, 23)))
     chunk = bb * int(2 ** rng.integers(0, 4))           # 1 .. 8 blocks a chunk
     n = int(np.exp(rng.uniform(0, np.log(3_000_000))))  # 1 .. 3 M elements, log-uniform
     kind = ("normal", "wide", "bits", "mixed")[int(rng.integers(0, 4))]
@@ -68,7 +69,7 @@ def case(seed):
     return dtype, n, bb, chunk, kind, x
 
 
-@pytest.mark.parametrize("seed", range(30))
+@pytest.mark.parametrize("seed", range(40))
 def test_sweep_matches_oracle(uz, seed):
     dtype, n, bb, chunk, kind, x = case(seed)
     say(f"[sweep] seed={seed} dtype={dtype} n={n} block={bb} chunk={chunk} kind={kind}")
@@ -104,7 +105,7 @@ def reduce_case(seed):
     rng = np.random.default_rng(5000 + seed)
     dtype = ("bf16", "fp16", "fp32")[seed % 3]
     n_in = int(rng.integers(1, 17))
-    bb = int(2 ** rng.integers(12, 19))
+    bb = int(2 ** (rng.integers(12, 19) if seed < 15 else rng.integers(19, 23)))   # from seed 15: 512 KiB .. 4 MiB
     n = int(np.exp(rng.uniform(0, np.log(400_000))))
     gen = {"bf16": lambda k: W.normal_bf16(n, sigma=float(rng.choice([0.02, 1.0])), seed=k),
            "fp16": lambda k: W.grad_fp16(n, seed=k), "fp32": lambda k: W.grad_fp32(n, seed=k)}[dtype]
@@ -113,7 +114,7 @@ def reduce_case(seed):
     return dtype, n_in, n, bb, xs, local
 
 
-@pytest.mark.parametrize("seed", range(15))
+@pytest.mark.parametrize("seed", range(20))
 def test_reduce_sweep_matches_oracle(uz, seed):
     dtype, n_in, n, bb, xs, local = reduce_case(seed)
     say(f"[sweep] reduce seed={seed} dtype={dtype} n_in={n_in} n={n} block={bb} local={local is not None}")

@@ -45,6 +45,8 @@ def test_noalloc_matches_compress_on_consecutive_calls(uz):
         (W.grad_fp16(3 << 20), "fp16", uz.FP16, 262144, np.int16),
         # smaller still, fp32 with a ragged tail
         (W.grad_fp32(300_001), "fp32", uz.FP32, 65536, np.int32),
+        # 4 MiB blocks (2 MiB slots) and a partial last block
+        (W.normal_bf16((5 << 20) + 999, seed=3), "bf16", uz.BF16, 1 << 22, np.int16),
     ]
     for x, name, code, bb, bits in cases:
         say(f"[noalloc] {name} n={x.size} block={bb}")

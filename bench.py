@@ -414,6 +414,26 @@ def main() -> int:
             log(f"[bench] {name}: ratio {gtot / gb:.4f} compress {cm:.3f} ms decompress {dm:.3f} ms")
             del gt, go, gw, gy
 
+        # ------------- the 1 GiB weight buffer in 1 MiB and 4 MiB blocks -------------
+        # (few, long blocks: each is one wave's serial chain)
+        for lb in (1 << 20, 1 << 22):
+            lname = f"weight_sync_bf16_1GiB_{lb >> 20}MiB_blocks"
+            mark(lname)
+            lo = torch.empty(uz.uzip_max_compressed_size(uz.BF16, n, lb), dtype=torch.uint8, device=dev)
+            lw = torch.empty(uz.uzip_workspace_size(uz.OP_COMPRESS, uz.BF16, n, lb), dtype=torch.uint8, device=dev)
+            ly = torch.empty_like(x)
+            ltot = int(uz.compress(x, lb, dtype=uz.BF16, out=lo, ws=lw)[1].item())
+            lreps = max(2, reps // 2)
+            ct = timed(lambda: uz.compress(x, lb, dtype=uz.BF16, out=lo, ws=lw), lreps)
+            dt = timed(lambda: uz.decompress(lo, uz.BF16, n, out=ly, ws=dws), lreps)
+            assert torch.equal(x, ly)
+            cm, dm = float(np.mean(ct)), float(np.mean(dt))
+            extras[lname] = {"block_bytes": lb, "ratio": round(ltot / nbytes, 4),
+                             "compress_ms": round(cm, 4), "decompress_ms": round(dm, 4),
+                             "compress_frac": frac(nbytes + ltot, cm), "decompress_frac": frac(nbytes + ltot, dm)}
+            log(f"[bench] {lname}: ratio {ltot / nbytes:.4f} compress {cm:.3f} ms decompress {dm:.3f} ms")
+            del lo, lw, ly
+
         # ------------- 2 GiB bf16 KV cache, 1 MiB chunks -------------
         mark("kv_chunked")
         kh = W.kv_cache()
